@@ -1,0 +1,295 @@
+// Oracle for sparse convolution (SC) and valid sparse convolution (VSC).
+//
+// TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+// CPU statement of what the GPU path computes.  Only the test suite, the
+// smoke check and the benchmark's CPU-baseline leg load it.  It shares no
+// code, header, table or helper with the HIP library, and neither side
+// includes or links the other.
+//
+// What it follows (Graham & van der Maaten, "Submanifold Sparse
+// Convolutional Networks"):
+//   * state of a layer: a map (location -> row) and a feature matrix with one
+//     row per active site (Section 4, Implementation);
+//   * SC(m,n,f,s): an output site is active when any input site in its f^d
+//     receptive field is active; the output extent is (l - f + s)/s; the
+//     ground state is replaced by zero (Section 3);
+//   * VSC(m,n,f,1): input padded by (f-1)/2, output active iff the central
+//     input site is active, features computed as for SC (Section 3);
+//   * rule book R = (R_i), R_i a list of (input row, output row) pairs per
+//     filter offset i (Section 4);
+//   * forward: output matrix starts at zero; for every pair of R_i add the
+//     input row times W^i to the output row (Section 4).
+//
+// Readings where the paper is silent (each one is listed in the design notes):
+//   * coordinate 0 is the sample index, with f[0] = s[0] = 1, so samples never
+//     interact;
+//   * SC takes any f >= 1, s >= 1 with no padding: extent floor((l-f)/s)+1;
+//   * W^i multiplies the input at s*y + i (SC) or y + i - (f-1)/2 (VSC): a
+//     cross-correlation, offsets flattened row-major (last dimension fastest);
+//   * SC output rows are numbered in lexicographic order of the output site;
+//   * pairs inside R_i are ordered by output row;
+//   * the bias (optional) is added once at every active output site;
+//   * accumulation is in double, rounded once to the output type (RNE).
+#include <array>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <set>
+#include <vector>
+
+namespace {
+
+enum { OK = 0, EINVAL_ = -1, EDUP_ = -2, ERANGE_ = -3 };
+enum { VSC = 0, SC = 1 };
+enum { F32 = 0, BF16 = 1 };
+
+using Site = std::array<int32_t, 4>;   // unused trailing entries are 0
+
+struct Rulebook {
+  int kind = 0, D = 0;
+  int64_t n_in = 0, n_out = 0, K = 0;
+  std::vector<int32_t> f, s, in_size, out_size;
+  std::vector<int32_t> out_coords;                       // [n_out][D]
+  std::vector<std::vector<std::array<int64_t, 2>>> R;    // R[i] = (in, out)
+};
+
+double bf16_to_double(uint16_t b) {
+  uint32_t u = static_cast<uint32_t>(b) << 16;
+  float v;
+  std::memcpy(&v, &u, 4);
+  return static_cast<double>(v);
+}
+
+double load(int dt, const void* p, int64_t idx) {
+  if (dt == F32) return static_cast<double>(static_cast<const float*>(p)[idx]);
+  return bf16_to_double(static_cast<const uint16_t*>(p)[idx]);
+}
+
+// Offset index i (flattened, last dimension fastest) -> per-dimension offset.
+void unflatten(int64_t i, int D, const std::vector<int32_t>& f, int32_t* o) {
+  for (int j = D - 1; j >= 0; --j) {
+    o[j] = static_cast<int32_t>(i % f[j]);
+    i /= f[j];
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Build the rule book of a VSC (kind 0) or SC (kind 1) layer.
+//   coords  host int32 [N][D], coordinate 0 = sample index
+//   size    host int32 [D], grid extent per dimension (size[0] = sample count)
+//   f, s    host int32 [D], filter size and stride, f[0] = s[0] = 1
+// Returns 0 and a handle in *out, or a negative status (EINVAL -1, EDUP -2,
+// ERANGE -3) with *out = NULL.
+int ref_build(int kind, int D, const int32_t* coords, int64_t N,
+              const int32_t* size, const int32_t* f, const int32_t* s,
+              void** out) {
+  *out = nullptr;
+  if (kind != VSC && kind != SC) return EINVAL_;
+  if (D < 2 || D > 4 || N < 0 || (N > 0 && !coords)) return EINVAL_;
+  if (!size || !f || !s) return EINVAL_;
+  if (f[0] != 1 || s[0] != 1) return EINVAL_;
+  for (int j = 0; j < D; ++j) {
+    if (size[j] < 1 || size[j] > 65535 || f[j] < 1 || s[j] < 1) return EINVAL_;
+    if (kind == VSC && (f[j] % 2 != 1 || s[j] != 1)) return EINVAL_;
+  }
+
+  auto* rb = new Rulebook;
+  rb->kind = kind;
+  rb->D = D;
+  rb->n_in = N;
+  rb->f.assign(f, f + D);
+  rb->s.assign(s, s + D);
+  rb->in_size.assign(size, size + D);
+  rb->K = 1;
+  for (int j = 0; j < D; ++j) rb->K *= f[j];
+
+  // Range check of every row first, then the input map (location -> row);
+  // a location given twice is an error, never merged.
+  for (int64_t r = 0; r < N; ++r)
+    for (int j = 0; j < D; ++j)
+      if (coords[r * D + j] < 0 || coords[r * D + j] >= size[j]) {
+        delete rb;
+        return ERANGE_;
+      }
+  std::map<Site, int64_t> in_map;
+  for (int64_t r = 0; r < N; ++r) {
+    Site x{0, 0, 0, 0};
+    for (int j = 0; j < D; ++j) x[j] = coords[r * D + j];
+    if (!in_map.emplace(x, r).second) {
+      delete rb;
+      return EDUP_;
+    }
+  }
+
+  // Output sites, in output-row order.
+  std::vector<Site> out_sites;
+  if (kind == VSC) {
+    rb->out_size = rb->in_size;
+    out_sites.resize(N);
+    for (int64_t r = 0; r < N; ++r) {
+      Site x{0, 0, 0, 0};
+      for (int j = 0; j < D; ++j) x[j] = coords[r * D + j];
+      out_sites[r] = x;        // output row r is input row r
+    }
+  } else {
+    rb->out_size.resize(D);
+    for (int j = 0; j < D; ++j)
+      rb->out_size[j] = size[j] >= f[j] ? (size[j] - f[j]) / s[j] + 1 : 0;
+    // y is active when some active input x = s*y + i with 0 <= i < f exists,
+    // i.e. t = x - i is a non-negative multiple of s inside the output grid.
+    std::set<Site> ys;
+    std::vector<int32_t> o(D);
+    for (const auto& kv : in_map) {
+      for (int64_t i = 0; i < rb->K; ++i) {
+        unflatten(i, D, rb->f, o.data());
+        Site y{0, 0, 0, 0};
+        bool ok = true;
+        for (int j = 0; j < D && ok; ++j) {
+          int32_t t = kv.first[j] - o[j];
+          if (t < 0 || t % s[j] != 0 || t / s[j] >= rb->out_size[j]) ok = false;
+          else y[j] = t / s[j];
+        }
+        if (ok) ys.insert(y);
+      }
+    }
+    out_sites.assign(ys.begin(), ys.end());   // lexicographic order
+  }
+  rb->n_out = static_cast<int64_t>(out_sites.size());
+  rb->out_coords.resize(rb->n_out * D);
+  for (int64_t r = 0; r < rb->n_out; ++r)
+    for (int j = 0; j < D; ++j) rb->out_coords[r * D + j] = out_sites[r][j];
+
+  // Rule book: for every offset i and output row y (ascending), the input
+  // site feeding y through W^i, if active.
+  rb->R.resize(rb->K);
+  std::vector<int32_t> o(D);
+  for (int64_t i = 0; i < rb->K; ++i) {
+    unflatten(i, D, rb->f, o.data());
+    for (int64_t y = 0; y < rb->n_out; ++y) {
+      Site x{0, 0, 0, 0};
+      for (int j = 0; j < D; ++j) {
+        if (kind == VSC) x[j] = out_sites[y][j] + o[j] - (f[j] - 1) / 2;
+        else x[j] = s[j] * out_sites[y][j] + o[j];
+      }
+      auto it = in_map.find(x);
+      if (it != in_map.end()) rb->R[i].push_back({it->second, y});
+    }
+  }
+  *out = rb;
+  return OK;
+}
+
+// Sizes of a built rule book.  out_size: host int32 [D] or NULL;
+// pair_off: host int64 [K+1] (prefix sums of k_i) or NULL.
+int ref_query(void* h, int64_t* n_in, int64_t* n_out, int64_t* K,
+              int32_t* out_size, int64_t* pair_off) {
+  if (!h) return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (n_in) *n_in = rb->n_in;
+  if (n_out) *n_out = rb->n_out;
+  if (K) *K = rb->K;
+  if (out_size)
+    for (int j = 0; j < rb->D; ++j) out_size[j] = rb->out_size[j];
+  if (pair_off) {
+    pair_off[0] = 0;
+    for (int64_t i = 0; i < rb->K; ++i)
+      pair_off[i + 1] = pair_off[i] + static_cast<int64_t>(rb->R[i].size());
+  }
+  return OK;
+}
+
+// Output coordinates (host int32 [n_out][D]) and pairs (host int32 [sum k][2],
+// R_0 first, each R_i ordered by output row).  Either may be NULL.
+int ref_export(void* h, int32_t* out_coords, int32_t* pairs) {
+  if (!h) return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (out_coords)
+    for (size_t k = 0; k < rb->out_coords.size(); ++k)
+      out_coords[k] = rb->out_coords[k];
+  if (pairs) {
+    int64_t p = 0;
+    for (const auto& Ri : rb->R)
+      for (const auto& pr : Ri) {
+        pairs[2 * p] = static_cast<int32_t>(pr[0]);
+        pairs[2 * p + 1] = static_cast<int32_t>(pr[1]);
+        ++p;
+      }
+  }
+  return OK;
+}
+
+// Forward pass.  x: host [n_in][C_in] of in_dt (0 = fp32, 1 = bf16 bits);
+// w: host [K][C_in][C_out] of in_dt; bias: host fp32 [C_out] or NULL.
+// y: host double [n_out][C_out], the exact-as-double result.
+// absb: host double [n_out][C_out] or NULL: |bias| + sum |x||w|, the scale the
+// tolerance is measured against.  x_absb: host double [n_in][C_in] or NULL; if
+// given it replaces |x| in absb (bounds carried through a stack of layers).
+int ref_forward(void* h, int in_dt, const void* x, const void* w,
+                const float* bias, int C_in, int C_out, double* y,
+                double* absb, const double* x_absb) {
+  if (!h || C_in < 1 || C_out < 1 || (in_dt != F32 && in_dt != BF16))
+    return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  for (int64_t r = 0; r < rb->n_out; ++r)
+    for (int n = 0; n < C_out; ++n) {
+      double b = bias ? static_cast<double>(bias[n]) : 0.0;
+      y[r * C_out + n] = b;
+      if (absb) absb[r * C_out + n] = std::fabs(b);
+    }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i]) {
+      const int64_t xi = pr[0], yo = pr[1];
+      for (int c = 0; c < C_in; ++c) {
+        const double xv = load(in_dt, x, xi * C_in + c);
+        const double xa = x_absb ? x_absb[xi * C_in + c] : std::fabs(xv);
+        for (int n = 0; n < C_out; ++n) {
+          const double wv = load(in_dt, w, (i * C_in + c) * C_out + n);
+          y[yo * C_out + n] += xv * wv;
+          if (absb) absb[yo * C_out + n] += xa * std::fabs(wv);
+        }
+      }
+    }
+  return OK;
+}
+
+// Round doubles once to the output type: fp32 (out: float*) or bf16 (out:
+// uint16_t* bit patterns), both round-to-nearest-even.
+int ref_round(const double* v, int64_t n, int out_dt, void* out) {
+  if (out_dt == F32) {
+    for (int64_t k = 0; k < n; ++k)
+      static_cast<float*>(out)[k] = static_cast<float>(v[k]);
+    return OK;
+  }
+  if (out_dt != BF16) return EINVAL_;
+  for (int64_t k = 0; k < n; ++k) {
+    double d = v[k];
+    float r;
+    if (std::isnan(d)) {
+      r = std::nanf("");
+    } else if (d == 0.0 || std::isinf(d)) {
+      r = static_cast<float>(d);
+    } else {
+      // bf16 keeps 8 significant bits; below 2^-126 the quantum is 2^-133.
+      int e;
+      std::frexp(d, &e);                       // |d| = m 2^e, 0.5 <= m < 1
+      int qe = e - 8 < -133 ? -133 : e - 8;
+      double q = std::nearbyint(std::ldexp(d, -qe));   // ties to even
+      double rd = std::ldexp(q, qe);
+      const double bf16_max = 3.3895313892515355e38;  // (2^8 - 1) 2^120
+      if (std::fabs(rd) > bf16_max) rd = std::copysign(INFINITY, d);
+      r = static_cast<float>(rd);              // exact: rd is a bf16 value
+    }
+    uint32_t u;
+    std::memcpy(&u, &r, 4);
+    static_cast<uint16_t*>(out)[k] = static_cast<uint16_t>(u >> 16);
+  }
+  return OK;
+}
+
+void ref_free(void* h) { delete static_cast<Rulebook*>(h); }
+
+}  // extern "C"
