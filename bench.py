@@ -1,0 +1,214 @@
+"""Benchmark: one VSC layer (rule-book build + forward) on MI355X.
+
+Workload (default): 8 voxelised surfaces on a 128^3 grid, ~100k active sites
+each (~900k in total), VSC 3^3, 64 -> 64 planes, bf16 features and weights,
+fp32 accumulation, bf16 output, fp32 bias.  A step is one pass of the whole
+hot path on resident inputs: build the rule book (hash, neighbour probe,
+per-offset compaction) and run the forward multiply-add.
+
+Prints one JSON line:
+  value      active sites per second over whole steps (build + forward)
+  roofline   the forward kernel (the dominant one) against the bf16 dense
+             matrix-core peak, from HIP events around each forward launch
+  cpu_baseline  the oracle on one sample of the same workload, host cores
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAKS = {  # MI355X published dense peaks
+    "bf16": 2500.0,    # TFLOP/s
+    "f32": 157.3,      # TFLOP/s
+    "hbm": 8000.0,     # GB/s
+}
+
+
+def _args():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="surf128x8_vsc3_c64_bf16")
+    p.add_argument("--variant", default="matched", choices=["matched", "literal"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget-s", type=float, default=20.0)
+    return p.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("forward.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_1706_01307_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, or
+    None when absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, x_bits, w_bits, bias, budget_s):
+    """Oracle (std::map build + double forward) on one sample of the workload."""
+    import oracle
+    c = wl.coords
+    sample = c[c[:, 0] == 0]
+    n = len(sample)
+    rows = np.nonzero(wl.coords[:, 0] == 0)[0]
+    t0 = time.perf_counter()
+    rb = oracle.Rulebook(oracle.VSC, sample, wl.spatial_size, [1] + [3] * wl.d)
+    t1 = time.perf_counter()
+    rb.forward(x_bits[rows], w_bits, bias, in_dt=oracle.BF16 if wl.dtype == "bf16" else oracle.F32)
+    t2 = time.perf_counter()
+    return {"value": n / (t2 - t0), "unit": "active sites/s", "cores": 1, "kind": "oracle",
+            "sample": f"sample 0 of the batch: {n} sites, rule book {t1 - t0:.2f} s + "
+                      f"forward {t2 - t1:.2f} s, single thread"}
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    import paper_1706_01307_amd as spc
+    from paper_1706_01307_amd import _lib, inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    wl = inputs.make_workload(a.workload, variant=a.variant)
+    layer = wl.layers[0]
+    assert layer.kind == "vsc" and len(wl.layers) == 1, "bench times a single VSC layer"
+    N, D = len(wl.coords), wl.d + 1
+    K = layer.f ** wl.d
+    Cin, Cout = layer.c_in, layer.c_out
+    bf16 = wl.dtype == "bf16"
+
+    xf = inputs.normal_f32((N, Cin), seed=11)
+    wf = inputs.normal_f32((K, Cin, Cout), std=1.0 / np.sqrt(K * Cin), seed=12)
+    bias = inputs.normal_f32((Cout,), std=0.1, seed=13)
+    if bf16:
+        x_bits, w_bits = inputs.to_bf16_bits(xf), inputs.to_bf16_bits(wf)
+        xt = torch.from_numpy(x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        wt = torch.from_numpy(w_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        in_dt = out_dt = _lib.BF16
+        yt = torch.empty((N, Cout), dtype=torch.bfloat16, device=dev)
+    else:
+        x_bits, w_bits = xf, wf
+        xt, wt = torch.from_numpy(xf).to(dev), torch.from_numpy(wf).to(dev)
+        in_dt = out_dt = _lib.F32
+        yt = torch.empty((N, Cout), dtype=torch.float32, device=dev)
+    bt = torch.from_numpy(bias).to(dev)
+    ct = torch.from_numpy(wl.coords).to(dev)
+
+    size = np.array(wl.spatial_size, np.int32)
+    fa = np.array([1] + [layer.f] * wl.d, np.int32)
+    sa = np.ones(D, np.int32)
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    h = ctypes.c_void_p()
+    args_build = (_lib.VSC, D, ctypes.c_void_p(ct.data_ptr()), N, size.ctypes.data,
+                  fa.ctypes.data, sa.ctypes.data, _lib.BUILD_ASYNC, sp, ctypes.byref(h))
+    xp, wp, bp, ypt = (ctypes.c_void_p(t.data_ptr()) for t in (xt, wt, bt, yt))
+
+    def step(evs=None):
+        if evs:
+            evs[0].record(stream)
+        _lib.check(lib.spconv_build_rulebook(*args_build), "build")
+        if evs:
+            evs[1].record(stream)
+        _lib.check(lib.spconv_vsc_forward(h, in_dt, xp, wp, bp, out_dt, ypt, Cin, Cout, sp),
+                   "forward")
+        if evs:
+            evs[2].record(stream)
+        lib.spconv_rulebook_destroy(h)
+
+    # correctness gate on this exact input before timing: a synchronous build
+    # must succeed and its rule book must satisfy the VSC invariants
+    rb = spc.build_rulebook(spc.VSC, ct, wl.spatial_size, fa)
+    off = rb.pair_off
+    k = np.diff(off)
+    assert k[K // 2] == N and np.array_equal(k, k[::-1]), "rule book invariants failed"
+    sum_k = int(off[-1])
+    rb.close()
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    rb_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    fwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_per_step = (t1 - t0) * 1e3 / a.steps
+
+    # a last asynchronous build, checked for device-side errors
+    _lib.check(lib.spconv_build_rulebook(*args_build), "build")
+    _lib.check(lib.spconv_rulebook_status(h), "build status")
+    lib.spconv_rulebook_destroy(h)
+
+    flops = 2.0 * sum_k * Cin * Cout
+    tflops = flops / (fwd_ms * 1e-3) / 1e12
+    dt = "bf16" if bf16 else "f32"
+    peak = PEAKS[dt]
+    kernel = "k_fwd_mfma"
+    traffic = load_traffic(kernel, a.workload)
+    # forward algorithmic bytes: features in/out, gather map, weights, bias
+    esz = 2 if bf16 else 4
+    fwd_bytes = N * Cin * esz + N * Cout * esz + 4 * K * N + K * Cin * Cout * esz + 4 * Cout
+
+    out = {
+        "metric": "VSC layer active sites/sec + effective TFLOP/s (3^3, C=64, 128^3 surfaces)",
+        "value": N / (ms_per_step * 1e-3),
+        "unit": "active sites/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic",
+        "config": {"workload": a.workload, "variant": a.variant, "batch": wl.batch,
+                   "grid": wl.size, "active_sites": N, "sum_k": sum_k, "K": K,
+                   "c_in": Cin, "c_out": Cout, "out_dtype": dt},
+        "effective_tflops": tflops,
+        "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
+        "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
+        "roofline": {"bound": "mfma", "kernel": kernel, "achieved": tflops, "peak": peak,
+                     "unit": "TFLOP/s", "frac": tflops / peak, "traffic": traffic,
+                     "algorithmic_bytes": fwd_bytes},
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, bias, a.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

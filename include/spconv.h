@@ -1,0 +1,159 @@
+/* spconv.h - C ABI of the MI355X (gfx950) sparse-convolution library.
+ *
+ * Implements the two sparse convolutions of Graham & van der Maaten,
+ * "Submanifold Sparse Convolutional Networks":
+ *   SC(m, n, f, s)   an output site is active when any input site of its
+ *                    f^d receptive field is active; output extent
+ *                    (l - f + s) / s; inactive inputs count as zero
+ *                    (Section 3, definition of SC);
+ *   VSC(m, n, f, 1)  input padded by (f - 1)/2, output active exactly where
+ *                    the central input site is active, so the output set is
+ *                    the input set (Section 3, definition of VSC).
+ * Each layer has two phases (Section 4, Implementation): building the rule
+ * book R = (R_i) of (input row, output row) pairs per filter offset i, and
+ * the forward multiply-add, which starts from a zero output and adds
+ * (input row R_i(j,1)) x W^i into output row R_i(j,2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Sites.   A site is a tuple of D = 1 + d int32 coordinates; coordinate 0 is
+ *          the sample index in a batch.  Filters and strides are per
+ *          dimension with f[0] = s[0] = 1, so samples never interact.
+ *          1 <= spatial_size[j] <= 65535; every coordinate must satisfy
+ *          0 <= c_j < spatial_size[j].  2 <= D <= 4.
+ * Offsets. Filter offsets o in prod_j [0, f_j) are flattened row-major, last
+ *          dimension fastest: i = sum_j o_j prod_{l>j} f_l; K = prod_j f_j.
+ *          W^i multiplies the input site y + o - (f-1)/2 (VSC) or s*y + o
+ *          (SC) for output site y: a cross-correlation, no filter flip.
+ * Rows.    VSC output row r is input row r.  SC output rows are numbered in
+ *          lexicographic order of the output site (sample first).
+ *          Pairs inside R_i are ordered by output row.
+ * Memory.  coords, x, w, bias, y are device pointers owned by the caller:
+ *          contiguous, row-major, 16-byte aligned.  Host pointers are marked
+ *          "host".  A rule book owns its device memory (stream-ordered
+ *          allocations on the build stream) until spconv_rulebook_destroy.
+ * Streams. `stream` is a hipStream_t passed as void*; NULL is the null
+ *          stream.  All work is enqueued on it.
+ * Errors.  Every call returns a spconv_status; nothing is printed and
+ *          nothing aborts.  Argument errors are detected on the host before
+ *          any work is enqueued.
+ */
+#ifndef SPCONV_H
+#define SPCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPCONV_OK = 0,
+  SPCONV_EINVAL = -1, /* bad argument, dtype, shape or rule-book kind       */
+  SPCONV_EDUP = -2,   /* a site appears twice in the input coordinates      */
+  SPCONV_ERANGE = -3, /* a coordinate lies outside [0, spatial_size)         */
+  SPCONV_ENOMEM = -4, /* device allocation failed                            */
+  SPCONV_ECAP = -5,   /* hash table full (only with a forced tiny capacity)  */
+  SPCONV_EHIP = -6    /* a HIP runtime call failed                           */
+} spconv_status;
+
+typedef enum { SPCONV_F32 = 0, SPCONV_BF16 = 1 } spconv_dtype;
+typedef enum { SPCONV_VSC = 0, SPCONV_SC = 1 } spconv_kind;
+
+/* Build flags. */
+enum {
+  /* Return as soon as the work is enqueued.  Device-detected errors
+   * (EDUP, ERANGE, ECAP) are then reported by spconv_rulebook_status. */
+  SPCONV_BUILD_ASYNC = 1
+};
+
+typedef struct spconv_rulebook_s* spconv_rulebook;
+
+/* Build the rule book of one layer (Section 4: hash the active sites, then
+ * list for every filter offset the (input row, output row) pairs; VSC
+ * re-uses the input site set as its output set).
+ *
+ *   kind          SPCONV_VSC or SPCONV_SC
+ *   D             coordinates per site, 2..4 (sample index + d spatial)
+ *   coords        device int32 [N][D], distinct sites
+ *   N             number of active input sites, >= 0 (0 gives an empty book)
+ *   spatial_size  host int32 [D], grid extent; spatial_size[0] = batch size
+ *   f, s          host int32 [D], filter size and stride; f[0] = s[0] = 1;
+ *                 VSC needs every f_j odd and every s_j = 1
+ *   flags         0 (wait for the device result) or SPCONV_BUILD_ASYNC
+ *   stream        hipStream_t as void*
+ *   out           receives the handle; NULL on any error
+ *
+ * Errors: EINVAL (arguments), EDUP, ERANGE, ECAP (device-detected; with
+ * flags = 0 they are returned here and nothing is kept), ENOMEM, EHIP.
+ * The rule book is immutable once built; any number of forwards, on any
+ * stream ordered after the build, may use it (Section 4: one rule book
+ * serves every layer with the same sparsity pattern). */
+int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
+                          const int32_t* spatial_size, const int32_t* f,
+                          const int32_t* s, unsigned flags, void* stream,
+                          spconv_rulebook* out);
+
+/* Wait for the build and return its device-detected status (OK, EDUP,
+ * ERANGE or ECAP).  Needed only after an SPCONV_BUILD_ASYNC build. */
+int spconv_rulebook_status(spconv_rulebook rb);
+
+/* Sizes of a rule book (waits for the build).  Any output may be NULL.
+ *   n_in, n_out       active input / output sites
+ *   K                 number of filter offsets, prod f_j
+ *   out_spatial_size  host int32 [D]: VSC = input size; SC = floor((l-f)/s)+1
+ *   pair_off          host int64 [K+1]: pair_off[i+1] - pair_off[i] = k_i,
+ *                     the length of R_i (Section 4, rule book). */
+int spconv_rulebook_query(spconv_rulebook rb, int64_t* n_in, int64_t* n_out,
+                          int64_t* K, int32_t* out_spatial_size,
+                          int64_t* pair_off);
+
+/* Copy the output sites and the rule book into caller buffers (device).
+ *   out_coords  device int32 [n_out][D] or NULL
+ *   pairs       device int32 [pair_off[K]][2] or NULL: (input row, output
+ *               row), R_0 first, each R_i ordered by output row.
+ * Enqueued on `stream` after the build. */
+int spconv_rulebook_export(spconv_rulebook rb, int32_t* out_coords,
+                           int32_t* pairs, void* stream);
+
+/* Device pointer to the rule book's own output sites, int32 [n_out][D],
+ * valid until the rule book is destroyed (lets an SC output feed the next
+ * build without a copy). */
+int spconv_rulebook_out_coords(spconv_rulebook rb, const int32_t** coords);
+
+/* Forward pass of a VSC layer (Section 4: zero the output, then for every
+ * offset i and pair j add x[R_i(j,1)] W^i into y[R_i(j,2)]; plus bias).
+ *   rb      a rule book of kind SPCONV_VSC
+ *   in_dt   dtype of x and w: SPCONV_F32 or SPCONV_BF16
+ *   x       device [n_in][C_in]
+ *   w       device [K][C_in][C_out] (W^i is w[i], an m x n matrix)
+ *   bias    device fp32 [C_out] or NULL; added once at every output site
+ *   out_dt  dtype of y: SPCONV_F32 or SPCONV_BF16
+ *   y       device [n_out][C_out], fully overwritten
+ * Accumulation is fp32, in ascending offset order, without atomics, so
+ * repeated calls give bit-identical results; the result is rounded once to
+ * out_dt (round to nearest even).  Nothing is allocated; the call is
+ * asynchronous on `stream`.  Errors: EINVAL (kind, dtype, C < 1, NULL). */
+int spconv_vsc_forward(spconv_rulebook rb, int in_dt, const void* x,
+                       const void* w, const float* bias, int out_dt, void* y,
+                       int C_in, int C_out, void* stream);
+
+/* Forward pass of an SC layer; arguments as spconv_vsc_forward, with rb of
+ * kind SPCONV_SC and y of n_out rows (Section 3 / Section 4). */
+int spconv_sc_forward(spconv_rulebook rb, int in_dt, const void* x,
+                      const void* w, const float* bias, int out_dt, void* y,
+                      int C_in, int C_out, void* stream);
+
+/* Release a rule book (stream-ordered on its build stream).  NULL is a
+ * no-op. */
+void spconv_rulebook_destroy(spconv_rulebook rb);
+
+/* Static string naming a status code. */
+const char* spconv_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPCONV_H */

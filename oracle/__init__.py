@@ -53,6 +53,8 @@ def _load():
     lib.ref_export.restype = I32
     lib.ref_forward.argtypes = [P, I32, P, P, P, I32, I32, P, P, P]
     lib.ref_forward.restype = I32
+    lib.ref_forward_rows.argtypes = [P, I32, P, P, P, I32, I32, P, P, P]
+    lib.ref_forward_rows.restype = I32
     lib.ref_round.argtypes = [P, I64, I32, P]
     lib.ref_round.restype = I32
     lib.ref_free.argtypes = [P]
@@ -121,6 +123,23 @@ class Rulebook:
         if st != OK:
             raise OracleError(st)
         return y, absb
+
+    def forward_rows(self, rows, x, w, bias=None, in_dt=F32):
+        """Output rows `rows` only: (y [len(rows), C_out], absb) in float64."""
+        lib = _load()
+        x = np.ascontiguousarray(x)
+        w = np.ascontiguousarray(w)
+        C_in, C_out = w.shape[1], w.shape[2]
+        mask = np.zeros(self.n_out, np.uint8)
+        mask[np.asarray(rows)] = 1
+        y = np.zeros((self.n_out, C_out), np.float64)
+        absb = np.zeros((self.n_out, C_out), np.float64)
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        st = lib.ref_forward_rows(self._h, in_dt, _ptr(x), _ptr(w), _ptr(b), C_in, C_out,
+                                  _ptr(mask), _ptr(y), _ptr(absb))
+        if st != OK:
+            raise OracleError(st)
+        return y[rows], absb[rows]
 
     def __del__(self):
         h = getattr(self, "_h", None)

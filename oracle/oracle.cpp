@@ -256,6 +256,40 @@ int ref_forward(void* h, int in_dt, const void* x, const void* w,
   return OK;
 }
 
+// Same as ref_forward restricted to the output rows with rows_mask[y] != 0
+// (host uint8 [n_out]); other rows of y / absb are left untouched.  Lets a
+// test check sampled rows of a layer too large for the full CPU forward.
+int ref_forward_rows(void* h, int in_dt, const void* x, const void* w,
+                     const float* bias, int C_in, int C_out,
+                     const uint8_t* rows_mask, double* y, double* absb) {
+  if (!h || !rows_mask || C_in < 1 || C_out < 1 ||
+      (in_dt != F32 && in_dt != BF16))
+    return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  for (int64_t r = 0; r < rb->n_out; ++r) {
+    if (!rows_mask[r]) continue;
+    for (int n = 0; n < C_out; ++n) {
+      double b = bias ? static_cast<double>(bias[n]) : 0.0;
+      y[r * C_out + n] = b;
+      absb[r * C_out + n] = std::fabs(b);
+    }
+  }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i]) {
+      const int64_t xi = pr[0], yo = pr[1];
+      if (!rows_mask[yo]) continue;
+      for (int c = 0; c < C_in; ++c) {
+        const double xv = load(in_dt, x, xi * C_in + c);
+        for (int n = 0; n < C_out; ++n) {
+          const double wv = load(in_dt, w, (i * C_in + c) * C_out + n);
+          y[yo * C_out + n] += xv * wv;
+          absb[yo * C_out + n] += std::fabs(xv) * std::fabs(wv);
+        }
+      }
+    }
+  return OK;
+}
+
 // Round doubles once to the output type: fp32 (out: float*) or bf16 (out:
 // uint16_t* bit patterns), both round-to-nearest-even.
 int ref_round(const double* v, int64_t n, int out_dt, void* out) {

@@ -1,0 +1,189 @@
+"""Sparse convolutions SC and VSC on MI355X (gfx950).
+
+Python face of libspconv.so.  The functions here marshal torch tensors into
+the C ABI (include/spconv.h); all computation runs in the HIP kernels.
+
+    rb = build_rulebook(VSC, coords, spatial_size, f)     # coords: int32 cuda [N, D]
+    y  = vsc_forward(rb, x, w, bias)                       # x: [N, C_in], w: [K, C_in, C_out]
+
+A rule book is reusable for every layer with the same site set (Section 4 of
+the paper).  Everything runs on torch's current stream.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+
+from . import _lib
+from ._lib import (BF16, BUILD_ASYNC, EDUP, EINVAL, ENOMEM, ERANGE, ECAP, EHIP, F32,
+                   OK, SC, VSC, SpconvError)
+
+__all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "Rulebook", "build_rulebook",
+           "vsc_forward", "sc_forward", "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE",
+           "ENOMEM", "ECAP", "EHIP"]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t == torch.float32:
+        return F32
+    if t == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t}: use float32 or bfloat16")
+
+
+def _i32_array(v, D, name):
+    a = np.ascontiguousarray(np.asarray(v, dtype=np.int32).reshape(-1))
+    if a.size != D:
+        raise ValueError(f"{name} needs {D} entries, got {a.size}")
+    return a
+
+
+class Rulebook:
+    """Owner of a libspconv rule-book handle."""
+
+    def __init__(self, handle, kind, D, stream):
+        self._h = handle
+        self.kind = kind
+        self.D = D
+        self._stream = stream
+        self._sizes = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    def _query(self):
+        if self._sizes is None:
+            lib = _lib.load()
+            n_in, n_out, K = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+            osz = np.zeros(self.D, np.int32)
+            _lib.check(lib.spconv_rulebook_query(self._h, ctypes.byref(n_in), ctypes.byref(n_out),
+                                                 ctypes.byref(K), osz.ctypes.data, None),
+                       "spconv_rulebook_query")
+            off = np.zeros(K.value + 1, np.int64)
+            _lib.check(lib.spconv_rulebook_query(self._h, None, None, None, None,
+                                                 off.ctypes.data), "spconv_rulebook_query")
+            self._sizes = (n_in.value, n_out.value, K.value, osz, off)
+        return self._sizes
+
+    def status(self):
+        return _lib.load().spconv_rulebook_status(self._h)
+
+    @property
+    def n_in(self):
+        return self._query()[0]
+
+    @property
+    def n_out(self):
+        return self._query()[1]
+
+    @property
+    def K(self):
+        return self._query()[2]
+
+    @property
+    def out_spatial_size(self):
+        return self._query()[3].copy()
+
+    @property
+    def pair_off(self):
+        return self._query()[4].copy()
+
+    def export(self):
+        """(out_coords int32 [n_out, D], pairs int32 [sum k, 2]) as cuda tensors."""
+        torch = _torch()
+        n_out, off = self.n_out, self.pair_off
+        oc = torch.empty((n_out, self.D), dtype=torch.int32, device="cuda")
+        pr = torch.empty((int(off[-1]), 2), dtype=torch.int32, device="cuda")
+        _lib.check(_lib.load().spconv_rulebook_export(
+            self._h, oc.data_ptr() if n_out else None, pr.data_ptr() if off[-1] else None,
+            _stream_ptr()), "spconv_rulebook_export")
+        return oc, pr
+
+    def close(self):
+        if self._h:
+            _lib.load().spconv_rulebook_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, stream=None):
+    """Build the rule book of one SC / VSC layer on the GPU.
+
+    coords: int32 cuda tensor [N, D] (column 0 = sample index).
+    spatial_size, f, s: length-D integer sequences, f[0] = s[0] = 1.
+    sync=False enqueues the build and returns at once; device-detected
+    errors are then reported by Rulebook.status().
+    """
+    torch = _torch()
+    lib = _lib.load()
+    if coords.dtype != torch.int32 or not coords.is_cuda or coords.dim() != 2:
+        raise TypeError("coords must be an int32 cuda tensor [N, D]")
+    coords = coords.contiguous()
+    D = coords.shape[1]
+    size = _i32_array(spatial_size, D, "spatial_size")
+    fa = _i32_array(f, D, "f")
+    sa = _i32_array(np.ones(D) if s is None else s, D, "s")
+    h = ctypes.c_void_p()
+    st_ptr = _stream_ptr(stream)
+    st = lib.spconv_build_rulebook(kind, D, coords.data_ptr() if coords.shape[0] else None,
+                                   coords.shape[0], size.ctypes.data, fa.ctypes.data,
+                                   sa.ctypes.data, 0 if sync else BUILD_ASYNC, st_ptr,
+                                   ctypes.byref(h))
+    _lib.check(st, "spconv_build_rulebook")
+    return Rulebook(h, kind, D, st_ptr)
+
+
+def _forward(fn, kind, rb, x, w, bias, out_dtype, out, stream):
+    torch = _torch()
+    if rb.kind != kind:
+        raise ValueError("rule book kind does not match the forward")
+    C_in, C_out = int(w.shape[1]), int(w.shape[2])
+    in_dt = _dtype_code(x.dtype)
+    if w.dtype != x.dtype:
+        raise TypeError("x and w must share a dtype")
+    out_dtype = x.dtype if out_dtype is None else out_dtype
+    out_dt = _dtype_code(out_dtype)
+    x = x.contiguous()
+    w = w.contiguous()
+    if bias is not None:
+        bias = bias.contiguous()
+        if bias.dtype != torch.float32:
+            raise TypeError("bias must be float32")
+    if out is None:
+        out = torch.empty((rb.n_out, C_out), dtype=out_dtype, device=x.device)
+    if out.numel() == 0:
+        return out
+    st = fn(rb.handle, in_dt, x.data_ptr() if x.numel() else None, w.data_ptr(),
+            bias.data_ptr() if bias is not None else None, out_dt,
+            out.data_ptr() if out.numel() else None, C_in, C_out, _stream_ptr(stream))
+    _lib.check(st, "forward")
+    return out
+
+
+def vsc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
+    """VSC forward: y[n_out, C_out] = bias + sum_i gathered x @ w[i]."""
+    return _forward(_lib.load().spconv_vsc_forward, VSC, rb, x, w, bias, out_dtype, out, stream)
+
+
+def sc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
+    """SC forward on an SC rule book (output rows = rb.n_out)."""
+    return _forward(_lib.load().spconv_sc_forward, SC, rb, x, w, bias, out_dtype, out, stream)

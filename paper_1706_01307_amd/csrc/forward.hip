@@ -1,0 +1,422 @@
+// Forward multiply-add of SC / VSC on gfx950 (Section 4 of the paper: zero
+// the output, then for every offset i and pair j add input row R_i(j,1)
+// times W^i into output row R_i(j,2); Table 1: a*m*n multiply-adds per active
+// output site).
+//
+// The kernels are output-stationary: a workgroup owns a tile of output rows
+// and keeps their fp32 accumulators in registers while it walks the offsets
+// in ascending order.  For offset i it gathers the input rows G[i][y] of its
+// output rows (the gather map built with the rule book; -1 = no active
+// input, read as zeros) and multiplies them by W^i.  Every output element is
+// written once, by one lane, after a fixed-order sum: no atomics, bitwise
+// reproducible.
+//
+//   k_fwd_mfma  dense contraction on the matrix cores: v_mfma 16x16x32 bf16
+//               or 16x16x4 f32.  W^i is staged into LDS transposed (one
+//               padded row per output column) and double-buffered across
+//               offsets; gathered rows go straight from memory to registers
+//               through buffer loads whose hardware range check returns zero
+//               for absent neighbours; a 16-row block whose 16 rows all lack
+//               offset i skips that offset's MFMAs.
+//   k_fwd_vec   any channel count: one lane per (output row, output column),
+//               fp32 FMA chain.  The low-channel path (e.g. 1 input plane).
+#include <cstdlib>
+#include <cstring>
+
+#include "internal.h"
+
+namespace spc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr uint32_t kBufDword3 = 0x00020000u;   // gfx9 raw buffer descriptor word 3
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename T> struct ElemIO;
+template <> struct ElemIO<float> {
+  __device__ static float load(const float* p, int64_t i) { return p[i]; }
+  __device__ static void store(float* p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct ElemIO<uint16_t> {
+  __device__ static float load(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+  __device__ static void store(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+// ---------------------------------------------------------------------------
+// Generic (vector ALU) path
+// ---------------------------------------------------------------------------
+template <typename TIn, typename TOut>
+__global__ __launch_bounds__(256) void k_fwd_vec(
+    const int32_t* __restrict__ gmap, int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K,
+    const TIn* __restrict__ x, const TIn* __restrict__ w, const float* __restrict__ bias,
+    TOut* __restrict__ y, int C_in, int C_out) {
+  const int64_t n_rows = hdr->n_out;
+  const int64_t total = n_rows * C_out;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; idx < total;
+       idx += stride) {
+    const int64_t row = idx / C_out;
+    const int col = static_cast<int>(idx - row * C_out);
+    float acc = 0.0f;
+    for (int i = 0; i < K; ++i) {
+      const int32_t g = gmap[i * n_cap + row];
+      if (g < 0) continue;
+      const int64_t xb = static_cast<int64_t>(g) * C_in;
+      const int64_t wb = static_cast<int64_t>(i) * C_in * C_out + col;
+      for (int c = 0; c < C_in; ++c)
+        acc = fmaf(ElemIO<TIn>::load(x, xb + c), ElemIO<TIn>::load(w, wb + c * C_out), acc);
+    }
+    if (bias) acc += bias[col];
+    ElemIO<TOut>::store(y, idx, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core path
+// ---------------------------------------------------------------------------
+// Element traits: a lane moves 16 bytes per k-chunk; KC real k per chunk
+// across the 4 lane groups of a 16x16 MFMA.
+template <typename T> struct MT;
+template <> struct MT<uint16_t> {          // bf16
+  static constexpr int KC = 32;            // 8 bf16 per lane x 4 groups
+  static constexpr int T = 8;              // transpose tile (elements per 16 B)
+  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct MT<float> {             // fp32
+  static constexpr int KC = 16;            // 4 fp32 per lane x 4 groups
+  static constexpr int T = 4;
+  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+    // The 4 elements of a lane's 16-byte chunk are consumed by 4 MFMA steps;
+    // step e pairs A[r][16ch + 4g + e] with B[16ch + 4g + e][c] in every lane
+    // group g, so the 4 steps cover the chunk's 16 k exactly once.
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[e]), __uint_as_float(b[e]), c,
+                                               0, 0, 0);
+    return c;
+  }
+};
+
+template <typename TOut, int NCB> struct OutStore;
+template <int NCB> struct OutStore<float, NCB> {
+  __device__ static void store(float* p, const float* v) {
+    if constexpr (NCB == 4) {
+      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    } else if constexpr (NCB == 2) {
+      *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+    } else {
+      p[0] = v[0];
+    }
+  }
+};
+template <int NCB> struct OutStore<uint16_t, NCB> {
+  __device__ static void store(uint16_t* p, const float* v) {
+    if constexpr (NCB == 4) {
+      uint2 u;
+      u.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+      u.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+      *reinterpret_cast<uint2*>(p) = u;
+    } else if constexpr (NCB == 2) {
+      *reinterpret_cast<uint32_t*>(p) =
+          f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    } else {
+      p[0] = f32_to_bf16(v[0]);
+    }
+  }
+};
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+// Tile of the output handled by one workgroup: 4 waves x RB blocks of 16 rows,
+// NCB blocks of 16 columns (the whole workgroup shares one column chunk).
+//
+// Lane layout (16x16 MFMA): lane l = 16 g + r.  A operand: row r of the
+// 16-row block, k-chunk bytes [16 g, 16 g + 16).  B operand: output column
+// r * NCB + cb of the chunk (so a lane ends up owning NCB adjacent columns),
+// same k bytes.  Result: lane l holds rows 4 g + v (v = 0..3), columns
+// r * NCB + cb.
+template <typename TIn, int NCH, int NCB, int RB, typename TOut>
+__global__ __launch_bounds__(256, 2) void k_fwd_mfma(
+    const int32_t* __restrict__ gmap, int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K,
+    const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
+    const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles) {
+  constexpr int KC = MT<TIn>::KC;
+  constexpr int CIN = NCH * KC;
+  constexpr int COLS = NCB * 16;
+  constexpr int ROWB = CIN * static_cast<int>(sizeof(TIn));     // bytes of one input row
+  constexpr int LDWB = ROWB + 16;                                // padded LDS row (bytes)
+  constexpr int T = MT<TIn>::T;
+  constexpr int NTILE = (CIN / T) * (COLS / T);                  // transpose tiles per offset
+  constexpr int TPT = (NTILE + 255) / 256;                       // tiles per thread
+  constexpr int WAVE_ROWS = RB * 16;
+  constexpr int TILE_ROWS = 4 * WAVE_ROWS;
+
+  __shared__ __attribute__((aligned(16))) unsigned char s_w[2][COLS * LDWB];
+
+  // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
+  // contiguous range of tiles so neighbouring tiles share that XCD's L2.
+  const int64_t per = gridDim.x / 8;
+  const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (tile >= ntiles) return;
+
+  const int64_t n_rows = hdr->n_out;
+  const int col0 = blockIdx.y * COLS;
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int lr = lane % 16, lg = lane / 16;
+  const int64_t row0 = tile * TILE_ROWS + wave * WAVE_ROWS;
+
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<TIn*>(x), 0, static_cast<int>(x_bytes),
+                                        static_cast<int>(kBufDword3));
+  constexpr uint32_t kOOB = 0x80000000u;   // past any x_bytes < 2^31: reads as zero
+
+  // --- W^i staging: tile (kt, ct) of T k-rows x T columns, transposed in
+  // registers, written as T LDS rows (one per column) of T k-values.
+  u32x4 wreg[TPT][T];
+  auto w_load = [&](int i) {
+#pragma unroll
+    for (int q = 0; q < TPT; ++q) {
+      const int t = threadIdx.x + q * 256;
+      if (t < NTILE) {
+        const int kt = t % (CIN / T), ct = t / (CIN / T);
+        const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * T) * C_out + col0 + ct * T;
+#pragma unroll
+        for (int r = 0; r < T; ++r)
+          wreg[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
+      }
+    }
+  };
+  auto w_store = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < TPT; ++q) {
+      const int t = threadIdx.x + q * 256;
+      if (t < NTILE) {
+        const int kt = t % (CIN / T), ct = t / (CIN / T);
+#pragma unroll
+        for (int cc = 0; cc < T; ++cc) {
+          u32x4 o;
+          if constexpr (sizeof(TIn) == 2) {
+            // column cc of the 8x8 bf16 tile: element cc of each of 8 rows
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+              const uint32_t lo = (wreg[q][2 * p][cc / 2] >> (16 * (cc % 2))) & 0xffffu;
+              const uint32_t hi = (wreg[q][2 * p + 1][cc / 2] >> (16 * (cc % 2))) & 0xffffu;
+              o[p] = lo | (hi << 16);
+            }
+          } else {
+#pragma unroll
+            for (int p = 0; p < 4; ++p) o[p] = wreg[q][p][cc];
+          }
+          *reinterpret_cast<u32x4*>(&s_w[buf][(ct * T + cc) * LDWB + kt * 16]) = o;
+        }
+      }
+    }
+  };
+
+  // --- gather-map rows of this wave: G[i][row0 + 16 b + r]
+  auto g_load = [&](int i, int32_t* g) {
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int64_t row = row0 + b * 16 + lr;
+      g[b] = (i < K && row < n_rows) ? gmap[static_cast<int64_t>(i) * n_cap + row] : -1;
+    }
+  };
+  auto a_load = [&](const int32_t* g, u32x4 (*a)[NCH]) {
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const uint32_t base = g[b] >= 0 ? static_cast<uint32_t>(g[b]) * ROWB + lg * 16 : kOOB;
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch)
+        a[b][ch] = buf_load16(xr, base == kOOB ? kOOB : base + ch * 64);
+    }
+  };
+
+  f32x4 acc[RB][NCB];
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[b][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  int32_t g_cur[RB], g_nxt[RB], g_nn[RB];
+  u32x4 a_cur[RB][NCH], a_nxt[RB][NCH];
+
+  w_load(0);
+  w_store(0);
+  g_load(0, g_cur);
+  a_load(g_cur, a_cur);
+  g_load(1, g_nxt);
+  __syncthreads();
+
+  for (int i = 0; i < K; ++i) {
+    const int buf = i & 1;
+    if (i + 1 < K) {
+      a_load(g_nxt, a_nxt);
+      w_load(i + 1);
+    }
+    g_load(i + 2, g_nn);
+
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      if (__ballot(g_cur[b] >= 0) == 0) continue;      // whole block lacks offset i
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const u32x4 bw = *reinterpret_cast<const u32x4*>(
+              &s_w[buf][(lr * NCB + cb) * LDWB + ch * 64 + lg * 16]);
+          acc[b][cb] = MT<TIn>::mma(a_cur[b][ch], bw, acc[b][cb]);
+        }
+      }
+    }
+
+    if (i + 1 < K) w_store(buf ^ 1);
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      g_cur[b] = g_nxt[b];
+      g_nxt[b] = g_nn[b];
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) a_cur[b][ch] = a_nxt[b][ch];
+    }
+  }
+
+  // --- epilogue: bias, round once, store NCB adjacent columns per lane-row
+  float bv[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t row = row0 + b * 16 + lg * 4 + v;
+      if (row < n_rows) {
+        float o[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
+        OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dispatch
+// ---------------------------------------------------------------------------
+// Row blocks per wave: fewer when the input rows are wide, so that the two
+// register sets of gathered rows (current and next offset) still fit.
+template <int NCH>
+constexpr int rows_blocks() { return NCH <= 2 ? 4 : (NCH <= 4 ? 2 : 1); }
+
+template <typename TIn, int NCH, int NCB, typename TOut>
+void launch_mfma(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
+                 const float* bias, void* y, int C_out, hipStream_t stream) {
+  constexpr int RB = rows_blocks<NCH>();
+  constexpr int kTileRows = 4 * RB * 16;
+  const int64_t ntiles = (rb->n_cap + kTileRows - 1) / kTileRows;
+  const int64_t per = (ntiles + 7) / 8;
+  dim3 grid(static_cast<unsigned>(8 * per), static_cast<unsigned>(C_out / (NCB * 16)));
+  k_fwd_mfma<TIn, NCH, NCB, RB, TOut><<<grid, 256, 0, stream>>>(
+      rb->gmap, rb->n_cap, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x), x_bytes,
+      static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_out, ntiles);
+}
+
+template <typename TIn, int NCH, typename TOut>
+void launch_mfma_ncb(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
+                     const float* bias, void* y, int C_out, hipStream_t stream) {
+  if (C_out % 64 == 0)
+    launch_mfma<TIn, NCH, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
+  else if (C_out % 32 == 0)
+    launch_mfma<TIn, NCH, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
+  else
+    launch_mfma<TIn, NCH, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
+}
+
+template <typename TOut>
+bool try_mfma(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
+              void* y, int C_in, int C_out, hipStream_t stream) {
+  if (C_out % 16 != 0) return false;
+  const uint64_t xb = static_cast<uint64_t>(rb->n_in) * C_in * (in_dt == SPCONV_BF16 ? 2 : 4);
+  if (xb >= 0x7fffffffull) return false;                 // buffer range is 31-bit here
+  const uint32_t x_bytes = static_cast<uint32_t>(xb);
+  if (in_dt == SPCONV_BF16) {
+    switch (C_in) {
+      case 32: launch_mfma_ncb<uint16_t, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+      case 64: launch_mfma_ncb<uint16_t, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+      case 96: launch_mfma_ncb<uint16_t, 3, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+      case 128: launch_mfma_ncb<uint16_t, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+      default: return false;
+    }
+  }
+  switch (C_in) {
+    case 16: launch_mfma_ncb<float, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+    case 32: launch_mfma_ncb<float, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+    case 64: launch_mfma_ncb<float, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+    case 96: launch_mfma_ncb<float, 6, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+    case 128: launch_mfma_ncb<float, 8, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
+    default: return false;
+  }
+}
+
+template <typename TIn, typename TOut>
+void launch_vec(spconv_rulebook rb, const void* x, const void* w, const float* bias, void* y,
+                int C_in, int C_out, hipStream_t stream) {
+  const int64_t total = rb->n_cap * C_out;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  k_fwd_vec<TIn, TOut><<<static_cast<unsigned>(blocks), 256, 0, stream>>>(
+      rb->gmap, rb->n_cap, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x),
+      static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_in, C_out);
+}
+
+bool force_vector_path() {
+  const char* e = std::getenv("SPCONV_FORCE_PATH");
+  return e && std::strcmp(e, "vec") == 0;
+}
+
+}  // namespace
+
+int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
+            int out_dt, void* y, int C_in, int C_out, hipStream_t stream) {
+  if (rb->n_cap == 0) return SPCONV_OK;
+  bool done = false;
+  if (!force_vector_path()) {
+    done = out_dt == SPCONV_F32
+               ? try_mfma<float>(rb, in_dt, x, w, bias, y, C_in, C_out, stream)
+               : try_mfma<uint16_t>(rb, in_dt, x, w, bias, y, C_in, C_out, stream);
+  }
+  if (!done) {
+    if (in_dt == SPCONV_F32 && out_dt == SPCONV_F32)
+      launch_vec<float, float>(rb, x, w, bias, y, C_in, C_out, stream);
+    else if (in_dt == SPCONV_F32)
+      launch_vec<float, uint16_t>(rb, x, w, bias, y, C_in, C_out, stream);
+    else if (out_dt == SPCONV_F32)
+      launch_vec<uint16_t, float>(rb, x, w, bias, y, C_in, C_out, stream);
+    else
+      launch_vec<uint16_t, uint16_t>(rb, x, w, bias, y, C_in, C_out, stream);
+  }
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+}  // namespace spc

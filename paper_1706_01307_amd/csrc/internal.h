@@ -1,0 +1,168 @@
+// Internal declarations of the gfx950 sparse-convolution library.
+//
+// Everything in here is device-side building blocks shared by the rule-book
+// and forward translation units, plus the host-side rule-book object.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "spconv.h"
+
+namespace spc {
+
+// ---------------------------------------------------------------------------
+// Status bits written by device kernels (OR-ed into one word).
+// ---------------------------------------------------------------------------
+enum : uint32_t { kStRange = 1u, kStDup = 2u, kStCap = 4u };
+
+constexpr int kMaxD = 4;
+constexpr int kMaxK = 1024;          // filter offsets per layer
+constexpr uint64_t kEmpty = ~0ull;   // empty hash slot
+constexpr int kBlock = 256;          // rows per rule-book block (4 waves)
+
+// ---------------------------------------------------------------------------
+// Order-preserving site codec: coordinate j occupies `bits[j]` bits at
+// `shift[j]`, coordinate 0 (sample) in the high bits, so integer order of
+// keys is lexicographic order of sites.
+// ---------------------------------------------------------------------------
+struct Codec {
+  int D;
+  int kbits;                 // total key bits
+  int shift[kMaxD];
+  uint32_t fmask[kMaxD];
+  int32_t size[kMaxD];
+};
+
+__host__ __device__ inline uint64_t pack_site(const Codec& c, const int32_t* x) {
+  uint64_t k = 0;
+  for (int j = 0; j < c.D; ++j) k |= static_cast<uint64_t>(x[j]) << c.shift[j];
+  return k;
+}
+
+__host__ __device__ inline void unpack_site(const Codec& c, uint64_t k, int32_t* x) {
+  for (int j = 0; j < c.D; ++j)
+    x[j] = static_cast<int32_t>((k >> c.shift[j]) & c.fmask[j]);
+}
+
+// ---------------------------------------------------------------------------
+// Open-addressing hash table of sites -> rows.  Slots are grouped in
+// buckets of 4 (32 bytes, one aligned sector of a cache line); a lookup reads
+// one bucket and only moves to the next bucket when all 4 slots are taken.
+// Packed layout: slot = key << rbits | row (one 64-bit word, one CAS per
+// insert).  Wide layout (when key bits + row bits exceed 64): key words in
+// `slots`, rows in `vals`.
+// ---------------------------------------------------------------------------
+struct Table {
+  uint64_t* slots;
+  int32_t* vals;       // wide layout only
+  uint64_t nbuckets;   // power of two
+  int rbits;           // packed layout: bits of the row field
+};
+
+__device__ __forceinline__ uint64_t mix64(uint64_t k) {
+  // 64-bit finaliser (xor-shift / multiply avalanche).
+  k ^= k >> 33;
+  k *= 0xff51afd7ed558ccdull;
+  k ^= k >> 33;
+  k *= 0xc4ceb9fe1a85ec53ull;
+  k ^= k >> 33;
+  return k;
+}
+
+__device__ __forceinline__ uint64_t home_bucket(const Table& t, uint64_t key) {
+  return mix64(key) & (t.nbuckets - 1);
+}
+
+// Match one bucket (4 slots already loaded) against `key`.
+// Returns the row (>= 0), -1 if the key is absent (an empty slot was seen),
+// or -2 if the bucket is full without the key (continue to the next bucket).
+template <bool WIDE>
+__device__ __forceinline__ int32_t match_bucket(const Table& t, uint64_t b,
+                                                const uint64_t s[4], uint64_t key) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (s[j] == kEmpty) return -1;
+    if (WIDE) {
+      if (s[j] == key) return t.vals[4 * b + j];
+    } else {
+      if ((s[j] >> t.rbits) == key)
+        return static_cast<int32_t>(s[j] & ((1ull << t.rbits) - 1));
+    }
+  }
+  return -2;
+}
+
+__device__ __forceinline__ void load_bucket(const Table& t, uint64_t b, uint64_t s[4]) {
+  const ulonglong2* p = reinterpret_cast<const ulonglong2*>(t.slots + 4 * b);
+  ulonglong2 a = p[0], c = p[1];
+  s[0] = a.x; s[1] = a.y; s[2] = c.x; s[3] = c.y;
+}
+
+// Slow path of a lookup: continue probing after bucket `b` was full.
+template <bool WIDE>
+__device__ __noinline__ int32_t find_from(const Table& t, uint64_t b, uint64_t key) {
+  for (uint64_t p = 1; p < t.nbuckets; ++p) {
+    b = (b + 1) & (t.nbuckets - 1);
+    uint64_t s[4];
+    load_bucket(t, b, s);
+    int32_t r = match_bucket<WIDE>(t, b, s, key);
+    if (r != -2) return r;
+  }
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// Host-side rule book.
+// ---------------------------------------------------------------------------
+struct DeviceHeader {          // first bytes of the rule book's allocation
+  uint32_t status;             // kSt* bits
+  uint32_t pad;
+  int64_t n_out;               // output rows (SC: computed on the device)
+};
+
+}  // namespace spc
+
+struct spconv_rulebook_s {
+  int kind;
+  int D;
+  int device;
+  int64_t n_in;
+  int64_t n_cap;               // output rows the buffers are sized for
+  int64_t K;
+  int32_t size[spc::kMaxD], f[spc::kMaxD], s[spc::kMaxD], out_size[spc::kMaxD];
+  hipStream_t stream;          // build stream (owns the allocation)
+  void* mem;                   // one stream-ordered allocation
+  size_t mem_bytes;
+  // carved device pointers
+  spc::DeviceHeader* hdr;
+  int32_t* out_coords;         // [n_cap][D]
+  int32_t* gmap;               // [K][n_cap] input row per (offset, output row), -1 absent
+  int32_t* blk_cnt;            // [K][nblk] per-block pair counts, then bases
+  int64_t* totals;             // [K] k_i
+  int64_t* pair_off;           // [K+1]
+  int32_t* pairs;              // [K * n_cap][2]
+  int64_t nblk;                // ceil(n_cap / kBlock)
+  // host state after synchronisation
+  bool synced;
+  int status;
+  int64_t n_out;
+};
+
+namespace spc {
+
+// Launchers (rulebook.hip).  All asynchronous on rb->stream.
+int build_vsc(spconv_rulebook rb, const int32_t* coords);
+int build_sc(spconv_rulebook rb, const int32_t* coords);
+
+// Forward (forward.hip).
+int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
+            const float* bias, int out_dt, void* y, int C_in, int C_out,
+            hipStream_t stream);
+
+// Host helpers (abi.cpp).
+Codec make_codec(int D, const int32_t* size);
+inline int bitlen(uint64_t v) { int b = 0; while (v) { ++b; v >>= 1; } return b; }
+
+}  // namespace spc

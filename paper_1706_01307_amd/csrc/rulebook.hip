@@ -1,0 +1,601 @@
+// Rule-book construction on gfx950 (Section 4 of the paper: hash the active
+// sites, then list the (input row, output row) pairs of every filter offset).
+//
+// VSC (output set = input set):
+//   k_init       clear the status word, set n_out = N, empty the table
+//   k_insert     pack every site into an order-preserving key; CAS-insert it
+//                into the open-addressing table (flags range errors and
+//                duplicates)
+//   k_probe      per output row and offset, look up the neighbour site ->
+//                gather map G[i][y] (input row or -1); per-block pair counts
+//   k_scan       per offset, exclusive scan of the block counts -> k_i
+//   k_compact    per-offset stream compaction of G into R_i, ordered by
+//                output row (wave ballot + mbcnt, block prefix in LDS)
+// SC (output set = sites with an active input in their receptive field):
+//   k_init, k_insert as above, then
+//   k_sc_mark    every input marks the output sites it feeds in a bitmap
+//                over the output grid (lexicographic linear index)
+//   k_bitsum / k_bitscan / k_sc_emit
+//                rank the marked sites by a popcount prefix sum, which
+//                numbers the output rows in lexicographic order
+//   k_probe, k_scan, k_compact as for VSC, probing input site s*y + o.
+#include <cstdlib>
+
+#include "internal.h"
+
+namespace spc {
+namespace {
+
+constexpr int kWave = 64;
+
+struct Extents {
+  int32_t e[kMaxD];
+};
+
+struct OffsetTable {
+  int K;
+  int D;
+  int32_t f[kMaxD];
+  int32_t s[kMaxD];
+  int32_t r[kMaxD];     // VSC: (f-1)/2; SC: 0
+  int centre;           // VSC: index of the zero offset; SC: -1
+};
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ int prefix_popc(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0));
+}
+
+// Inclusive prefix sum over a wave of 64 lanes.
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    T t = __shfl_up(v, d, kWave);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over a 256-thread block; *total receives the sum.
+template <typename T>
+__device__ __forceinline__ T block_excl_scan(T v, T* total) {
+  __shared__ T s_w[kBlock / kWave];
+  const int wave = threadIdx.x / kWave;
+  T inc = wave_incl_scan(v);
+  if (lane_id() == kWave - 1) s_w[wave] = inc;
+  __syncthreads();
+  T base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / kWave; ++w) {
+    if (w < wave) base += s_w[w];
+    tot += s_w[w];
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+// Per-dimension offset o_j - r_j of every filter offset i, in LDS.
+__device__ void fill_offsets(const OffsetTable& ot, int16_t (*s_off)[kMaxD]) {
+  for (int i = threadIdx.x; i < ot.K; i += blockDim.x) {
+    int rem = i;
+    for (int j = ot.D - 1; j >= 0; --j) {
+      int o = rem % ot.f[j];
+      rem /= ot.f[j];
+      s_off[i][j] = static_cast<int16_t>(o - ot.r[j]);
+    }
+  }
+}
+
+__global__ void k_fill_u64(uint64_t* __restrict__ p, uint64_t v, uint64_t n) {
+  uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+  for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n;
+       i += stride)
+    p[i] = v;
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, uint64_t n) {
+  uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+  for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n;
+       i += stride)
+    p[i] = v;
+}
+
+__global__ void k_init_header(DeviceHeader* h, int64_t n_out) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    h->status = 0;
+    h->pad = 0;
+    h->n_out = n_out;
+  }
+}
+
+// Insert input row r's site into the table.
+template <bool WIDE>
+__global__ __launch_bounds__(kBlock) void k_insert(
+    const int32_t* __restrict__ coords, int64_t N, Codec c, Table t,
+    uint64_t* __restrict__ keys, int32_t* __restrict__ copy_out,
+    uint32_t* __restrict__ status) {
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (r >= N) return;
+  int32_t x[kMaxD];
+  bool ok = true;
+  for (int j = 0; j < c.D; ++j) {
+    x[j] = coords[r * c.D + j];
+    ok = ok && x[j] >= 0 && x[j] < c.size[j];
+    if (copy_out) copy_out[r * c.D + j] = x[j];
+  }
+  if (!ok) {
+    keys[r] = kEmpty;
+    atomicOr(status, kStRange);
+    return;
+  }
+  const uint64_t key = pack_site(c, x);
+  keys[r] = key;
+  const uint64_t entry = WIDE ? key : (key << t.rbits) | static_cast<uint64_t>(r);
+  uint64_t b = home_bucket(t, key);
+  for (uint64_t p = 0; p < t.nbuckets; ++p) {
+    uint64_t* B = t.slots + 4 * b;
+    for (int j = 0; j < 4; ++j) {
+      uint64_t cur = __hip_atomic_load(&B[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (cur == kEmpty) {
+        cur = atomicCAS(reinterpret_cast<unsigned long long*>(&B[j]),
+                        static_cast<unsigned long long>(kEmpty),
+                        static_cast<unsigned long long>(entry));
+        if (cur == kEmpty) {
+          if (WIDE) t.vals[4 * b + j] = static_cast<int32_t>(r);
+          return;
+        }
+      }
+      const bool same = WIDE ? (cur == key) : ((cur >> t.rbits) == key);
+      if (same) {
+        atomicOr(status, kStDup);
+        return;
+      }
+    }
+    b = (b + 1) & (t.nbuckets - 1);
+  }
+  atomicOr(status, kStCap);
+}
+
+// Neighbour probe.  Row y's site is unpacked from rowkeys[y] with `crow`; the
+// site feeding it through offset i is y + o_i - r (VSC) or s*y + o_i (SC),
+// packed with `cin` and looked up in the input table.  Offsets are processed
+// in batches of 8 so that 8 bucket loads per thread are in flight at once.
+template <bool WIDE, bool SC>
+__global__ __launch_bounds__(kBlock) void k_probe(
+    const uint64_t* __restrict__ rowkeys, const DeviceHeader* __restrict__ hdr,
+    int64_t n_cap, Codec crow, Codec cin, Table t, OffsetTable ot,
+    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nblk) {
+  __shared__ int16_t s_off[kMaxK][kMaxD];
+  __shared__ int32_t s_cnt[kBlock / kWave][kMaxK];
+  fill_offsets(ot, s_off);
+  __syncthreads();
+
+  const int64_t n_rows = hdr->n_out;
+  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = y < n_rows;
+  const int wave = threadIdx.x / kWave;
+  int32_t c[kMaxD] = {0, 0, 0, 0};
+  if (valid) {
+    unpack_site(crow, rowkeys[y], c);
+    if (SC)
+      for (int j = 0; j < ot.D; ++j) c[j] *= ot.s[j];
+  }
+
+  constexpr int B = 8;
+  for (int i0 = 0; i0 < ot.K; i0 += B) {
+    uint64_t key[B], bk[B];
+    uint64_t sl[B][4];
+    bool need[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int i = i0 + u;
+      need[u] = valid && i < ot.K && i != ot.centre;
+      key[u] = 0;
+      if (need[u]) {
+        int32_t n[kMaxD];
+        for (int j = 0; j < ot.D; ++j) {
+          n[j] = c[j] + s_off[i][j];
+          need[u] = need[u] && n[j] >= 0 && n[j] < cin.size[j];
+        }
+        if (need[u]) key[u] = pack_site(cin, n);
+      }
+      bk[u] = need[u] ? home_bucket(t, key[u]) : 0;
+      if (need[u]) load_bucket(t, bk[u], sl[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int i = i0 + u;
+      if (i >= ot.K) break;
+      int32_t row = -1;
+      if (need[u]) {
+        row = match_bucket<WIDE>(t, bk[u], sl[u], key[u]);
+        if (row == -2) row = find_from<WIDE>(t, bk[u], key[u]);
+      } else if (valid && i == ot.centre) {
+        row = static_cast<int32_t>(y);
+      }
+      if (y < n_cap) gmap[i * n_cap + y] = row;
+      const uint64_t m = __ballot(row >= 0);
+      if (lane_id() == 0) s_cnt[wave][i] = __popcll(m);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < ot.K; i += kBlock) {
+    int32_t v = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / kWave; ++w) v += s_cnt[w][i];
+    blk_cnt[i * nblk + blockIdx.x] = v;
+  }
+}
+
+// One block per offset: exclusive scan of its block counts, in place; total
+// into totals[i].
+__global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, int64_t nblk,
+                                                 int64_t* __restrict__ totals) {
+  int32_t* c = blk_cnt + blockIdx.x * nblk;
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nblk; base += 4 * kBlock) {
+    int32_t v[4];
+    int64_t sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = base + 4 * threadIdx.x + u;
+      v[u] = k < nblk ? c[k] : 0;
+      sum += v[u];
+    }
+    int64_t tot;
+    int64_t ex = block_excl_scan<int64_t>(sum, &tot) + carry;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = base + 4 * threadIdx.x + u;
+      if (k < nblk) c[k] = static_cast<int32_t>(ex);
+      ex += v[u];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+}
+
+// Compaction of the gather map into the per-offset pair lists.
+__global__ __launch_bounds__(kBlock) void k_compact(
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ blk_base,
+    const int64_t* __restrict__ totals, int K, int64_t n_cap,
+    const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
+    int64_t* __restrict__ pair_off) {
+  __shared__ int64_t s_off[kMaxK + 1];
+  __shared__ int32_t s_w[kBlock / kWave][kMaxK];
+  // pair_off = exclusive prefix of totals (K <= 1024, 4 per thread).
+  {
+    int64_t v[4], sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = 4 * threadIdx.x + u;
+      v[u] = k < K ? totals[k] : 0;
+      sum += v[u];
+    }
+    int64_t tot;
+    int64_t ex = block_excl_scan<int64_t>(sum, &tot);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = 4 * threadIdx.x + u;
+      if (k < K) s_off[k] = ex;
+      ex += v[u];
+    }
+    if (threadIdx.x == 0) s_off[K] = tot;
+  }
+  const int64_t n_rows = hdr->n_out;
+  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = y < n_rows;
+  const int wave = threadIdx.x / kWave;
+  for (int i = 0; i < K; ++i) {
+    const int32_t row = valid ? gmap[i * n_cap + y] : -1;
+    const uint64_t m = __ballot(row >= 0);
+    if (lane_id() == 0) s_w[wave][i] = __popcll(m);
+  }
+  __syncthreads();
+  if (blockIdx.x == 0)
+    for (int k = threadIdx.x; k <= K; k += kBlock) pair_off[k] = s_off[k];
+  for (int i = 0; i < K; ++i) {
+    const int32_t row = valid ? gmap[i * n_cap + y] : -1;
+    const uint64_t m = __ballot(row >= 0);
+    if (row >= 0) {
+      int64_t pos = s_off[i] + blk_base[i * nblk + blockIdx.x] + prefix_popc(m);
+      for (int w = 0; w < wave; ++w) pos += s_w[w][i];
+      pairs[pos] = make_int2(row, static_cast<int32_t>(y));
+    }
+  }
+}
+
+// SC: mark every output site some input feeds.  Output site y with
+// y_j = (x_j - o_j) / s_j when that is a non-negative integer inside the
+// output extent E_j; bit L(y) = lexicographic linear index of y.
+__global__ __launch_bounds__(kBlock) void k_sc_mark(
+    const uint64_t* __restrict__ keys, int64_t N, Codec cin, OffsetTable ot, Extents E,
+    uint32_t* __restrict__ bitmap) {
+  __shared__ int16_t s_off[kMaxK][kMaxD];
+  fill_offsets(ot, s_off);
+  __syncthreads();
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (r >= N) return;
+  const uint64_t key = keys[r];
+  if (key == kEmpty) return;
+  int32_t x[kMaxD];
+  unpack_site(cin, key, x);
+  for (int i = 0; i < ot.K; ++i) {
+    uint32_t L = 0;
+    bool ok = true;
+    for (int j = 0; j < ot.D; ++j) {
+      const int32_t t = x[j] - s_off[i][j];
+      const int32_t q = t / ot.s[j];
+      ok = ok && t >= 0 && q * ot.s[j] == t && q < E.e[j];
+      L = L * static_cast<uint32_t>(E.e[j]) + static_cast<uint32_t>(q);
+    }
+    if (ok) {
+      const uint32_t bit = 1u << (L & 31);
+      if (!(bitmap[L >> 5] & bit)) atomicOr(&bitmap[L >> 5], bit);
+    }
+  }
+}
+
+// Popcount of 1024 bitmap words per block.
+__global__ __launch_bounds__(kBlock) void k_bitsum(const uint32_t* __restrict__ bitmap,
+                                                   uint64_t nwords, uint32_t* __restrict__ bsum) {
+  const uint64_t base = blockIdx.x * 4ull * kBlock + 4ull * threadIdx.x;
+  uint32_t v = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (base + u < nwords) v += __popc(bitmap[base + u]);
+  uint32_t tot;
+  block_excl_scan<uint32_t>(v, &tot);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
+}
+
+// Single block: exclusive scan of the block sums; n_out = total.
+__global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum, int64_t nb,
+                                                    DeviceHeader* __restrict__ hdr) {
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += 4 * kBlock) {
+    uint32_t v[4];
+    int64_t sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = base + 4 * threadIdx.x + u;
+      v[u] = k < nb ? bsum[k] : 0;
+      sum += v[u];
+    }
+    int64_t tot;
+    int64_t ex = block_excl_scan<int64_t>(sum, &tot) + carry;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = base + 4 * threadIdx.x + u;
+      if (k < nb) bsum[k] = static_cast<uint32_t>(ex);
+      ex += v[u];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0) hdr->n_out = carry;
+}
+
+// Emit the marked output sites in rank order: coordinates and packed keys.
+__global__ __launch_bounds__(kBlock) void k_sc_emit(
+    const uint32_t* __restrict__ bitmap, uint64_t nwords, const uint32_t* __restrict__ bbase,
+    Codec cout, Extents E, int32_t* __restrict__ out_coords,
+    uint64_t* __restrict__ out_keys) {
+  const uint64_t base = blockIdx.x * 4ull * kBlock + 4ull * threadIdx.x;
+  uint32_t w[4];
+  uint32_t v = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    w[u] = base + u < nwords ? bitmap[base + u] : 0u;
+    v += __popc(w[u]);
+  }
+  uint32_t tot;
+  uint32_t rank = block_excl_scan<uint32_t>(v, &tot) + bbase[blockIdx.x];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    uint32_t word = w[u];
+    while (word) {
+      const int b = __builtin_ctz(word);
+      word &= word - 1;
+      uint32_t L = static_cast<uint32_t>((base + u) * 32 + b);
+      int32_t yv[kMaxD];
+      for (int j = cout.D - 1; j >= 0; --j) {
+        yv[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
+        L /= static_cast<uint32_t>(E.e[j]);
+      }
+      for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
+      out_keys[rank] = pack_site(cout, yv);
+      ++rank;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host orchestration
+// ---------------------------------------------------------------------------
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    T* p = reinterpret_cast<T*>(base + off);
+    off = align_up(off + count * sizeof(T), 256);
+    return p;
+  }
+};
+
+inline unsigned grid_for(int64_t n, int per = kBlock) {
+  int64_t g = (n + per - 1) / per;
+  return static_cast<unsigned>(g < 1 ? 1 : g);
+}
+
+OffsetTable make_offsets(spconv_rulebook rb) {
+  OffsetTable ot{};
+  ot.K = static_cast<int>(rb->K);
+  ot.D = rb->D;
+  int centre = 0;
+  for (int j = 0; j < rb->D; ++j) {
+    ot.f[j] = rb->f[j];
+    ot.s[j] = rb->s[j];
+    ot.r[j] = rb->kind == SPCONV_VSC ? (rb->f[j] - 1) / 2 : 0;
+    centre = centre * rb->f[j] + ot.r[j];
+  }
+  ot.centre = rb->kind == SPCONV_VSC ? centre : -1;
+  return ot;
+}
+
+// Table geometry: slots = power of two >= 2N (at least 64); the test-only
+// environment variable SPCONV_TEST_HASH_SLOTS forces a (tiny) slot count.
+uint64_t table_slots(int64_t N) {
+  if (const char* e = std::getenv("SPCONV_TEST_HASH_SLOTS")) {
+    uint64_t v = std::strtoull(e, nullptr, 10);
+    uint64_t p = 4;
+    while (p < v) p <<= 1;
+    return p;
+  }
+  uint64_t p = 64;
+  while (p < 2ull * static_cast<uint64_t>(N)) p <<= 1;
+  return p;
+}
+
+struct Transient {
+  void* mem = nullptr;
+  uint64_t* keys = nullptr;
+  Table table{};
+  bool wide = false;
+};
+
+int alloc_transient(spconv_rulebook rb, int64_t N, const Codec& cin, size_t extra_bytes,
+                    Transient* tr, Carver* cv) {
+  const uint64_t slots = table_slots(N);
+  const int rbits = bitlen(static_cast<uint64_t>(N));
+  tr->wide = cin.kbits + rbits > 64;
+  size_t bytes = align_up(N * sizeof(uint64_t), 256) + align_up(slots * 8, 256) +
+                 (tr->wide ? align_up(slots * 4, 256) : 0) + extra_bytes + 256;
+  if (hipMallocAsync(&tr->mem, bytes, rb->stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_ENOMEM;
+  }
+  cv->base = static_cast<char*>(tr->mem);
+  tr->keys = cv->take<uint64_t>(N);
+  tr->table.slots = cv->take<uint64_t>(slots);
+  tr->table.vals = tr->wide ? cv->take<int32_t>(slots) : nullptr;
+  tr->table.nbuckets = slots / 4;
+  tr->table.rbits = tr->wide ? 0 : rbits;
+  return SPCONV_OK;
+}
+
+int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Codec& cin,
+                  Transient& tr, int32_t* copy_out) {
+  const uint64_t slots = tr.table.nbuckets * 4;
+  k_fill_u64<<<grid_for(static_cast<int64_t>(slots / 4), kBlock), kBlock, 0, rb->stream>>>(
+      tr.table.slots, kEmpty, slots);
+  if (N == 0) return SPCONV_OK;
+  if (tr.wide)
+    k_insert<true><<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, cin, tr.table, tr.keys,
+                                                           copy_out, &rb->hdr->status);
+  else
+    k_insert<false><<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, cin, tr.table, tr.keys,
+                                                            copy_out, &rb->hdr->status);
+  return SPCONV_OK;
+}
+
+void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
+                               const Codec& cin, const Transient& tr) {
+  const OffsetTable ot = make_offsets(rb);
+  const unsigned g = static_cast<unsigned>(rb->nblk);
+  if (rb->kind == SPCONV_VSC) {
+    if (tr.wide)
+      k_probe<true, false><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
+                                                         tr.table, ot, rb->gmap, rb->blk_cnt,
+                                                         rb->nblk);
+    else
+      k_probe<false, false><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
+                                                          tr.table, ot, rb->gmap, rb->blk_cnt,
+                                                          rb->nblk);
+  } else {
+    if (tr.wide)
+      k_probe<true, true><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
+                                                        tr.table, ot, rb->gmap, rb->blk_cnt,
+                                                        rb->nblk);
+    else
+      k_probe<false, true><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
+                                                         tr.table, ot, rb->gmap, rb->blk_cnt,
+                                                         rb->nblk);
+  }
+  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
+                                                                  rb->totals);
+  k_compact<<<g, kBlock, 0, rb->stream>>>(rb->gmap, rb->blk_cnt, rb->totals,
+                                          static_cast<int>(rb->K), rb->n_cap, rb->hdr, rb->nblk,
+                                          reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+}
+
+int finish(spconv_rulebook rb, Transient& tr) {
+  if (hipFreeAsync(tr.mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+}  // namespace
+
+int build_vsc(spconv_rulebook rb, const int32_t* coords) {
+  const int64_t N = rb->n_in;
+  const Codec cin = make_codec(rb->D, rb->size);
+  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
+  Transient tr;
+  Carver cv;
+  int st = alloc_transient(rb, N, cin, 0, &tr, &cv);
+  if (st != SPCONV_OK) return st;
+  launch_insert(rb, coords, N, cin, tr, rb->out_coords);
+  if (N > 0) launch_probe_scan_compact(rb, tr.keys, cin, cin, tr);
+  else
+    k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,
+                                         static_cast<uint64_t>(rb->K + 1));
+  return finish(rb, tr);
+}
+
+int build_sc(spconv_rulebook rb, const int32_t* coords) {
+  const int64_t N = rb->n_in;
+  const Codec cin = make_codec(rb->D, rb->size);
+  const Codec cout = make_codec(rb->D, rb->out_size);
+  uint64_t cells = 1;
+  for (int j = 0; j < rb->D; ++j) cells *= static_cast<uint64_t>(rb->out_size[j]);
+  const uint64_t nwords = (cells + 31) / 32;
+  const int64_t nbw = static_cast<int64_t>((nwords + 4 * kBlock - 1) / (4 * kBlock));
+  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, 0);
+  const size_t extra = align_up(nwords * 4, 256) + align_up(nbw * 4, 256) +
+                       align_up(static_cast<size_t>(rb->n_cap) * 8, 256);
+  Transient tr;
+  Carver cv;
+  int st = alloc_transient(rb, N, cin, extra, &tr, &cv);
+  if (st != SPCONV_OK) return st;
+  uint32_t* bitmap = cv.take<uint32_t>(nwords);
+  uint32_t* bsum = cv.take<uint32_t>(nbw);
+  uint64_t* out_keys = cv.take<uint64_t>(rb->n_cap);
+  Extents E{};
+  for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
+  launch_insert(rb, coords, N, cin, tr, nullptr);
+  if (N > 0 && cells > 0) {
+    k_fill_u32<<<grid_for(static_cast<int64_t>(nwords)), kBlock, 0, rb->stream>>>(bitmap, 0u,
+                                                                               nwords);
+    const OffsetTable ot = make_offsets(rb);
+    k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(tr.keys, N, cin, ot, E, bitmap);
+    k_bitsum<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(bitmap, nwords, bsum);
+    k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr);
+    k_sc_emit<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(
+        bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
+    launch_probe_scan_compact(rb, out_keys, cout, cin, tr);
+  } else {
+    k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,
+                                         static_cast<uint64_t>(rb->K + 1));
+  }
+  return finish(rb, tr);
+}
+
+}  // namespace spc

@@ -1,0 +1,81 @@
+"""The C-ABI library on a machine without a GPU: it loads, it exports every
+symbol the header declares, and host-side argument checks return the same
+status codes as the oracle (no compute call is made)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1706_01307_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "spconv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spconv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    names = _declared_symbols()
+    assert len(names) == 9, names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_status_strings():
+    lib = _lib.load()
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        s = lib.spconv_status_string(code).decode()
+        assert s and s != "unknown status"
+    assert lib.spconv_status_string(-99).decode() == "unknown status"
+
+
+def _build_status(kind, D, N, size, f, s):
+    lib = _lib.load()
+    size = np.asarray(size, np.int32)
+    f = np.asarray(f, np.int32)
+    s = np.asarray(s, np.int32)
+    h = ctypes.c_void_p()
+    # coords pointer: a non-null dummy; every case below fails before any
+    # device access
+    dummy = ctypes.c_void_p(16) if N else None
+    return lib.spconv_build_rulebook(kind, D, dummy, N, size.ctypes.data, f.ctypes.data,
+                                     s.ctypes.data, 0, None, ctypes.byref(h)), h.value
+
+
+@pytest.mark.parametrize("kind,size,f,s", [
+    (0, [1, 4, 4], [1, 2, 2], [1, 1, 1]),      # even VSC filter
+    (0, [1, 4, 4], [1, 3, 3], [1, 2, 2]),      # VSC with a stride
+    (1, [1, 4, 4], [3, 3, 3], [1, 2, 2]),      # filter on the sample axis
+    (1, [1, 4, 4], [1, 2, 2], [2, 2, 2]),      # stride on the sample axis
+    (1, [1, 4, 4], [1, 0, 2], [1, 2, 2]),      # zero filter
+    (1, [1, 4, 4], [1, 2, 2], [1, 0, 2]),      # zero stride
+    (1, [1, 4, 70000], [1, 2, 2], [1, 2, 2]),  # extent beyond 65535
+    (0, [0, 4, 4], [1, 3, 3], [1, 1, 1]),      # empty extent
+])
+def test_host_argument_errors_match_oracle(kind, size, f, s):
+    st, h = _build_status(kind, len(size), 1, size, f, s)
+    assert st == _lib.EINVAL and h is None
+    coords = np.zeros((1, len(size)), np.int32)
+    assert oracle.status_of_build(kind, coords, size, f, s) == oracle.EINVAL
+
+
+def test_other_host_errors():
+    assert _build_status(2, 3, 1, [1, 4, 4], [1, 3, 3], [1, 1, 1])[0] == _lib.EINVAL  # kind
+    assert _build_status(0, 5, 1, [1] * 5, [1] * 5, [1] * 5)[0] == _lib.EINVAL       # D
+    assert _build_status(0, 3, -1, [1, 4, 4], [1, 3, 3], [1, 1, 1])[0] == _lib.EINVAL
+    # more offsets than the library supports (K > 1024)
+    assert _build_status(0, 4, 1, [1, 99, 99, 99], [1, 11, 11, 11], [1, 1, 1, 1])[0] == _lib.EINVAL
+    lib = _lib.load()
+    # NULL handle / kind mismatch on the forward side
+    assert lib.spconv_vsc_forward(None, 0, None, None, None, 0, None, 1, 1, None) == _lib.EINVAL
+    assert lib.spconv_rulebook_status(None) == _lib.EINVAL
+    assert lib.spconv_rulebook_query(None, None, None, None, None, None) == _lib.EINVAL
+    lib.spconv_rulebook_destroy(None)
