@@ -119,7 +119,7 @@ def main():
         in_dt = out_dt = _lib.F32
         yt = torch.empty((N, Cout), dtype=torch.float32, device=dev)
     bt = torch.from_numpy(bias).to(dev)
-    ct = torch.from_numpy(wl.coords).to(dev)
+    ct = torch.from_numpy(np.ascontiguousarray(wl.coords)).to(dev).contiguous()
 
     size = np.array(wl.spatial_size, np.int32)
     fa = np.array([1] + [layer.f] * wl.d, np.int32)

@@ -86,7 +86,7 @@ def pen_strokes(n_grids, size=64, n_strokes=8, seed=0, variant="matched",
             [np.full((len(xy), 1), g, dtype=np.int64), xy], axis=1))
     if not out:
         return np.zeros((0, 3), dtype=np.int32)
-    return np.concatenate(out, axis=0).astype(np.int32)
+    return np.ascontiguousarray(np.concatenate(out, axis=0), dtype=np.int32)
 
 
 # ----------------------------------------------------------------------------
@@ -171,7 +171,7 @@ def surfaces(n_samples, size, r_lo, r_hi, seed=0, variant="matched",
             [np.full((len(xyz), 1), s, dtype=np.int64), xyz], axis=1))
     if not out:
         return np.zeros((0, 4), dtype=np.int32)
-    return np.concatenate(out, axis=0).astype(np.int32)
+    return np.ascontiguousarray(np.concatenate(out, axis=0), dtype=np.int32)
 
 
 # ----------------------------------------------------------------------------
