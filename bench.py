@@ -43,6 +43,8 @@ def _args():
     p.add_argument("--variant", default="matched", choices=["matched", "literal"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=20.0)
+    p.add_argument("--calib-copy-mb", type=int, default=0,
+                   help="run one plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
 
 
@@ -142,6 +144,13 @@ def main():
         if evs:
             evs[2].record(stream)
         lib.spconv_rulebook_destroy(h)
+
+    if a.calib_copy_mb:
+        src = torch.ones(a.calib_copy_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # correctness gate on this exact input before timing: a synchronous build
     # must succeed and its rule book must satisfy the VSC invariants

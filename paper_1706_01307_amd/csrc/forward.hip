@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void k_fwd_vec(
     const int col = static_cast<int>(idx - row * C_out);
     float acc = 0.0f;
     for (int i = 0; i < K; ++i) {
-      const int32_t g = gmap[i * n_cap + row];
+      const int32_t g = gmap[i * n_cap + row] - 1;
       if (g < 0) continue;
       const int64_t xb = static_cast<int64_t>(g) * C_in;
       const int64_t wb = static_cast<int64_t>(i) * C_in * C_out + col;
@@ -155,19 +155,32 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
 // r * NCB + cb of the chunk (so a lane ends up owning NCB adjacent columns),
 // same k bytes.  Result: lane l holds rows 4 g + v (v = 0..3), columns
 // r * NCB + cb.
-template <typename TIn, int NCH, int NCB, int RB, typename TOut>
+//
+// Pipeline over the offsets (iteration i): G(i+3) and W^(i+2) are fetched,
+// gathered rows A(i+2) are issued (their gather-map entries G(i+2) arrived
+// one iteration earlier), the MFMAs of offset i run on A(i) and the LDS copy
+// of W^i, and W^(i+1) (fetched one iteration earlier) is written transposed
+// into the other LDS buffer.  One barrier per offset publishes W^(i+1).
+template <typename TIn, int NCH, int NCB, int RB, typename TOut, int KT, bool SKIP = false>
 __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
-    const int32_t* __restrict__ gmap, int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K,
+    const int32_t* __restrict__ gmap, int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K_arg,
     const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
     const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles) {
+  // KT > 0: the offset count is a compile-time constant and the offset loop
+  // is unrolled completely (no loop-carried register hazards).
+  const int K = KT > 0 ? KT : K_arg;
   constexpr int KC = MT<TIn>::KC;
   constexpr int CIN = NCH * KC;
   constexpr int COLS = NCB * 16;
-  constexpr int ROWB = CIN * static_cast<int>(sizeof(TIn));     // bytes of one input row
-  constexpr int LDWB = ROWB + 16;                                // padded LDS row (bytes)
-  constexpr int T = MT<TIn>::T;
-  constexpr int NTILE = (CIN / T) * (COLS / T);                  // transpose tiles per offset
-  constexpr int TPT = (NTILE + 255) / 256;                       // tiles per thread
+  constexpr int ESZ = static_cast<int>(sizeof(TIn));
+  constexpr int ROWB = CIN * ESZ;                 // bytes of one input row
+  constexpr int LDWB = ROWB + 16;                 // padded LDS row of W^T (bytes)
+  // W^T staging tasks: bf16 takes 2 k-rows x 8 columns (packed in pairs),
+  // fp32 1 k-row x 4 columns; each task is one 16-byte load per k-row.
+  constexpr int KPT = ESZ == 2 ? 2 : 1;           // k-rows per task
+  constexpr int NPT = 16 / ESZ;                   // columns per task
+  constexpr int NTASK = (CIN / KPT) * (COLS / NPT);
+  constexpr int TPT = (NTASK + 255) / 256;        // tasks per thread
   constexpr int WAVE_ROWS = RB * 16;
   constexpr int TILE_ROWS = 4 * WAVE_ROWS;
 
@@ -191,65 +204,82 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
                                         static_cast<int>(kBufDword3));
   constexpr uint32_t kOOB = 0x80000000u;   // past any x_bytes < 2^31: reads as zero
 
-  // --- W^i staging: tile (kt, ct) of T k-rows x T columns, transposed in
-  // registers, written as T LDS rows (one per column) of T k-values.
-  u32x4 wreg[TPT][T];
-  auto w_load = [&](int i) {
+  // ---- W^i -> registers (coalesced 16-byte loads)
+  typedef u32x4 WRegs[TPT][KPT];
+  auto w_load = [&](int i, WRegs& wr) {
+    if (i >= K) return;
 #pragma unroll
     for (int q = 0; q < TPT; ++q) {
-      const int t = threadIdx.x + q * 256;
-      if (t < NTILE) {
-        const int kt = t % (CIN / T), ct = t / (CIN / T);
-        const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * T) * C_out + col0 + ct * T;
+      // tasks beyond NTASK (only when NTASK is not a multiple of 256) re-read
+      // task 0 and are never stored
+      const int t0 = threadIdx.x + q * 256;
+      const int t = (NTASK % 256 == 0 || t0 < NTASK) ? t0 : 0;
+      const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
+      const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
 #pragma unroll
-        for (int r = 0; r < T; ++r)
-          wreg[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
-      }
+      for (int r = 0; r < KPT; ++r)
+        wr[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
     }
   };
-  auto w_store = [&](int buf) {
+  // ---- registers -> LDS, transposed: LDS row n holds W^i[k][n] for all k
+  auto w_store = [&](int i, const WRegs& wr) {
+    if (i >= K) return;
+    unsigned char* dst = s_w[i & 1];
 #pragma unroll
     for (int q = 0; q < TPT; ++q) {
       const int t = threadIdx.x + q * 256;
-      if (t < NTILE) {
-        const int kt = t % (CIN / T), ct = t / (CIN / T);
+      if (NTASK % 256 == 0 || t < NTASK) {
+        const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
+        if constexpr (ESZ == 2) {
+          // pack (W[2kt][n], W[2kt+1][n]) into one 32-bit LDS word per column
 #pragma unroll
-        for (int cc = 0; cc < T; ++cc) {
-          u32x4 o;
-          if constexpr (sizeof(TIn) == 2) {
-            // column cc of the 8x8 bf16 tile: element cc of each of 8 rows
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-              const uint32_t lo = (wreg[q][2 * p][cc / 2] >> (16 * (cc % 2))) & 0xffffu;
-              const uint32_t hi = (wreg[q][2 * p + 1][cc / 2] >> (16 * (cc % 2))) & 0xffffu;
-              o[p] = lo | (hi << 16);
-            }
-          } else {
-#pragma unroll
-            for (int p = 0; p < 4; ++p) o[p] = wreg[q][p][cc];
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t a = wr[q][0][j / 2], b = wr[q][1][j / 2];
+            const uint32_t v = (j & 1) ? ((a >> 16) | (b & 0xffff0000u))
+                                       : ((a & 0xffffu) | (b << 16));
+            *reinterpret_cast<uint32_t*>(&dst[(nt * 8 + j) * LDWB + kt * 4]) = v;
           }
-          *reinterpret_cast<u32x4*>(&s_w[buf][(ct * T + cc) * LDWB + kt * 16]) = o;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<uint32_t*>(&dst[(nt * 4 + j) * LDWB + kt * 4]) = wr[q][0][j];
         }
       }
     }
   };
 
-  // --- gather-map rows of this wave: G[i][row0 + 16 b + r]
-  auto g_load = [&](int i, int32_t* g) {
+  // ---- gather-map entries of this wave's rows: G[i][row0 + 16 b + r]
+  typedef int32_t GRegs[RB];
+  // Gather-map entries (1 + input row, 0 = none) through buffer loads: an
+  // offset past the map's range reads 0, so rows past the end and offsets
+  // past K need no branch (a load under a divergent branch would force a
+  // full wait for every load in flight).
+  const uint32_t gmap_bytes = static_cast<uint32_t>(n_cap * 4);
+  auto g_load = [&](int i, GRegs& g) {
+    const int ic = i < K ? i : 0;
+    const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(gmap + static_cast<int64_t>(ic) * n_cap), 0,
+        static_cast<int>(gmap_bytes), static_cast<int>(kBufDword3));
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       const int64_t row = row0 + b * 16 + lr;
-      g[b] = (i < K && row < n_rows) ? gmap[static_cast<int64_t>(i) * n_cap + row] : -1;
+      const uint32_t off = (i < K && row < n_rows) ? static_cast<uint32_t>(row) * 4u : kOOB;
+      g[b] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(gr, off, 0, 0)) - 1;
     }
   };
-  auto a_load = [&](const int32_t* g, u32x4 (*a)[NCH]) {
+  // ---- gathered rows; returns the blocks (bit b) with at least one row
+  typedef u32x4 ARegs[RB][NCH];
+  auto a_load = [&](const GRegs& g, ARegs& a) -> uint32_t {
+    uint32_t pres = 0;
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       const uint32_t base = g[b] >= 0 ? static_cast<uint32_t>(g[b]) * ROWB + lg * 16 : kOOB;
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch)
         a[b][ch] = buf_load16(xr, base == kOOB ? kOOB : base + ch * 64);
+      if (__ballot(g[b] >= 0) != 0) pres |= 1u << b;
     }
+    return pres;
   };
 
   f32x4 acc[RB][NCB];
@@ -258,50 +288,72 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[b][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int32_t g_cur[RB], g_nxt[RB], g_nn[RB];
-  u32x4 a_cur[RB][NCH], a_nxt[RB][NCH];
-
-  w_load(0);
-  w_store(0);
-  g_load(0, g_cur);
-  a_load(g_cur, a_cur);
-  g_load(1, g_nxt);
-  __syncthreads();
-
-  for (int i = 0; i < K; ++i) {
-    const int buf = i & 1;
-    if (i + 1 < K) {
-      a_load(g_nxt, a_nxt);
-      w_load(i + 1);
-    }
-    g_load(i + 2, g_nn);
-
+  auto mma = [&](int i, const ARegs& a, uint32_t pres) {
+    const unsigned char* sw = s_w[i & 1];
 #pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      if (__ballot(g_cur[b] >= 0) == 0) continue;      // whole block lacks offset i
+    for (int ch = 0; ch < NCH; ++ch) {
+      u32x4 bw[NCB];                               // W^i fragments of chunk ch
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
+      for (int cb = 0; cb < NCB; ++cb)
+        bw[cb] = *reinterpret_cast<const u32x4*>(
+            &sw[(lr * NCB + cb) * LDWB + ch * 64 + lg * 16]);
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-          const u32x4 bw = *reinterpret_cast<const u32x4*>(
-              &s_w[buf][(lr * NCB + cb) * LDWB + ch * 64 + lg * 16]);
-          acc[b][cb] = MT<TIn>::mma(a_cur[b][ch], bw, acc[b][cb]);
-        }
+      for (int b = 0; b < RB; ++b) {
+        if (SKIP && !(pres & (1u << b))) continue;   // all 16 rows lack offset i
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+          acc[b][cb] = MT<TIn>::mma(a[b][ch], bw[cb], acc[b][cb]);
       }
     }
+  };
 
-    if (i + 1 < K) w_store(buf ^ 1);
+  // Three rotating register sets (offsets i, i+1, i+2 modulo 3).
+  GRegs g0, g1, g2;
+  ARegs a0, a1, a2;
+  WRegs w0, w1, w2;
+  uint32_t p0 = 0, p1 = 0, p2 = 0;
+
+  // prologue: W^0 into LDS, W^1 in registers, A(0), A(1), G(2) in flight
+  g_load(0, g0);
+  g_load(1, g1);
+  g_load(2, g2);
+  w_load(0, w0);
+  w_load(1, w1);
+  p0 = a_load(g0, a0);
+  p1 = a_load(g1, a1);
+  w_store(0, w0);
+  __syncthreads();
+
+  // iteration i uses set (i mod 3): A(i) in aU, G(i+2) in gF -> A(i+2) into aF,
+  // G(i+3) into gU; W^(i+1) stored from wN, W^(i+2) loaded into wF.
+  auto step = [&](int i, ARegs& aU, uint32_t& pU, ARegs& aF, uint32_t& pF, GRegs& gU,
+                  GRegs& gF, WRegs& wN, WRegs& wF) {
+    if (i >= K) return;
+    // issue order matters: the in-order load counter lets a later wait for
+    // G(i+3) or W^(i+2) leave the gathered rows issued after them in flight
+    g_load(i + 3, gU);
+    w_load(i + 2, wF);
+    pF = a_load(gF, aF);
+    mma(i, aU, pU);
+    w_store(i + 1, wN);
     __syncthreads();
+  };
+  if constexpr (KT > 0) {
 #pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      g_cur[b] = g_nxt[b];
-      g_nxt[b] = g_nn[b];
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) a_cur[b][ch] = a_nxt[b][ch];
+    for (int i = 0; i < KT; i += 3) {
+      step(i, a0, p0, a2, p2, g0, g2, w1, w2);
+      step(i + 1, a1, p1, a0, p0, g1, g0, w2, w0);
+      step(i + 2, a2, p2, a1, p1, g2, g1, w0, w1);
+    }
+  } else {
+    for (int i = 0; i < K; i += 3) {
+      step(i, a0, p0, a2, p2, g0, g2, w1, w2);
+      step(i + 1, a1, p1, a0, p0, g1, g0, w2, w0);
+      step(i + 2, a2, p2, a1, p1, g2, g1, w0, w1);
     }
   }
 
-  // --- epilogue: bias, round once, store NCB adjacent columns per lane-row
+  // ---- epilogue: bias, round once, store NCB adjacent columns per lane-row
   float bv[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
@@ -336,7 +388,9 @@ void launch_mfma(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void
   const int64_t ntiles = (rb->n_cap + kTileRows - 1) / kTileRows;
   const int64_t per = (ntiles + 7) / 8;
   dim3 grid(static_cast<unsigned>(8 * per), static_cast<unsigned>(C_out / (NCB * 16)));
-  k_fwd_mfma<TIn, NCH, NCB, RB, TOut><<<grid, 256, 0, stream>>>(
+  auto kern = rb->K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27>
+                          : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0>;
+  kern<<<grid, 256, 0, stream>>>(
       rb->gmap, rb->n_cap, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x), x_bytes,
       static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_out, ntiles);
 }
@@ -344,8 +398,10 @@ void launch_mfma(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void
 template <typename TIn, int NCH, typename TOut>
 void launch_mfma_ncb(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
                      const float* bias, void* y, int C_out, hipStream_t stream) {
-  if (C_out % 64 == 0)
-    launch_mfma<TIn, NCH, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
+  // wide fp32 rows leave no registers for 4 column blocks
+  constexpr bool four = !(sizeof(TIn) == 4 && NCH >= 6);
+  if (four && C_out % 64 == 0)
+    launch_mfma<TIn, NCH, four ? 4 : 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
   else if (C_out % 32 == 0)
     launch_mfma<TIn, NCH, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
   else
@@ -357,7 +413,8 @@ bool try_mfma(spconv_rulebook rb, int in_dt, const void* x, const void* w, const
               void* y, int C_in, int C_out, hipStream_t stream) {
   if (C_out % 16 != 0) return false;
   const uint64_t xb = static_cast<uint64_t>(rb->n_in) * C_in * (in_dt == SPCONV_BF16 ? 2 : 4);
-  if (xb >= 0x7fffffffull) return false;                 // buffer range is 31-bit here
+  // buffer ranges are kept below 2^31 bytes (inputs and one offset's map row)
+  if (xb >= 0x7fffffffull || static_cast<uint64_t>(rb->n_cap) * 4 >= 0x7fffffffull) return false;
   const uint32_t x_bytes = static_cast<uint32_t>(xb);
   if (in_dt == SPCONV_BF16) {
     switch (C_in) {

@@ -48,8 +48,13 @@ __host__ __device__ inline void unpack_site(const Codec& c, uint64_t k, int32_t*
 
 // ---------------------------------------------------------------------------
 // Open-addressing hash table of sites -> rows.  Slots are grouped in
-// buckets of 4 (32 bytes, one aligned sector of a cache line); a lookup reads
-// one bucket and only moves to the next bucket when all 4 slots are taken.
+// buckets of 4 (32 bytes) and buckets in lines of 4 (128 bytes, one cache
+// line).  The home line of a site is a hash of its 2x2(x2) brick, i.e. of the
+// key with the lowest bit of every spatial coordinate cleared; the bucket
+// inside the line is picked by two of those low bits.  So the sites of one
+// brick share a cache line, and the 3^d neighbours of a site fall in at most
+// 2^d lines, which neighbouring sites share as well.  A lookup reads its home
+// bucket and moves on (linearly) only when all 4 slots are taken.
 // Packed layout: slot = key << rbits | row (one 64-bit word, one CAS per
 // insert).  Wide layout (when key bits + row bits exceed 64): key words in
 // `slots`, rows in `vals`.
@@ -59,6 +64,10 @@ struct Table {
   int32_t* vals;       // wide layout only
   uint64_t nbuckets;   // power of two
   int rbits;           // packed layout: bits of the row field
+  uint64_t brick_mask; // key bits that identify the brick
+  uint64_t lmask1;     // key bit selecting bucket bit 1 (0: none)
+  uint64_t lmask0;     // key bit selecting bucket bit 0 (0: none)
+  int line_shift;      // log2(buckets per line): 2 = brick lines, 0 = plain hash
 };
 
 __device__ __forceinline__ uint64_t mix64(uint64_t k) {
@@ -72,26 +81,37 @@ __device__ __forceinline__ uint64_t mix64(uint64_t k) {
 }
 
 __device__ __forceinline__ uint64_t home_bucket(const Table& t, uint64_t key) {
-  return mix64(key) & (t.nbuckets - 1);
+  const uint64_t nlines = (t.nbuckets >> t.line_shift) ? (t.nbuckets >> t.line_shift) : 1;
+  const uint64_t line = mix64(key & t.brick_mask) & (nlines - 1);
+  const uint64_t local = ((key & t.lmask1) ? 2u : 0u) | ((key & t.lmask0) ? 1u : 0u);
+  return ((line << t.line_shift) | local) & (t.nbuckets - 1);
 }
 
 // Match one bucket (4 slots already loaded) against `key`.
 // Returns the row (>= 0), -1 if the key is absent (an empty slot was seen),
 // or -2 if the bucket is full without the key (continue to the next bucket).
+// Slots fill in order, so the first empty slot ends the search.  Written as a
+// select chain over all 4 slots (last slot first): every loaded slot is used
+// on every path, so the compiler keeps the whole bucket load unconditional.
 template <bool WIDE>
 __device__ __forceinline__ int32_t match_bucket(const Table& t, uint64_t b,
                                                 const uint64_t s[4], uint64_t key) {
+  int32_t res = -2;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (s[j] == kEmpty) return -1;
+  for (int j = 3; j >= 0; --j) {
+    const bool empty = s[j] == kEmpty;
+    bool hit;
+    int32_t row;
     if (WIDE) {
-      if (s[j] == key) return t.vals[4 * b + j];
+      hit = !empty && s[j] == key;
+      row = hit ? t.vals[4 * b + j] : 0;
     } else {
-      if ((s[j] >> t.rbits) == key)
-        return static_cast<int32_t>(s[j] & ((1ull << t.rbits) - 1));
+      hit = !empty && (s[j] >> t.rbits) == key;
+      row = static_cast<int32_t>(s[j] & ((1ull << t.rbits) - 1));
     }
+    res = hit ? row : (empty ? -1 : res);
   }
-  return -2;
+  return res;
 }
 
 __device__ __forceinline__ void load_bucket(const Table& t, uint64_t b, uint64_t s[4]) {
@@ -138,8 +158,8 @@ struct spconv_rulebook_s {
   // carved device pointers
   spc::DeviceHeader* hdr;
   int32_t* out_coords;         // [n_cap][D]
-  int32_t* gmap;               // [K][n_cap] input row per (offset, output row), -1 absent
-  int32_t* blk_cnt;            // [K][nblk] per-block pair counts, then bases
+  int32_t* gmap;               // [K][n_cap] 1 + input row per (offset, output row); 0 = none
+  int32_t* blk_cnt;            // [K][4 nblk] per-wave pair counts, then bases
   int64_t* totals;             // [K] k_i
   int64_t* pair_off;           // [K+1]
   int32_t* pairs;              // [K * n_cap][2]

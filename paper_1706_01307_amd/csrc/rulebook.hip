@@ -7,7 +7,8 @@
 //                into the open-addressing table (flags range errors and
 //                duplicates)
 //   k_probe      per output row and offset, look up the neighbour site ->
-//                gather map G[i][y] (input row or -1); per-block pair counts
+//                gather map G[i][y] (1 + input row, 0 if none); per-block
+//                pair counts
 //   k_scan       per offset, exclusive scan of the block counts -> k_i
 //   k_compact    per-offset stream compaction of G into R_i, ordered by
 //                output row (wave ballot + mbcnt, block prefix in LDS)
@@ -20,6 +21,7 @@
 //                numbers the output rows in lexicographic order
 //   k_probe, k_scan, k_compact as for VSC, probing input site s*y + o.
 #include <cstdlib>
+#include <cstring>
 
 #include "internal.h"
 
@@ -163,15 +165,17 @@ __global__ __launch_bounds__(kBlock) void k_insert(
 
 // Neighbour probe.  Row y's site is unpacked from rowkeys[y] with `crow`; the
 // site feeding it through offset i is y + o_i - r (VSC) or s*y + o_i (SC),
-// packed with `cin` and looked up in the input table.  Offsets are processed
-// in batches of 8 so that 8 bucket loads per thread are in flight at once.
-template <bool WIDE, bool SC>
+// packed with `cin` and looked up in the input table.  Offsets go in batches
+// of 8 and every bucket load of a batch is issued unconditionally (lanes
+// whose neighbour is off the grid read some valid bucket and ignore it), so
+// 8 loads per thread are in flight at once; a load under a divergent branch
+// would instead be waited for on its own.
+template <bool WIDE, bool SC, int D>
 __global__ __launch_bounds__(kBlock) void k_probe(
     const uint64_t* __restrict__ rowkeys, const DeviceHeader* __restrict__ hdr,
     int64_t n_cap, Codec crow, Codec cin, Table t, OffsetTable ot,
-    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nblk) {
+    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nw) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
-  __shared__ int32_t s_cnt[kBlock / kWave][kMaxK];
   fill_offsets(ot, s_off);
   __syncthreads();
 
@@ -179,60 +183,72 @@ __global__ __launch_bounds__(kBlock) void k_probe(
   const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   const bool valid = y < n_rows;
   const int wave = threadIdx.x / kWave;
-  int32_t c[kMaxD] = {0, 0, 0, 0};
-  if (valid) {
-    unpack_site(crow, rowkeys[y], c);
-    if (SC)
-      for (int j = 0; j < ot.D; ++j) c[j] *= ot.s[j];
+  const uint64_t rk = rowkeys[valid ? y : 0];
+  int32_t c[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    c[j] = static_cast<int32_t>((rk >> crow.shift[j]) & crow.fmask[j]);
+    if (SC) c[j] *= ot.s[j];
   }
 
   constexpr int B = 8;
   for (int i0 = 0; i0 < ot.K; i0 += B) {
     uint64_t key[B], bk[B];
     uint64_t sl[B][4];
-    bool need[B];
+    bool inb[B];
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       const int i = i0 + u;
-      need[u] = valid && i < ot.K && i != ot.centre;
-      key[u] = 0;
-      if (need[u]) {
-        int32_t n[kMaxD];
-        for (int j = 0; j < ot.D; ++j) {
-          n[j] = c[j] + s_off[i][j];
-          need[u] = need[u] && n[j] >= 0 && n[j] < cin.size[j];
-        }
-        if (need[u]) key[u] = pack_site(cin, n);
+      const int ic = i < ot.K ? i : ot.K - 1;
+      bool ok = valid && i < ot.K && i != ot.centre;
+      uint64_t k = 0;
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        const int32_t n = c[j] + s_off[ic][j];
+        ok = ok && n >= 0 && n < cin.size[j];
+        k |= static_cast<uint64_t>(static_cast<uint32_t>(n) & cin.fmask[j]) << cin.shift[j];
       }
-      bk[u] = need[u] ? home_bucket(t, key[u]) : 0;
-      if (need[u]) load_bucket(t, bk[u], sl[u]);
+      key[u] = k;
+      inb[u] = ok;
+      bk[u] = home_bucket(t, k);
+      load_bucket(t, bk[u], sl[u]);
+    }
+    int32_t r[B];
+    bool more = false;
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      r[u] = match_bucket<WIDE>(t, bk[u], sl[u], key[u]);
+      more = more || (inb[u] && r[u] == -2);
+    }
+    // Home buckets that were full without the key: one more batched round on
+    // the next bucket for the whole wave, then (very rarely) a serial walk.
+    if (__ballot(more) != 0) {
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        bk[u] = (bk[u] + 1) & (t.nbuckets - 1);
+        load_bucket(t, bk[u], sl[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int32_t r2 = match_bucket<WIDE>(t, bk[u], sl[u], key[u]);
+        r[u] = r[u] == -2 ? r2 : r[u];
+      }
     }
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       const int i = i0 + u;
       if (i >= ot.K) break;
-      int32_t row = -1;
-      if (need[u]) {
-        row = match_bucket<WIDE>(t, bk[u], sl[u], key[u]);
-        if (row == -2) row = find_from<WIDE>(t, bk[u], key[u]);
-      } else if (valid && i == ot.centre) {
-        row = static_cast<int32_t>(y);
-      }
-      if (y < n_cap) gmap[i * n_cap + y] = row;
+      int32_t row = inb[u] ? r[u] : ((valid && i == ot.centre) ? static_cast<int32_t>(y) : -1);
+      if (inb[u] && r[u] == -2) row = find_from<WIDE>(t, bk[u], key[u]);
+      if (y < n_cap) gmap[i * n_cap + y] = row + 1;   // 0 = no active input
       const uint64_t m = __ballot(row >= 0);
-      if (lane_id() == 0) s_cnt[wave][i] = __popcll(m);
+      if (lane_id() == 0)
+        blk_cnt[i * nw + blockIdx.x * (kBlock / kWave) + wave] = __popcll(m);
     }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < ot.K; i += kBlock) {
-    int32_t v = 0;
-#pragma unroll
-    for (int w = 0; w < kBlock / kWave; ++w) v += s_cnt[w][i];
-    blk_cnt[i * nblk + blockIdx.x] = v;
   }
 }
 
-// One block per offset: exclusive scan of its block counts, in place; total
+// One block per offset: exclusive scan of its per-wave counts, in place; total
 // into totals[i].
 __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, int64_t nblk,
                                                  int64_t* __restrict__ totals) {
@@ -260,14 +276,16 @@ __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, 
   if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
-// Compaction of the gather map into the per-offset pair lists.
+// Compaction of the gather map into the per-offset pair lists: every wave
+// writes its pairs of offset i at pair_off[i] + (exclusive count of the waves
+// before it) + (set lanes before it in its ballot), so R_i comes out ordered
+// by output row without any further sorting.
 __global__ __launch_bounds__(kBlock) void k_compact(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ blk_base,
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ wave_base,
     const int64_t* __restrict__ totals, int K, int64_t n_cap,
-    const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
+    const DeviceHeader* __restrict__ hdr, int64_t nw, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ int64_t s_off[kMaxK + 1];
-  __shared__ int32_t s_w[kBlock / kWave][kMaxK];
   // pair_off = exclusive prefix of totals (K <= 1024, 4 per thread).
   {
     int64_t v[4], sum = 0;
@@ -287,24 +305,18 @@ __global__ __launch_bounds__(kBlock) void k_compact(
     }
     if (threadIdx.x == 0) s_off[K] = tot;
   }
-  const int64_t n_rows = hdr->n_out;
-  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
-  const bool valid = y < n_rows;
-  const int wave = threadIdx.x / kWave;
-  for (int i = 0; i < K; ++i) {
-    const int32_t row = valid ? gmap[i * n_cap + y] : -1;
-    const uint64_t m = __ballot(row >= 0);
-    if (lane_id() == 0) s_w[wave][i] = __popcll(m);
-  }
   __syncthreads();
   if (blockIdx.x == 0)
     for (int k = threadIdx.x; k <= K; k += kBlock) pair_off[k] = s_off[k];
+  const int64_t n_rows = hdr->n_out;
+  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = y < n_rows;
+  const int64_t wslot = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
   for (int i = 0; i < K; ++i) {
-    const int32_t row = valid ? gmap[i * n_cap + y] : -1;
+    const int32_t row = valid ? gmap[i * n_cap + y] - 1 : -1;
     const uint64_t m = __ballot(row >= 0);
     if (row >= 0) {
-      int64_t pos = s_off[i] + blk_base[i * nblk + blockIdx.x] + prefix_popc(m);
-      for (int w = 0; w < wave; ++w) pos += s_w[w][i];
+      const int64_t pos = s_off[i] + wave_base[i * nw + wslot] + prefix_popc(m);
       pairs[pos] = make_int2(row, static_cast<int32_t>(y));
     }
   }
@@ -451,8 +463,9 @@ OffsetTable make_offsets(spconv_rulebook rb) {
   return ot;
 }
 
-// Table geometry: slots = power of two >= 2N (at least 64); the test-only
-// environment variable SPCONV_TEST_HASH_SLOTS forces a (tiny) slot count.
+// Table geometry: slots = power of two >= 4N (at least 64), so a home bucket
+// of 4 is rarely full; the test-only environment variable
+// SPCONV_TEST_HASH_SLOTS forces a (tiny) slot count.
 uint64_t table_slots(int64_t N) {
   if (const char* e = std::getenv("SPCONV_TEST_HASH_SLOTS")) {
     uint64_t v = std::strtoull(e, nullptr, 10);
@@ -461,7 +474,7 @@ uint64_t table_slots(int64_t N) {
     return p;
   }
   uint64_t p = 64;
-  while (p < 2ull * static_cast<uint64_t>(N)) p <<= 1;
+  while (p < 4ull * static_cast<uint64_t>(N)) p <<= 1;
   return p;
 }
 
@@ -489,6 +502,28 @@ int alloc_transient(spconv_rulebook rb, int64_t N, const Codec& cin, size_t extr
   tr->table.vals = tr->wide ? cv->take<int32_t>(slots) : nullptr;
   tr->table.nbuckets = slots / 4;
   tr->table.rbits = tr->wide ? 0 : rbits;
+  // brick = the key with the lowest bit of every spatial coordinate cleared;
+  // the first two spatial low bits pick the bucket inside the home line
+  uint64_t low = 0;
+  tr->table.lmask1 = tr->table.lmask0 = 0;
+  int picked = 0;
+  for (int j = 1; j < cin.D; ++j) {
+    if (cin.fmask[j] == 0) continue;
+    const uint64_t bit = 1ull << cin.shift[j];
+    low |= bit;
+    if (picked == 0) tr->table.lmask1 = bit;
+    else if (picked == 1) tr->table.lmask0 = bit;
+    ++picked;
+  }
+  tr->table.brick_mask = ~low;
+  tr->table.line_shift = 2;
+  if (const char* e = std::getenv("SPCONV_HASH_LAYOUT")) {
+    if (std::strcmp(e, "random") == 0) {     // one bucket per line, hash of the whole key
+      tr->table.brick_mask = ~0ull;
+      tr->table.lmask1 = tr->table.lmask0 = 0;
+      tr->table.line_shift = 0;
+    }
+  }
   return SPCONV_OK;
 }
 
@@ -511,29 +546,28 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
                                const Codec& cin, const Transient& tr) {
   const OffsetTable ot = make_offsets(rb);
   const unsigned g = static_cast<unsigned>(rb->nblk);
-  if (rb->kind == SPCONV_VSC) {
-    if (tr.wide)
-      k_probe<true, false><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
-                                                         tr.table, ot, rb->gmap, rb->blk_cnt,
-                                                         rb->nblk);
-    else
-      k_probe<false, false><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
-                                                          tr.table, ot, rb->gmap, rb->blk_cnt,
-                                                          rb->nblk);
-  } else {
-    if (tr.wide)
-      k_probe<true, true><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
-                                                        tr.table, ot, rb->gmap, rb->blk_cnt,
-                                                        rb->nblk);
-    else
-      k_probe<false, true><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin,
-                                                         tr.table, ot, rb->gmap, rb->blk_cnt,
-                                                         rb->nblk);
+  const int64_t nw = rb->nblk * (kBlock / kWave);     // waves (count slots) per offset
+  auto launch = [&](auto kern) {
+    kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin, tr.table, ot,
+                                       rb->gmap, rb->blk_cnt, nw);
+  };
+  const bool sc = rb->kind == SPCONV_SC;
+#define SPC_PROBE(W, S)                                      \
+  switch (rb->D) {                                           \
+    case 2: launch(k_probe<W, S, 2>); break;                 \
+    case 3: launch(k_probe<W, S, 3>); break;                 \
+    default: launch(k_probe<W, S, 4>); break;                \
   }
-  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
+  if (tr.wide) {
+    if (sc) { SPC_PROBE(true, true) } else { SPC_PROBE(true, false) }
+  } else {
+    if (sc) { SPC_PROBE(false, true) } else { SPC_PROBE(false, false) }
+  }
+#undef SPC_PROBE
+  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, nw,
                                                                   rb->totals);
   k_compact<<<g, kBlock, 0, rb->stream>>>(rb->gmap, rb->blk_cnt, rb->totals,
-                                          static_cast<int>(rb->K), rb->n_cap, rb->hdr, rb->nblk,
+                                          static_cast<int>(rb->K), rb->n_cap, rb->hdr, nw,
                                           reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
 }
 
