@@ -142,15 +142,14 @@ __global__ __launch_bounds__(kBlock) void k_insert(
   for (uint64_t p = 0; p < t.nbuckets; ++p) {
     uint64_t* B = t.slots + 4 * b;
     for (int j = 0; j < 4; ++j) {
-      uint64_t cur = __hip_atomic_load(&B[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // CAS straight away (at a quarter load the first try usually wins); a
+      // failed CAS returns the occupant, which decides duplicate or move on
+      const uint64_t cur = atomicCAS(reinterpret_cast<unsigned long long*>(&B[j]),
+                                     static_cast<unsigned long long>(kEmpty),
+                                     static_cast<unsigned long long>(entry));
       if (cur == kEmpty) {
-        cur = atomicCAS(reinterpret_cast<unsigned long long*>(&B[j]),
-                        static_cast<unsigned long long>(kEmpty),
-                        static_cast<unsigned long long>(entry));
-        if (cur == kEmpty) {
-          if (WIDE) t.vals[4 * b + j] = static_cast<int32_t>(r);
-          return;
-        }
+        if (WIDE) t.vals[4 * b + j] = static_cast<int32_t>(r);
+        return;
       }
       const bool same = WIDE ? (cur == key) : ((cur >> t.rbits) == key);
       if (same) {

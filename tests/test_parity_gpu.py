@@ -384,3 +384,14 @@ def test_kind_mismatch():
     st = lib.spconv_sc_forward(rb.handle, 0, x.data_ptr(), w.data_ptr(), None, 0, y.data_ptr(),
                                4, 4, None)
     assert st == spc.EINVAL
+
+
+def test_non_contiguous_coords_through_python_api():
+    """Column-major coordinate tensors are made contiguous before the ABI."""
+    coords = inputs.pen_strokes(2, 32, seed=22, target=120)
+    cf = torch.from_numpy(np.asfortranarray(coords)).cuda()
+    assert not cf.is_contiguous()
+    rb = spc.build_rulebook(spc.VSC, cf, [2, 32, 32], [1, 3, 3])
+    ref = oracle.Rulebook(oracle.VSC, coords, [2, 32, 32], [1, 3, 3])
+    _, pairs = rb.export()
+    np.testing.assert_array_equal(pairs.cpu().numpy(), ref.pairs)
