@@ -27,9 +27,12 @@
 //   * W^i multiplies the input at s*y + i (SC) or y + i - (f-1)/2 (VSC): a
 //     cross-correlation, offsets flattened row-major (last dimension fastest);
 //   * SC output rows are numbered in lexicographic order of the output site;
-//   * pairs inside R_i are ordered by output row;
+//   * pairs inside R_i are ordered along the Z-order (Morton) curve of their
+//     output site: sample index first, then the coordinates' bits level by
+//     level from the most significant, dimension 1 first within a level;
 //   * the bias (optional) is added once at every active output site;
 //   * accumulation is in double, rounded once to the output type (RNE).
+#include <algorithm>
 #include <array>
 #include <cmath>
 #include <cstdint>
@@ -64,6 +67,17 @@ double bf16_to_double(uint16_t b) {
 double load(int dt, const void* p, int64_t idx) {
   if (dt == F32) return static_cast<double>(static_cast<const float*>(p)[idx]);
   return bf16_to_double(static_cast<const uint16_t*>(p)[idx]);
+}
+
+// Z-order comparison of two sites (see the readings above).
+bool zorder_less(const Site& a, const Site& b, int D) {
+  if (a[0] != b[0]) return a[0] < b[0];
+  for (int L = 15; L >= 0; --L)
+    for (int j = 1; j < D; ++j) {
+      const int ba = (a[j] >> L) & 1, bb = (b[j] >> L) & 1;
+      if (ba != bb) return ba < bb;
+    }
+  return false;
 }
 
 // Offset index i (flattened, last dimension fastest) -> per-dimension offset.
@@ -163,13 +177,18 @@ int ref_build(int kind, int D, const int32_t* coords, int64_t N,
   for (int64_t r = 0; r < rb->n_out; ++r)
     for (int j = 0; j < D; ++j) rb->out_coords[r * D + j] = out_sites[r][j];
 
-  // Rule book: for every offset i and output row y (ascending), the input
-  // site feeding y through W^i, if active.
+  // Rule book: for every offset i and every output row y, visited in Z-order
+  // of the output site, the input site feeding y through W^i, if active.
+  std::vector<int64_t> visit(rb->n_out);
+  for (int64_t y = 0; y < rb->n_out; ++y) visit[y] = y;
+  std::sort(visit.begin(), visit.end(), [&](int64_t a, int64_t b) {
+    return zorder_less(out_sites[a], out_sites[b], D);
+  });
   rb->R.resize(rb->K);
   std::vector<int32_t> o(D);
   for (int64_t i = 0; i < rb->K; ++i) {
     unflatten(i, D, rb->f, o.data());
-    for (int64_t y = 0; y < rb->n_out; ++y) {
+    for (int64_t y : visit) {
       Site x{0, 0, 0, 0};
       for (int j = 0; j < D; ++j) {
         if (kind == VSC) x[j] = out_sites[y][j] + o[j] - (f[j] - 1) / 2;
@@ -203,7 +222,7 @@ int ref_query(void* h, int64_t* n_in, int64_t* n_out, int64_t* K,
 }
 
 // Output coordinates (host int32 [n_out][D]) and pairs (host int32 [sum k][2],
-// R_0 first, each R_i ordered by output row).  Either may be NULL.
+// R_0 first, each R_i in Z-order of the output site).  Either may be NULL.
 int ref_export(void* h, int32_t* out_coords, int32_t* pairs) {
   if (!h) return EINVAL_;
   auto* rb = static_cast<Rulebook*>(h);

@@ -85,8 +85,21 @@ def sc_dense(coords, size, f, s, x, w, bias=None):
     return oc.astype(np.int32), out[tuple(oc.T)]
 
 
+def zorder(sites):
+    """Permutation visiting sites along the Z-order curve: sample first, then
+    bit planes from bit 15 down, dimension 1 first inside a plane (a plain
+    lexicographic sort of the bit columns)."""
+    sites = np.asarray(sites, np.int64)
+    cols = [sites[:, 0]]
+    for L in range(15, -1, -1):
+        for j in range(1, sites.shape[1]):
+            cols.append((sites[:, j] >> L) & 1)
+    return np.lexsort(cols[::-1])
+
+
 def rulebook_dense(kind, coords, size, f, s, out_coords):
-    """Per-offset (input row, output row) lists from a dense row grid."""
+    """Per-offset (input row, output row) lists from a dense row grid, each
+    list ordered along the Z-order curve of the output site."""
     size = list(size)
     D = len(size)
     rg = row_grid(coords, size)
@@ -99,7 +112,8 @@ def rulebook_dense(kind, coords, size, f, s, out_coords):
         inb = np.all((x >= 0) & (x < np.array(size)), axis=1)
         rows = np.full(len(out_coords), -1, np.int64)
         rows[inb] = rg[tuple(x[inb].T)]
-        y = np.nonzero(rows >= 0)[0]
+        y = zorder(out_coords)
+        y = y[rows[y] >= 0]
         R.append(np.stack([rows[y], y], axis=1).astype(np.int32))
     return R
 

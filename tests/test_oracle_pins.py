@@ -171,10 +171,40 @@ def test_filter_size_one_is_a_matmul():
     size, coords, x, w, b = _case(rng, 3, 6, 2, 0.2, 5, 7, [1, 1, 1, 1])
     rb = oracle.Rulebook(oracle.VSC, coords, size, [1, 1, 1, 1])
     assert rb.K == 1
-    np.testing.assert_array_equal(rb.pairs, np.stack([np.arange(len(coords))] * 2, 1))
+    np.testing.assert_array_equal(rb.pairs[:, 0], rb.pairs[:, 1])
+    np.testing.assert_array_equal(np.sort(rb.pairs[:, 0]), np.arange(len(coords)))
     y, _ = rb.forward(x, w, b)
     np.testing.assert_allclose(y, x.astype(np.float64) @ w[0].astype(np.float64) + b,
                                rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Pair order inside R_i: the Z-order (Morton) curve of the output site
+# ---------------------------------------------------------------------------
+
+def test_zorder_reference_is_the_textbook_curve():
+    # 4x4 grid, first coordinate most significant inside each bit level
+    sites = np.array([[0, x, y] for x in range(4) for y in range(4)])
+    seq = [tuple(sites[k, 1:]) for k in dense_ref.zorder(sites)]
+    assert seq == [(0, 0), (0, 1), (1, 0), (1, 1), (0, 2), (0, 3), (1, 2), (1, 3),
+                   (2, 0), (2, 1), (3, 0), (3, 1), (2, 2), (2, 3), (3, 2), (3, 3)]
+    # samples come first, whatever the coordinates
+    two = np.array([[1, 0, 0], [0, 3, 3]])
+    assert list(dense_ref.zorder(two)) == [1, 0]
+
+
+def test_rule_book_pairs_follow_zorder_of_output_site():
+    rng = np.random.default_rng(55)
+    size = [2, 16, 16, 16]
+    coords = dense_ref.random_sites(rng, size, 0.1)
+    for kind, f, s in ((oracle.VSC, [1, 3, 3, 3], [1, 1, 1, 1]),
+                       (oracle.SC, [1, 2, 2, 2], [1, 2, 2, 2])):
+        rb = oracle.Rulebook(kind, coords, size, f, s)
+        rank = np.empty(rb.n_out, np.int64)
+        rank[dense_ref.zorder(rb.out_coords)] = np.arange(rb.n_out)
+        for i in range(rb.K):
+            r = rank[rb.offset_pairs(i)[:, 1]]
+            assert np.all(np.diff(r) > 0)
 
 
 # ---------------------------------------------------------------------------
