@@ -27,7 +27,10 @@
  *          (SC) for output site y: a cross-correlation, no filter flip.
  * Rows.    VSC output row r is input row r.  SC output rows are numbered in
  *          lexicographic order of the output site (sample first).
- *          Pairs inside R_i are ordered by output row.
+ *          Pairs inside R_i are ordered along the Z-order (Morton) curve of
+ *          their output site: sample first, then the coordinates' bits level
+ *          by level from the most significant, coordinate 1 first within a
+ *          level (the order the forward walks its output tiles).
  * Memory.  coords, x, w, bias, y are device pointers owned by the caller:
  *          contiguous, row-major, 16-byte aligned.  Host pointers are marked
  *          "host".  A rule book owns its device memory (stream-ordered
@@ -112,7 +115,7 @@ int spconv_rulebook_query(spconv_rulebook rb, int64_t* n_in, int64_t* n_out,
 /* Copy the output sites and the rule book into caller buffers (device).
  *   out_coords  device int32 [n_out][D] or NULL
  *   pairs       device int32 [pair_off[K]][2] or NULL: (input row, output
- *               row), R_0 first, each R_i ordered by output row.
+ *               row), R_0 first, each R_i in Z-order of the output site.
  * Enqueued on `stream` after the build. */
 int spconv_rulebook_export(spconv_rulebook rb, int32_t* out_coords,
                            int32_t* pairs, void* stream);

@@ -165,6 +165,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   bytes += align_up(Kz * 8, 256);
   bytes += align_up((Kz + 1) * 8, 256);
   bytes += align_up(Kz * n_cap * 8, 256);
+  bytes += align_up(n_cap * 4, 256);
   if (hipMallocAsync(&rb->mem, bytes, rb->stream) != hipSuccess) {
     (void)hipGetLastError();
     delete rb;
@@ -185,6 +186,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   rb->totals = reinterpret_cast<int64_t*>(take(Kz * 8));
   rb->pair_off = reinterpret_cast<int64_t*>(take((Kz + 1) * 8));
   rb->pairs = reinterpret_cast<int32_t*>(take(Kz * n_cap * 8));
+  rb->perm = reinterpret_cast<int32_t*>(take(n_cap * 4));
 
   int st = kind == SPCONV_VSC ? build_vsc(rb, coords) : build_sc(rb, coords);
   if (st != SPCONV_OK) {

@@ -158,11 +158,12 @@ struct spconv_rulebook_s {
   // carved device pointers
   spc::DeviceHeader* hdr;
   int32_t* out_coords;         // [n_cap][D]
-  int32_t* gmap;               // [K][n_cap] 1 + input row per (offset, output row); 0 = none
+  int32_t* gmap;               // [K][n_cap] 1 + input row per (offset, schedule position); 0 = none
   int32_t* blk_cnt;            // [K][4 nblk] per-wave pair counts, then bases
   int64_t* totals;             // [K] k_i
   int64_t* pair_off;           // [K+1]
   int32_t* pairs;              // [K * n_cap][2]
+  int32_t* perm;               // [n_cap] schedule: output rows in Z-order of their sites
   int64_t nblk;                // ceil(n_cap / kBlock)
   // host state after synchronisation
   bool synced;
@@ -175,6 +176,12 @@ namespace spc {
 // Launchers (rulebook.hip).  All asynchronous on rb->stream.
 int build_vsc(spconv_rulebook rb, const int32_t* coords);
 int build_sc(spconv_rulebook rb, const int32_t* coords);
+
+// Radix sort (sort.hip).
+size_t radix_sort_scratch_bytes(int64_t n_cap);
+bool radix_sort_pairs(uint64_t* keys, int32_t* vals, uint64_t* keys_tmp, int32_t* vals_tmp,
+                      const DeviceHeader* hdr, int64_t n_cap, int key_bits, void* scratch,
+                      hipStream_t stream);
 
 // Forward (forward.hip).
 int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,

@@ -6,12 +6,15 @@
 //   k_insert     pack every site into an order-preserving key; CAS-insert it
 //                into the open-addressing table (flags range errors and
 //                duplicates)
-//   k_probe      per output row and offset, look up the neighbour site ->
-//                gather map G[i][y] (1 + input row, 0 if none); per-block
-//                pair counts
+//   k_morton + radix sort
+//                output rows in Z-order (Morton) of their sites: the
+//                schedule the probe, the compaction and the forward walk
+//   k_probe      per schedule position and offset, look up the neighbour
+//                site -> gather map G[i][p] (1 + input row, 0 if none);
+//                per-wave pair counts
 //   k_scan       per offset, exclusive scan of the block counts -> k_i
-//   k_compact    per-offset stream compaction of G into R_i, ordered by
-//                output row (wave ballot + mbcnt, block prefix in LDS)
+//   k_compact    per-offset stream compaction of G into R_i, in schedule
+//                order (wave ballot + mbcnt, per-wave prefix)
 // SC (output set = sites with an active input in their receptive field):
 //   k_init, k_insert as above, then
 //   k_sc_mark    every input marks the output sites it feeds in a bitmap
@@ -19,7 +22,8 @@
 //   k_bitsum / k_bitscan / k_sc_emit
 //                rank the marked sites by a popcount prefix sum, which
 //                numbers the output rows in lexicographic order
-//   k_probe, k_scan, k_compact as for VSC, probing input site s*y + o.
+//   k_morton + sort, k_probe, k_scan, k_compact as for VSC, probing input
+//                site s*y + o.
 #include <cstdlib>
 #include <cstring>
 
@@ -171,18 +175,20 @@ __global__ __launch_bounds__(kBlock) void k_insert(
 // would instead be waited for on its own.
 template <bool WIDE, bool SC, int D>
 __global__ __launch_bounds__(kBlock) void k_probe(
-    const uint64_t* __restrict__ rowkeys, const DeviceHeader* __restrict__ hdr,
-    int64_t n_cap, Codec crow, Codec cin, Table t, OffsetTable ot,
-    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nw) {
+    const uint64_t* __restrict__ rowkeys, const int32_t* __restrict__ perm,
+    const DeviceHeader* __restrict__ hdr, int64_t n_cap, Codec crow, Codec cin, Table t,
+    OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nw) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
   fill_offsets(ot, s_off);
   __syncthreads();
 
+  // thread = schedule position p; its output row is perm[p]
   const int64_t n_rows = hdr->n_out;
-  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
-  const bool valid = y < n_rows;
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = p < n_rows;
   const int wave = threadIdx.x / kWave;
-  const uint64_t rk = rowkeys[valid ? y : 0];
+  const int32_t y = valid ? perm[p] : 0;
+  const uint64_t rk = rowkeys[y];
   int32_t c[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) {
@@ -237,9 +243,9 @@ __global__ __launch_bounds__(kBlock) void k_probe(
     for (int u = 0; u < B; ++u) {
       const int i = i0 + u;
       if (i >= ot.K) break;
-      int32_t row = inb[u] ? r[u] : ((valid && i == ot.centre) ? static_cast<int32_t>(y) : -1);
+      int32_t row = inb[u] ? r[u] : ((valid && i == ot.centre) ? y : -1);
       if (inb[u] && r[u] == -2) row = find_from<WIDE>(t, bk[u], key[u]);
-      if (y < n_cap) gmap[i * n_cap + y] = row + 1;   // 0 = no active input
+      if (p < n_cap) gmap[i * n_cap + p] = row + 1;   // 0 = no active input
       const uint64_t m = __ballot(row >= 0);
       if (lane_id() == 0)
         blk_cnt[i * nw + blockIdx.x * (kBlock / kWave) + wave] = __popcll(m);
@@ -277,10 +283,11 @@ __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, 
 
 // Compaction of the gather map into the per-offset pair lists: every wave
 // writes its pairs of offset i at pair_off[i] + (exclusive count of the waves
-// before it) + (set lanes before it in its ballot), so R_i comes out ordered
-// by output row without any further sorting.
+// before it) + (set lanes before it in its ballot), so R_i comes out in
+// schedule (Z-order) order without any further sorting.
 __global__ __launch_bounds__(kBlock) void k_compact(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ wave_base,
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ wave_base,
     const int64_t* __restrict__ totals, int K, int64_t n_cap,
     const DeviceHeader* __restrict__ hdr, int64_t nw, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
@@ -308,15 +315,16 @@ __global__ __launch_bounds__(kBlock) void k_compact(
   if (blockIdx.x == 0)
     for (int k = threadIdx.x; k <= K; k += kBlock) pair_off[k] = s_off[k];
   const int64_t n_rows = hdr->n_out;
-  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
-  const bool valid = y < n_rows;
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = p < n_rows;
+  const int32_t y = valid ? perm[p] : 0;
   const int64_t wslot = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
   for (int i = 0; i < K; ++i) {
-    const int32_t row = valid ? gmap[i * n_cap + y] - 1 : -1;
+    const int32_t row = valid ? gmap[i * n_cap + p] - 1 : -1;
     const uint64_t m = __ballot(row >= 0);
     if (row >= 0) {
       const int64_t pos = s_off[i] + wave_base[i * nw + wslot] + prefix_popc(m);
-      pairs[pos] = make_int2(row, static_cast<int32_t>(y));
+      pairs[pos] = make_int2(row, y);
     }
   }
 }
@@ -425,6 +433,33 @@ __global__ __launch_bounds__(kBlock) void k_sc_emit(
   }
 }
 
+// Forward schedule: Morton code of every output row (sample index on top,
+// then the spatial coordinates' bits interleaved from the most significant),
+// sorted together with the row index.  Consecutive rows of the sorted order
+// are spatially compact, so a tile of them touches a small halo of inputs.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_morton(const uint64_t* __restrict__ rowkeys,
+                                                   const DeviceHeader* __restrict__ hdr,
+                                                   Codec c, int maxb, int sbits,
+                                                   uint64_t* __restrict__ mk,
+                                                   int32_t* __restrict__ mv) {
+  const int64_t y = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (y >= hdr->n_out) return;
+  const uint64_t key = rowkeys[y];
+  uint32_t v[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) v[j] = static_cast<uint32_t>((key >> c.shift[j]) & c.fmask[j]);
+  uint64_t m = 0;
+  for (int L = maxb - 1; L >= 0; --L) {
+#pragma unroll
+    for (int j = 1; j < D; ++j)
+      if (c.fmask[j] >> L) m = (m << 1) | ((v[j] >> L) & 1u);
+  }
+  m |= static_cast<uint64_t>(v[0]) << sbits;
+  mk[y] = m;
+  mv[y] = static_cast<int32_t>(y);
+}
+
 // ---------------------------------------------------------------------------
 // Host orchestration
 // ---------------------------------------------------------------------------
@@ -526,6 +561,39 @@ int alloc_transient(spconv_rulebook rb, int64_t N, const Codec& cin, size_t extr
   return SPCONV_OK;
 }
 
+size_t schedule_bytes(int64_t n_cap) {
+  return 2 * align_up(static_cast<size_t>(n_cap) * 8, 256) +
+         2 * align_up(static_cast<size_t>(n_cap) * 4, 256) +
+         align_up(radix_sort_scratch_bytes(n_cap), 256);
+}
+
+// Output rows in Morton order -> rb->perm (scratch carved from the transient
+// allocation by `cv`).
+void launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow, Carver* cv) {
+  const int64_t n = rb->n_cap;
+  uint64_t* mk = cv->take<uint64_t>(n);
+  uint64_t* mk2 = cv->take<uint64_t>(n);
+  int32_t* mv = cv->take<int32_t>(n);
+  int32_t* mv2 = cv->take<int32_t>(n);
+  void* scratch = cv->take<unsigned char>(radix_sort_scratch_bytes(n));
+  int maxb = 0, sbits = 0;
+  for (int j = 1; j < crow.D; ++j) {
+    const int b = bitlen(crow.fmask[j]);
+    maxb = b > maxb ? b : maxb;
+    sbits += b;
+  }
+  const int total = sbits + bitlen(crow.fmask[0]);
+  const unsigned g = grid_for(n);
+  switch (crow.D) {
+    case 2: k_morton<2><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+    case 3: k_morton<3><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+    default: k_morton<4><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+  }
+  const bool in_tmp = radix_sort_pairs(mk, mv, mk2, mv2, rb->hdr, n, total, scratch, rb->stream);
+  (void)hipMemcpyAsync(rb->perm, in_tmp ? mv2 : mv, static_cast<size_t>(n) * 4,
+                       hipMemcpyDeviceToDevice, rb->stream);
+}
+
 int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Codec& cin,
                   Transient& tr, int32_t* copy_out) {
   const uint64_t slots = tr.table.nbuckets * 4;
@@ -547,8 +615,8 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
   const unsigned g = static_cast<unsigned>(rb->nblk);
   const int64_t nw = rb->nblk * (kBlock / kWave);     // waves (count slots) per offset
   auto launch = [&](auto kern) {
-    kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, rb->n_cap, crow, cin, tr.table, ot,
-                                       rb->gmap, rb->blk_cnt, nw);
+    kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->n_cap, crow, cin,
+                                       tr.table, ot, rb->gmap, rb->blk_cnt, nw);
   };
   const bool sc = rb->kind == SPCONV_SC;
 #define SPC_PROBE(W, S)                                      \
@@ -565,7 +633,7 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
 #undef SPC_PROBE
   k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, nw,
                                                                   rb->totals);
-  k_compact<<<g, kBlock, 0, rb->stream>>>(rb->gmap, rb->blk_cnt, rb->totals,
+  k_compact<<<g, kBlock, 0, rb->stream>>>(rb->gmap, rb->perm, rb->blk_cnt, rb->totals,
                                           static_cast<int>(rb->K), rb->n_cap, rb->hdr, nw,
                                           reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
 }
@@ -583,10 +651,13 @@ int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
   Transient tr;
   Carver cv;
-  int st = alloc_transient(rb, N, cin, 0, &tr, &cv);
+  int st = alloc_transient(rb, N, cin, schedule_bytes(rb->n_cap), &tr, &cv);
   if (st != SPCONV_OK) return st;
   launch_insert(rb, coords, N, cin, tr, rb->out_coords);
-  if (N > 0) launch_probe_scan_compact(rb, tr.keys, cin, cin, tr);
+  if (N > 0) {
+    launch_schedule(rb, tr.keys, cin, &cv);
+    launch_probe_scan_compact(rb, tr.keys, cin, cin, tr);
+  }
   else
     k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,
                                          static_cast<uint64_t>(rb->K + 1));
@@ -603,7 +674,8 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
   const int64_t nbw = static_cast<int64_t>((nwords + 4 * kBlock - 1) / (4 * kBlock));
   k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, 0);
   const size_t extra = align_up(nwords * 4, 256) + align_up(nbw * 4, 256) +
-                       align_up(static_cast<size_t>(rb->n_cap) * 8, 256);
+                       align_up(static_cast<size_t>(rb->n_cap) * 8, 256) +
+                       schedule_bytes(rb->n_cap);
   Transient tr;
   Carver cv;
   int st = alloc_transient(rb, N, cin, extra, &tr, &cv);
@@ -623,6 +695,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr);
     k_sc_emit<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
+    launch_schedule(rb, out_keys, cout, &cv);
     launch_probe_scan_compact(rb, out_keys, cout, cin, tr);
   } else {
     k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,

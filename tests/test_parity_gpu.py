@@ -395,3 +395,29 @@ def test_non_contiguous_coords_through_python_api():
     ref = oracle.Rulebook(oracle.VSC, coords, [2, 32, 32], [1, 3, 3])
     _, pairs = rb.export()
     np.testing.assert_array_equal(pairs.cpu().numpy(), ref.pairs)
+
+
+@pytest.mark.parametrize("dtype,ci", [("bf16", 64), ("f32", 32)])
+def test_halo_overflow_fallback(monkeypatch, dtype, ci):
+    """Halo kernel (opt-in): tiles whose input halo exceeds the LDS budget
+    gather directly instead."""
+    monkeypatch.setenv("SPCONV_FORCE_PATH", "halo")
+    coords = inputs.surfaces(1, 40, 5.0, 16.0, seed=23, target=4000)
+    size = [1, 40, 40, 40]
+    y_ref, yo, absb, _, _ = compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1],
+                                          ci, 64, dtype=dtype, what="halo path")
+    for cap in ("100", "0"):
+        monkeypatch.setenv("SPCONV_TEST_HALO_CAP", cap)
+        y, _, _, _, _ = compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], ci, 64,
+                                      dtype=dtype, what=f"halo cap {cap}")
+        # both routes sum the same products in the same order
+        np.testing.assert_array_equal(y, y_ref)
+
+
+def test_halo_path_forced_sc_and_wide_out(monkeypatch):
+    monkeypatch.setenv("SPCONV_FORCE_PATH", "halo")
+    coords = inputs.surfaces(1, 40, 5.0, 16.0, seed=24, target=4000)
+    compare_layer(spc.VSC, coords, [1, 40, 40, 40], [1, 3, 3, 3], [1, 1, 1, 1], 64, 128,
+                  dtype="bf16", what="forced halo C_out 128")
+    compare_layer(spc.SC, coords, [1, 40, 40, 40], [1, 3, 3, 3], [1, 2, 2, 2], 32, 64,
+                  what="forced halo SC f32")
