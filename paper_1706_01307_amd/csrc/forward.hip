@@ -218,8 +218,10 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
                                         static_cast<int>(kBufDword3));
   constexpr uint32_t kOOB = 0x80000000u;   // past any x_bytes < 2^31: reads as zero
 
-  // ---- W^i -> registers (coalesced 16-byte loads)
+  // ---- W^i -> registers.  Task t = (k-row group kt, column group nt) with nt
+  // fastest, so consecutive lanes read one k-row of the chunk end to end.
   typedef u32x4 WRegs[TPT][KPT];
+  constexpr int NGRP = COLS / NPT;                // column groups per k-row
   auto w_load = [&](int i, WRegs& wr) {
     if (i >= K) return;
 #pragma unroll
@@ -228,14 +230,18 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
       // task 0 and are never stored
       const int t0 = threadIdx.x + q * 256;
       const int t = (NTASK % 256 == 0 || t0 < NTASK) ? t0 : 0;
-      const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
+      const int kt = t / NGRP, nt = t % NGRP;
       const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
 #pragma unroll
       for (int r = 0; r < KPT; ++r)
         wr[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
     }
   };
-  // ---- registers -> LDS, transposed: LDS row n holds W^i[k][n] for all k
+  // ---- registers -> LDS, transposed: one LDS row per column n holding
+  // W^i[k][n] for all k.  Column n = NCB r + cb (lane r's cb-th column) sits
+  // in LDS row 16 cb + r, so the 8 lanes that read one fragment row together
+  // hit 8 consecutive padded rows, i.e. 8 different bank groups.
+  auto w_row = [](int n) { return (n % NCB) * 16 + n / NCB; };
   auto w_store = [&](int i, const WRegs& wr) {
     if (i >= K) return;
     unsigned char* dst = s_w[i & 1];
@@ -243,7 +249,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     for (int q = 0; q < TPT; ++q) {
       const int t = threadIdx.x + q * 256;
       if (NTASK % 256 == 0 || t < NTASK) {
-        const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
+        const int kt = t / NGRP, nt = t % NGRP;
         if constexpr (ESZ == 2) {
           // pack (W[2kt][n], W[2kt+1][n]) into one 32-bit LDS word per column
 #pragma unroll
@@ -251,12 +257,12 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
             const uint32_t a = wr[q][0][j / 2], b = wr[q][1][j / 2];
             const uint32_t v = (j & 1) ? ((a >> 16) | (b & 0xffff0000u))
                                        : ((a & 0xffffu) | (b << 16));
-            *reinterpret_cast<uint32_t*>(&dst[(nt * 8 + j) * LDWB + kt * 4]) = v;
+            *reinterpret_cast<uint32_t*>(&dst[w_row(nt * 8 + j) * LDWB + kt * 4]) = v;
           }
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<uint32_t*>(&dst[(nt * 4 + j) * LDWB + kt * 4]) = wr[q][0][j];
+            *reinterpret_cast<uint32_t*>(&dst[w_row(nt * 4 + j) * LDWB + kt * 4]) = wr[q][0][j];
         }
       }
     }
@@ -309,8 +315,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
       u32x4 bw[NCB];                               // W^i fragments of chunk ch
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb)
-        bw[cb] = *reinterpret_cast<const u32x4*>(
-            &sw[(lr * NCB + cb) * LDWB + ch * 64 + lg * 16]);
+        bw[cb] = *reinterpret_cast<const u32x4*>(&sw[(cb * 16 + lr) * LDWB + ch * 64 + lg * 16]);
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
         if (SKIP && !(pres & (1u << b))) continue;   // all 16 rows lack offset i

@@ -1,29 +1,38 @@
-// Rule-book construction on gfx950 (Section 4 of the paper: hash the active
-// sites, then list the (input row, output row) pairs of every filter offset).
+// Rule-book construction on gfx950 (Section 4 of the paper: map the active
+// sites to rows, then list the (input row, output row) pairs of every filter
+// offset).  Two interchangeable site maps, chosen per build:
 //
-// VSC (output set = input set):
-//   k_init       clear the status word, set n_out = N, empty the table
+// Dense grid (grids of up to 2^29 cells and at most ~64 cells per site):
+//   every cell of the grid holds 1 + row (0 = empty), cells laid out along
+//   the Z-order curve of the sites.
+//   k_zero_u32 + k_grid_scatter   clear, then CAS 1 + r into r's cell
+//                                 (range errors, duplicates)
+//   k_grid_bits / k_bitscan / k_grid_emit
+//                                 occupancy bitmap, its prefix counts, and
+//                                 the rows in cell order = the Z-order
+//                                 schedule the probe, the compaction and the
+//                                 forward walk
+//   k_probe_grid                  per schedule position and offset, one load
+//                                 of the neighbour's cell -> gather map
+//                                 G[i][p] (1 + input row, 0 if none)
+// Hash table (any grid up to 65535 per side):
 //   k_insert     pack every site into an order-preserving key; CAS-insert it
-//                into the open-addressing table (flags range errors and
-//                duplicates)
-//   k_morton + radix sort
-//                output rows in Z-order (Morton) of their sites: the
-//                schedule the probe, the compaction and the forward walk
-//   k_probe      per schedule position and offset, look up the neighbour
-//                site -> gather map G[i][p] (1 + input row, 0 if none);
-//                per-wave pair counts
-//   k_scan       per offset, exclusive scan of the block counts -> k_i
+//                into the open-addressing table (range errors, duplicates)
+//   k_morton + radix sort    the Z-order schedule
+//   k_probe      hash lookups -> G[i][p]
+// Both then run
+//   k_scan       per offset, exclusive scan of the per-wave pair counts
 //   k_compact    per-offset stream compaction of G into R_i, in schedule
 //                order (wave ballot + mbcnt, per-wave prefix)
 // SC (output set = sites with an active input in their receptive field):
-//   k_init, k_insert as above, then
+//   the input sites go into the grid or table as above, then
 //   k_sc_mark    every input marks the output sites it feeds in a bitmap
 //                over the output grid (lexicographic linear index)
 //   k_bitsum / k_bitscan / k_sc_emit
 //                rank the marked sites by a popcount prefix sum, which
 //                numbers the output rows in lexicographic order
-//   k_morton + sort, k_probe, k_scan, k_compact as for VSC, probing input
-//                site s*y + o.
+//   then the schedule of the output sites (an output grid, or Morton codes
+//   and the sort), and probe / scan / compact on input site s*y + o.
 #include <cstdlib>
 #include <cstring>
 
@@ -109,6 +118,16 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, uint64_t n) {
   for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n;
        i += stride)
     p[i] = v;
+}
+
+// Zero n 32-bit words at a 16-byte aligned p: 16-byte stores, then the tail.
+__global__ void k_zero_u32(uint32_t* __restrict__ p, uint64_t n) {
+  const uint64_t n4 = n / 4;
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+  const uint64_t t = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x;
+  uint4* q = reinterpret_cast<uint4*>(p);
+  for (uint64_t i = t; i < n4; i += stride) q[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (t < n - 4 * n4) p[4 * n4 + t] = 0u;
 }
 
 __global__ void k_init_header(DeviceHeader* h, int64_t n_out) {
@@ -427,7 +446,7 @@ __global__ __launch_bounds__(kBlock) void k_sc_emit(
         L /= static_cast<uint32_t>(E.e[j]);
       }
       for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
-      out_keys[rank] = pack_site(cout, yv);
+      if (out_keys) out_keys[rank] = pack_site(cout, yv);
       ++rank;
     }
   }
@@ -461,6 +480,191 @@ __global__ __launch_bounds__(kBlock) void k_morton(const uint64_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// Dense index grid (used when the grid is small enough to hold one int32 per
+// cell; the sites' cells are laid out along the Z-order curve)
+// ---------------------------------------------------------------------------
+// Cell of site (b, c_1..c_d) = b << B | Z(c), where Z interleaves the bits of
+// the spatial coordinates, most significant level first and coordinate 1
+// first inside a level, keeping only the bits a coordinate can have
+// (B = sum_j bits_j).  Walking cells in increasing order is the Z-order of
+// the sites.  M[j] marks the bits of Z that hold coordinate j.
+struct GridGeom {
+  int D;
+  int B;
+  uint32_t M[kMaxD];
+  int32_t size[kMaxD];
+};
+
+// Scatter bits of v into the set positions of m, lowest first.
+__host__ __device__ inline uint32_t deposit(uint32_t v, uint32_t m) {
+  uint32_t r = 0;
+  for (uint32_t bb = 1; m; bb <<= 1) {
+    const uint32_t low = m & (0u - m);
+    if (v & bb) r |= low;
+    m &= m - 1;
+  }
+  return r;
+}
+
+__device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* x) {
+  uint32_t cell = static_cast<uint32_t>(x[0]) << g.B;
+  for (int j = 1; j < g.D; ++j) cell |= deposit(static_cast<uint32_t>(x[j]), g.M[j]);
+  return cell;
+}
+
+// Place input row r at its cell: grid[cell] = r + 1 by compare-and-swap
+// from 0 (empty); finding the cell taken means a duplicate site.  Lanes of
+// a wave hit distinct words, so the swaps do not contend.  Optionally copies
+// the coordinates (VSC output sites) and writes packed keys (SC marking).
+// With `count` set, only the first *count (<= N) rows exist.
+__global__ __launch_bounds__(kBlock) void k_grid_scatter(
+    const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
+    GridGeom g, uint32_t* __restrict__ grid, int32_t* __restrict__ copy_out, Codec ckey,
+    uint64_t* __restrict__ keys_out, uint32_t* __restrict__ status) {
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (r >= N || (count && r >= *count)) return;
+  int32_t x[kMaxD];
+  bool ok = true;
+  for (int j = 0; j < g.D; ++j) {
+    x[j] = coords[r * g.D + j];
+    ok = ok && x[j] >= 0 && x[j] < g.size[j];
+    if (copy_out) copy_out[r * g.D + j] = x[j];
+  }
+  if (!ok) {
+    if (keys_out) keys_out[r] = kEmpty;
+    atomicOr(status, kStRange);
+    return;
+  }
+  if (keys_out) keys_out[r] = pack_site(ckey, x);
+  if (atomicCAS(&grid[grid_cell(g, x)], 0u, static_cast<uint32_t>(r + 1)) != 0u)
+    atomicOr(status, kStDup);
+}
+
+// Occupancy bitmap of the grid, one word (32 cells) per thread, and the
+// number of occupied cells of every block of 256 words.
+__global__ __launch_bounds__(kBlock) void k_grid_bits(const uint32_t* __restrict__ grid,
+                                                      uint64_t cells, uint64_t nwords,
+                                                      uint32_t* __restrict__ bitmap,
+                                                      uint32_t* __restrict__ bsum) {
+  const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
+  uint32_t word = 0;
+  if (w < nwords) {
+    if (32 * w + 32 <= cells) {
+      const uint4* q = reinterpret_cast<const uint4*>(grid + 32 * w);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint4 v = q[k];
+        word |= (v.x ? 1u : 0u) << (4 * k) | (v.y ? 2u : 0u) << (4 * k) |
+                (v.z ? 4u : 0u) << (4 * k) | (v.w ? 8u : 0u) << (4 * k);
+      }
+    } else {
+      for (uint64_t c = 32 * w; c < cells; ++c)
+        word |= (grid[c] ? 1u : 0u) << (c - 32 * w);
+    }
+    bitmap[w] = word;
+  }
+  uint32_t tot;
+  block_excl_scan<uint32_t>(__popc(word), &tot);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
+}
+
+// Rows of the occupied cells in cell order -> perm (the Z-order schedule),
+// one bitmap word per thread; block bases from k_grid_bits + k_bitscan.
+__global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict__ bitmap,
+                                                      uint64_t nwords,
+                                                      const uint32_t* __restrict__ bbase,
+                                                      const uint32_t* __restrict__ grid,
+                                                      int32_t* __restrict__ perm) {
+  const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
+  uint32_t word = w < nwords ? bitmap[w] : 0u;
+  uint32_t tot;
+  uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
+  while (word) {
+    const int b = __builtin_ctz(word);
+    word &= word - 1;
+    perm[rank++] = static_cast<int32_t>(grid[32 * w + b]) - 1;
+  }
+}
+
+constexpr uint32_t kBufDword3 = 0x00020000u;   // gfx9 raw buffer descriptor word 3
+constexpr uint32_t kOOB = 0x80000000u;         // byte offset past every buffer: loads 0
+
+// Neighbour probe on the dense grid.  Thread = schedule position p, output
+// row y = perm[p] with site c (rows_sites[y]).  The input site of offset i
+// is c + o_i - r (VSC) or s*c + o_i (SC); its cell follows from c's cell by
+// one dilated addition per dimension, ((Z_j | ~M_j) + Z(o_ij)) & M_j, which
+// carries through the bits of the other dimensions.  The grid holds 1 + row
+// (0 = empty), which is the gather-map entry as it stands.  Every lookup of
+// a batch is an unconditional buffer load (off-grid neighbours use an offset
+// past the buffer, which reads 0), so the whole batch is in flight at once.
+template <bool SC, int D>
+__global__ __launch_bounds__(kBlock) void k_probe_grid(
+    const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
+    const DeviceHeader* __restrict__ hdr, int64_t n_cap, GridGeom g, OffsetTable ot,
+    const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
+    int32_t* __restrict__ blk_cnt, int64_t nw) {
+  __shared__ int16_t s_off[kMaxK][kMaxD];
+  __shared__ uint32_t s_dil[kMaxK][kMaxD];
+  for (int i = threadIdx.x; i < ot.K; i += blockDim.x) {
+    int rem = i;
+    for (int j = ot.D - 1; j >= 0; --j) {
+      const int o = rem % ot.f[j] - ot.r[j];
+      rem /= ot.f[j];
+      s_off[i][j] = static_cast<int16_t>(o);
+      const uint32_t low = (1u << __popc(g.M[j])) - 1u;
+      s_dil[i][j] = j ? deposit(static_cast<uint32_t>(o) & low, g.M[j]) : 0u;
+    }
+  }
+  __syncthreads();
+
+  const int64_t n_rows = hdr->n_out;
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const bool valid = p < n_rows;
+  const int wave = threadIdx.x / kWave;
+  const int32_t y = valid ? perm[p] : 0;
+  int32_t c[D];
+  uint32_t zc[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    c[j] = valid ? rows_sites[static_cast<int64_t>(y) * D + j] : 0;
+    if (SC) c[j] *= ot.s[j];
+    zc[j] = j ? (deposit(static_cast<uint32_t>(c[j]), g.M[j]) | ~g.M[j]) : 0u;
+  }
+  const uint32_t base = static_cast<uint32_t>(c[0]) << g.B;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(grid), 0, static_cast<int>(cells * 4), static_cast<int>(kBufDword3));
+
+  constexpr int NB = 14;
+  for (int i0 = 0; i0 < ot.K; i0 += NB) {
+    uint32_t gv[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int i = i0 + u;
+      const int ic = i < ot.K ? i : ot.K - 1;
+      bool ok = valid && i < ot.K && i != ot.centre;
+      uint32_t cell = base;
+#pragma unroll
+      for (int j = 1; j < D; ++j) {
+        const int32_t n = c[j] + s_off[ic][j];
+        ok = ok && n >= 0 && n < g.size[j];
+        cell |= (zc[j] + s_dil[ic][j]) & g.M[j];
+      }
+      gv[u] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, ok ? cell * 4 : kOOB, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int i = i0 + u;
+      if (i >= ot.K) break;
+      const int32_t e = (valid && i == ot.centre) ? y + 1 : static_cast<int32_t>(gv[u]);
+      if (p < n_cap) gmap[i * n_cap + p] = e;   // 1 + input row, 0 = none
+      const uint64_t m = __ballot(e != 0);
+      if (lane_id() == 0)
+        blk_cnt[i * nw + blockIdx.x * (kBlock / kWave) + wave] = __popcll(m);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host orchestration
 // ---------------------------------------------------------------------------
 
@@ -480,6 +684,13 @@ struct Carver {
 inline unsigned grid_for(int64_t n, int per = kBlock) {
   int64_t g = (n + per - 1) / per;
   return static_cast<unsigned>(g < 1 ? 1 : g);
+}
+
+void launch_zero(uint32_t* p, uint64_t n, hipStream_t stream) {
+  const uint64_t n4 = n / 4;
+  uint64_t blocks = (n4 + 4 * kBlock - 1) / (4 * kBlock);   // 4 stores per thread
+  blocks = blocks < 1 ? 1 : (blocks > 65536 ? 65536 : blocks);
+  k_zero_u32<<<static_cast<unsigned>(blocks), kBlock, 0, stream>>>(p, n);
 }
 
 OffsetTable make_offsets(spconv_rulebook rb) {
@@ -609,6 +820,16 @@ int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Co
   return SPCONV_OK;
 }
 
+// Per-offset pair counts -> k_i and pair_off; gather map -> pair lists.
+void launch_scan_compact(spconv_rulebook rb) {
+  const int64_t nw = rb->nblk * (kBlock / kWave);
+  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, nw,
+                                                                  rb->totals);
+  k_compact<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
+      rb->gmap, rb->perm, rb->blk_cnt, rb->totals, static_cast<int>(rb->K), rb->n_cap, rb->hdr,
+      nw, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+}
+
 void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
                                const Codec& cin, const Transient& tr) {
   const OffsetTable ot = make_offsets(rb);
@@ -631,11 +852,7 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
     if (sc) { SPC_PROBE(false, true) } else { SPC_PROBE(false, false) }
   }
 #undef SPC_PROBE
-  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, nw,
-                                                                  rb->totals);
-  k_compact<<<g, kBlock, 0, rb->stream>>>(rb->gmap, rb->perm, rb->blk_cnt, rb->totals,
-                                          static_cast<int>(rb->K), rb->n_cap, rb->hdr, nw,
-                                          reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+  launch_scan_compact(rb);
 }
 
 int finish(spconv_rulebook rb, Transient& tr) {
@@ -643,10 +860,183 @@ int finish(spconv_rulebook rb, Transient& tr) {
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
+
+// Dense-grid geometry of a grid with extents `size` (coordinate 0 = sample).
+// False unless it has fewer than kGridMaxCells cells (grid bytes must stay
+// below 2^31 for the probe's buffer loads).
+constexpr uint64_t kGridMaxCells = 1ull << 29;
+
+bool make_grid_geom(int D, const int32_t* size, GridGeom* g, uint64_t* cells) {
+  *g = GridGeom{};
+  g->D = D;
+  int bits[kMaxD] = {0, 0, 0, 0};
+  int maxb = 0;
+  for (int j = 0; j < D; ++j) g->size[j] = size[j];
+  for (int j = 1; j < D; ++j) {
+    bits[j] = bitlen(static_cast<uint64_t>(size[j] - 1));
+    maxb = bits[j] > maxb ? bits[j] : maxb;
+    g->B += bits[j];
+  }
+  // lowest Z bit = level 0 of the last coordinate; coordinate 1 is the most
+  // significant inside every level
+  int pos = 0;
+  for (int L = 0; L < maxb; ++L)
+    for (int j = D - 1; j >= 1; --j)
+      if (bits[j] > L) g->M[j] |= 1u << pos++;
+  if (g->B > 29) return false;
+  *cells = static_cast<uint64_t>(size[0]) << g->B;
+  return *cells < kGridMaxCells;
+}
+
+// Dense grid or hash table for the input sites.  The grid costs about 8
+// bytes of memory traffic per cell (clearing it, deriving its bitmap), the
+// hash table a few hundred nanoseconds of latency-bound work per thousand
+// sites; the grid is taken while it has at most 64 cells per site (plus 4M
+// cells for small inputs).  SPCONV_RULEBOOK=hash / =grid forces a choice.
+bool use_grid(uint64_t cells, int64_t N) {
+  if (const char* e = std::getenv("SPCONV_RULEBOOK")) {
+    if (std::strcmp(e, "hash") == 0) return false;
+    if (std::strcmp(e, "grid") == 0) return true;
+  }
+  return cells <= 64ull * static_cast<uint64_t>(N) + (1ull << 22);
+}
+
+struct GridBufs {
+  uint32_t* grid;     // [cells] 1 + row, 0 = empty
+  uint32_t* bitmap;   // [nwords] occupancy
+  uint32_t* bsum;     // [nbw] occupied cells per 256 words, then their bases
+  uint64_t nwords;
+  int64_t nbw;
+};
+
+size_t grid_bytes(uint64_t cells) {
+  const uint64_t nwords = (cells + 31) / 32;
+  const uint64_t nbw = (nwords + kBlock - 1) / kBlock;
+  return align_up(cells * 4, 256) + align_up(nwords * 4, 256) + align_up(nbw * 4, 256);
+}
+
+GridBufs take_grid(Carver* cv, uint64_t cells) {
+  GridBufs b{};
+  b.nwords = (cells + 31) / 32;
+  b.nbw = static_cast<int64_t>((b.nwords + kBlock - 1) / kBlock);
+  b.grid = cv->take<uint32_t>(cells);
+  b.bitmap = cv->take<uint32_t>(b.nwords);
+  b.bsum = cv->take<uint32_t>(static_cast<size_t>(b.nbw));
+  return b;
+}
+
+// Clear the grid and scatter rows [0, N) (or [0, *count)) into it.
+void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
+                         const int64_t* count, const GridGeom& g, uint64_t cells,
+                         const GridBufs& b, int32_t* copy_out, const Codec& ckey,
+                         uint64_t* keys_out) {
+  launch_zero(b.grid, cells, rb->stream);
+  k_grid_scatter<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out,
+                                                         ckey, keys_out, &rb->hdr->status);
+}
+
+// Z-order schedule from the grid; also sets n_out to the number of occupied
+// cells.
+void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells) {
+  k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
+                                                                        b.bitmap, b.bsum);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr);
+  k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.bitmap, b.nwords,
+                                                                        b.bsum, b.grid, rb->perm);
+}
+
+void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const GridGeom& g,
+                       const GridBufs& b, uint64_t cells) {
+  const OffsetTable ot = make_offsets(rb);
+  const int64_t nw = rb->nblk * (kBlock / kWave);
+  auto launch = [&](auto kern) {
+    kern<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
+        rows_sites, rb->perm, rb->hdr, rb->n_cap, g, ot, b.grid, static_cast<uint32_t>(cells),
+        rb->gmap, rb->blk_cnt, nw);
+  };
+  const bool sc = rb->kind == SPCONV_SC;
+#define SPC_PROBE(S)                                         \
+  switch (rb->D) {                                           \
+    case 2: launch(k_probe_grid<S, 2>); break;               \
+    case 3: launch(k_probe_grid<S, 3>); break;               \
+    default: launch(k_probe_grid<S, 4>); break;              \
+  }
+  if (sc) { SPC_PROBE(true) } else { SPC_PROBE(false) }
+#undef SPC_PROBE
+  launch_scan_compact(rb);
+}
+
+int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
+                   uint64_t cells) {
+  const int64_t N = rb->n_in;
+  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
+  void* mem = nullptr;
+  if (hipMallocAsync(&mem, grid_bytes(cells) + 256, rb->stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_ENOMEM;
+  }
+  Carver cv{static_cast<char*>(mem)};
+  const GridBufs b = take_grid(&cv, cells);
+  launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr);
+  launch_grid_schedule(rb, b, cells);
+  launch_probe_grid(rb, rb->out_coords, g, b, cells);
+  if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+// SC on dense grids: input sites scattered into the input grid; the output
+// set marked in a lexicographic bitmap over the output grid and ranked (rows
+// in lexicographic order); the output sites then scattered into an output
+// grid whose bitmap gives the Z-order schedule.
+int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
+                  uint64_t cells_in, const GridGeom& go, uint64_t cells_out) {
+  const int64_t N = rb->n_in;
+  const Codec cin = make_codec(rb->D, rb->size);
+  const Codec cout = make_codec(rb->D, rb->out_size);
+  uint64_t lex_cells = 1;
+  for (int j = 0; j < rb->D; ++j) lex_cells *= static_cast<uint64_t>(rb->out_size[j]);
+  const uint64_t lwords = (lex_cells + 31) / 32;
+  const int64_t lnbw = static_cast<int64_t>((lwords + 4 * kBlock - 1) / (4 * kBlock));
+  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, 0);
+  const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out) + align_up(lwords * 4, 256) +
+                       align_up(static_cast<size_t>(lnbw) * 4, 256) +
+                       align_up(static_cast<size_t>(N) * 8, 256) + 256;
+  void* mem = nullptr;
+  if (hipMallocAsync(&mem, bytes, rb->stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_ENOMEM;
+  }
+  Carver cv{static_cast<char*>(mem)};
+  const GridBufs bi = take_grid(&cv, cells_in);
+  const GridBufs bo = take_grid(&cv, cells_out);
+  uint32_t* lex = cv.take<uint32_t>(lwords);
+  uint32_t* lsum = cv.take<uint32_t>(static_cast<size_t>(lnbw));
+  uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
+  Extents E{};
+  for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
+  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys);
+  k_fill_u32<<<grid_for(static_cast<int64_t>(lwords)), kBlock, 0, rb->stream>>>(lex, 0u, lwords);
+  const OffsetTable ot = make_offsets(rb);
+  k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, cin, ot, E, lex);
+  k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr);
+  k_sc_emit<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
+                                                                     rb->out_coords, nullptr);
+  launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
+                      cout, nullptr);
+  launch_grid_schedule(rb, bo, cells_out);
+  launch_probe_grid(rb, rb->out_coords, gi, bi, cells_in);
+  if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
 }  // namespace
 
 int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   const int64_t N = rb->n_in;
+  GridGeom g;
+  uint64_t cells = 0;
+  if (N > 0 && make_grid_geom(rb->D, rb->size, &g, &cells) && use_grid(cells, N))
+    return build_vsc_grid(rb, coords, g, cells);
   const Codec cin = make_codec(rb->D, rb->size);
   k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
   Transient tr;
@@ -666,6 +1056,15 @@ int build_vsc(spconv_rulebook rb, const int32_t* coords) {
 
 int build_sc(spconv_rulebook rb, const int32_t* coords) {
   const int64_t N = rb->n_in;
+  {
+    GridGeom gi, go;
+    uint64_t ci = 0, co = 0;
+    bool any_out = true;
+    for (int j = 0; j < rb->D; ++j) any_out = any_out && rb->out_size[j] > 0;
+    if (N > 0 && any_out && make_grid_geom(rb->D, rb->size, &gi, &ci) &&
+        make_grid_geom(rb->D, rb->out_size, &go, &co) && use_grid(ci, N))
+      return build_sc_grid(rb, coords, gi, ci, go, co);
+  }
   const Codec cin = make_codec(rb->D, rb->size);
   const Codec cout = make_codec(rb->D, rb->out_size);
   uint64_t cells = 1;

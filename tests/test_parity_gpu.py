@@ -278,6 +278,50 @@ def test_wide_hash_layout():
                   what="wide keys")
 
 
+RULEBOOK_CASES = [
+    # kind, grid, f, s, C_in, C_out, dtype
+    (0, "surf", [1, 3, 3, 3], [1, 1, 1, 1], 64, 64, "bf16"),
+    (1, "surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 64, "f32"),
+    (1, "surf", [1, 3, 3, 3], [1, 2, 2, 2], 16, 32, "f32"),
+    (0, "pen", [1, 3, 3], [1, 1, 1], 16, 16, "f32"),
+    (1, "pen", [1, 3, 3], [1, 2, 2], 16, 16, "f32"),
+    (0, "aniso", [1, 3, 5, 1], [1, 1, 1, 1], 16, 16, "f32"),
+    (1, "aniso", [1, 2, 3, 1], [1, 2, 1, 1], 16, 16, "f32"),
+]
+
+
+def _rulebook_case_sites(name):
+    if name == "surf":
+        return inputs.surfaces(2, 37, 4.0, 14.0, seed=31, target=2500), [2, 37, 37, 37]
+    if name == "pen":
+        return inputs.pen_strokes(5, 45, seed=32, target=300), [5, 45, 45]
+    rng = np.random.default_rng(33)
+    size = [3, 5, 70, 3]
+    return dense_ref.random_sites(rng, size, 0.3), size
+
+
+@pytest.mark.parametrize("path", ["hash", "grid"])
+@pytest.mark.parametrize("case", range(len(RULEBOOK_CASES)))
+def test_rulebook_paths(monkeypatch, path, case):
+    """Hash-table and dense-grid rule books give the same (oracle) result."""
+    monkeypatch.setenv("SPCONV_RULEBOOK", path)
+    kind, name, f, s, ci, co, dt = RULEBOOK_CASES[case]
+    coords, size = _rulebook_case_sites(name)
+    compare_layer(kind, coords, size, f, s, ci, co, dtype=dt, what=f"{path} {name}")
+
+
+def test_grid_forced_on_sparse_wide_grid(monkeypatch):
+    """The dense grid also serves grids far larger than the site count."""
+    monkeypatch.setenv("SPCONV_RULEBOOK", "grid")
+    rng = np.random.default_rng(34)
+    c = np.unique(rng.integers(0, [2, 1500, 1500], size=(4000, 3)), axis=0).astype(np.int32)
+    c = np.unique(np.concatenate([c, c + [0, 0, 1], c + [0, 1, 1]]), axis=0)
+    c = c[np.all(c < [2, 1500, 1500], axis=1)].astype(np.int32)
+    compare_layer(spc.VSC, c, [2, 1500, 1500], [1, 3, 3], [1, 1, 1], 16, 16, what="grid sparse")
+    compare_layer(spc.SC, c, [2, 1500, 1500], [1, 3, 3], [1, 2, 2], 16, 16,
+                  what="grid sparse SC")
+
+
 def test_permuted_rows():
     """VSC output permutes with its input; SC output does not move."""
     coords = inputs.pen_strokes(4, 32, seed=17, target=150)
@@ -341,8 +385,10 @@ def _status(kind, coords, size, f, s):
         return e.status
 
 
+@pytest.mark.parametrize("path", ["hash", "grid"])
 @pytest.mark.parametrize("kind", [0, 1])
-def test_errors_match_oracle(kind):
+def test_errors_match_oracle(monkeypatch, kind, path):
+    monkeypatch.setenv("SPCONV_RULEBOOK", path)
     f = [1, 3, 3] if kind == spc.VSC else [1, 2, 2]
     s = [1, 1, 1] if kind == spc.VSC else [1, 2, 2]
     dup = np.array([[0, 1, 1], [0, 2, 2], [0, 1, 1]], np.int32)
@@ -356,14 +402,21 @@ def test_errors_match_oracle(kind):
     assert _status(kind, oor, [2, 8, 8], f, s) == spc.ERANGE
 
 
-def test_async_error_reported_by_status():
+@pytest.mark.parametrize("path", ["hash", "grid"])
+def test_async_error_reported_by_status(monkeypatch, path):
+    monkeypatch.setenv("SPCONV_RULEBOOK", path)
     dup = np.array([[0, 1, 1], [0, 1, 1]], np.int32)
     rb = spc.build_rulebook(spc.VSC, _t(dup), [1, 8, 8], [1, 3, 3], sync=False)
     assert rb.status() == spc.EDUP
     rb.close()
+    oor = np.array([[0, 1, 1], [0, 1, 9]], np.int32)
+    rb = spc.build_rulebook(spc.SC, _t(oor), [1, 8, 8], [1, 2, 2], [1, 2, 2], sync=False)
+    assert rb.status() == spc.ERANGE
+    rb.close()
 
 
 def test_table_full_is_reported_not_hung(monkeypatch):
+    monkeypatch.setenv("SPCONV_RULEBOOK", "hash")
     monkeypatch.setenv("SPCONV_TEST_HASH_SLOTS", "8")
     coords = inputs.pen_strokes(1, 32, seed=20, target=100)
     assert len(coords) > 8
