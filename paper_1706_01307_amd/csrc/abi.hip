@@ -161,7 +161,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   size_t bytes = 256;
   bytes += align_up(n_cap * D * 4, 256);
   bytes += align_up(Kz * n_cap * 4, 256);
-  bytes += align_up(Kz * static_cast<size_t>(rb->nblk) * 4 * 4, 256);
+  bytes += align_up(Kz * static_cast<size_t>(rb->nblk) * 4 * 2, 256);
   bytes += align_up(Kz * 8, 256);
   bytes += align_up((Kz + 1) * 8, 256);
   bytes += align_up(Kz * n_cap * 8, 256);
@@ -182,7 +182,8 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   rb->hdr = reinterpret_cast<DeviceHeader*>(take(256));
   rb->out_coords = reinterpret_cast<int32_t*>(take(n_cap * D * 4));
   rb->gmap = reinterpret_cast<int32_t*>(take(Kz * n_cap * 4));
-  rb->blk_cnt = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->nblk) * 4 * 4));
+  rb->blk_cnt = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->nblk) * 4 * 2));
+  rb->wpre = reinterpret_cast<uint32_t*>(rb->blk_cnt + Kz * static_cast<size_t>(rb->nblk));
   rb->totals = reinterpret_cast<int64_t*>(take(Kz * 8));
   rb->pair_off = reinterpret_cast<int64_t*>(take((Kz + 1) * 8));
   rb->pairs = reinterpret_cast<int32_t*>(take(Kz * n_cap * 8));

@@ -34,16 +34,12 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
-// Test and tuning knob: SPCONV_FORCE_PATH=vec runs the vector path, =halo
-// the LDS-staged halo kernel for the shapes it covers (128-byte input rows);
-// by default those shapes take the gathering matrix-core kernel, which is
-// faster on the surface workloads.
-bool force_path(const char* which) {
+// Test knob: SPCONV_FORCE_PATH=vec runs the vector path for shapes the
+// matrix-core kernel covers.
+bool force_vector_path() {
   const char* e = std::getenv("SPCONV_FORCE_PATH");
-  return e && std::strcmp(e, which) == 0;
+  return e && std::strcmp(e, "vec") == 0;
 }
-bool force_vector_path() { return force_path("vec"); }
-bool force_halo_path() { return force_path("halo"); }
 
 constexpr uint32_t kBufDword3 = 0x00020000u;   // gfx9 raw buffer descriptor word 3
 
@@ -160,6 +156,23 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
+// LDS image of W^i transposed: one row per output column of the chunk, ROWB
+// bytes of k.  Rows whose length is a multiple of 128 bytes store 16-byte
+// chunk c at c ^ (row & 7) (measured conflict-free for the fragment reads,
+// where 16 lanes read one chunk of 16 consecutive rows; a 16-byte pad per
+// row, used for other lengths, leaves a 2-way conflict).
+template <int ROWB>
+struct WImage {
+  static constexpr bool kSwz = ROWB % 128 == 0;
+  static constexpr int kRowBytes = kSwz ? ROWB : ROWB + 16;
+  __device__ static int at(int row, int byte) {
+    if constexpr (kSwz)
+      return row * kRowBytes + ((((byte >> 4) ^ (row & 7)) << 4) | (byte & 15));
+    else
+      return row * kRowBytes + byte;
+  }
+};
+
 // Tile of the output handled by one workgroup: 4 waves x RB blocks of 16 rows,
 // NCB blocks of 16 columns (the whole workgroup shares one column chunk).
 //
@@ -188,7 +201,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   constexpr int COLS = NCB * 16;
   constexpr int ESZ = static_cast<int>(sizeof(TIn));
   constexpr int ROWB = CIN * ESZ;                 // bytes of one input row
-  constexpr int LDWB = ROWB + 16;                 // padded LDS row of W^T (bytes)
+  constexpr int LDWB = WImage<ROWB>::kRowBytes;   // LDS row of W^T (bytes)
   // W^T staging tasks: bf16 takes 2 k-rows x 8 columns (packed in pairs),
   // fp32 1 k-row x 4 columns; each task is one 16-byte load per k-row.
   constexpr int KPT = ESZ == 2 ? 2 : 1;           // k-rows per task
@@ -239,8 +252,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   };
   // ---- registers -> LDS, transposed: one LDS row per column n holding
   // W^i[k][n] for all k.  Column n = NCB r + cb (lane r's cb-th column) sits
-  // in LDS row 16 cb + r, so the 8 lanes that read one fragment row together
-  // hit 8 consecutive padded rows, i.e. 8 different bank groups.
+  // in LDS row 16 cb + r, so the lanes that read one fragment chunk together
+  // read 16 consecutive rows (spread over the banks by WImage).
   auto w_row = [](int n) { return (n % NCB) * 16 + n / NCB; };
   auto w_store = [&](int i, const WRegs& wr) {
     if (i >= K) return;
@@ -257,12 +270,13 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
             const uint32_t a = wr[q][0][j / 2], b = wr[q][1][j / 2];
             const uint32_t v = (j & 1) ? ((a >> 16) | (b & 0xffff0000u))
                                        : ((a & 0xffffu) | (b << 16));
-            *reinterpret_cast<uint32_t*>(&dst[w_row(nt * 8 + j) * LDWB + kt * 4]) = v;
+            *reinterpret_cast<uint32_t*>(&dst[WImage<ROWB>::at(w_row(nt * 8 + j), kt * 4)]) = v;
           }
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<uint32_t*>(&dst[w_row(nt * 4 + j) * LDWB + kt * 4]) = wr[q][0][j];
+            *reinterpret_cast<uint32_t*>(&dst[WImage<ROWB>::at(w_row(nt * 4 + j), kt * 4)]) =
+                wr[q][0][j];
         }
       }
     }
@@ -315,7 +329,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
       u32x4 bw[NCB];                               // W^i fragments of chunk ch
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb)
-        bw[cb] = *reinterpret_cast<const u32x4*>(&sw[(cb * 16 + lr) * LDWB + ch * 64 + lg * 16]);
+        bw[cb] = *reinterpret_cast<const u32x4*>(
+            &sw[WImage<ROWB>::at(cb * 16 + lr, ch * 64 + lg * 16)]);
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
         if (SKIP && !(pres & (1u << b))) continue;   // all 16 rows lack offset i
@@ -393,322 +408,6 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
 }
 
 // ---------------------------------------------------------------------------
-// Halo-staged matrix-core path
-// ---------------------------------------------------------------------------
-// Output rows are visited in the rule book's Morton-order schedule (perm), in
-// tiles of 128.  A tile's gather-map entries reference a small set of input
-// rows (its halo, ~1.6-1.9x the tile for surfaces): they are de-duplicated
-// with an LDS hash set, the halo rows are loaded into LDS once, and the
-// offset loop reads its A operands from LDS instead of gathering each input
-// row ~12 times from memory.  Absent neighbours point at an all-zero LDS row.
-// A tile whose halo does not fit (not seen on surfaces in Morton order) is
-// computed with direct gathers instead.
-constexpr int kHaloTR = 128;         // output rows per tile (4 waves x 2 blocks)
-constexpr int kHaloCap = 384;        // halo rows held in LDS
-constexpr int kHaloMaxK = 27;        // offsets whose local maps fit in LDS
-constexpr int kHashSlots = 2048;     // LDS hash set for the de-duplication
-
-template <typename TIn, int NCB, typename TOut, int KT>
-__global__ __launch_bounds__(256, 2) void k_fwd_halo(
-    const int32_t* __restrict__ gmap, int64_t n_cap, const DeviceHeader* __restrict__ hdr,
-    int K_arg, const int32_t* __restrict__ perm, const TIn* __restrict__ x, uint32_t x_bytes,
-    const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_out,
-    int64_t ntiles, int cap) {
-  const int K = KT > 0 ? KT : K_arg;
-  constexpr int ESZ = static_cast<int>(sizeof(TIn));
-  constexpr int ROWB = 128;                      // input row bytes (8 chunks of 16 B)
-  constexpr int CIN = ROWB / ESZ;
-  constexpr int NCH = 2;                         // k-chunks of 64 B per row
-  constexpr int COLS = NCB * 16;
-  constexpr int LDWB = ROWB + 16;
-  constexpr int KPT = ESZ == 2 ? 2 : 1;
-  constexpr int NPT = 16 / ESZ;
-  constexpr int NTASK = (CIN / KPT) * (COLS / NPT);
-  constexpr int TPT = (NTASK + 255) / 256;
-  constexpr int RB = 2;
-  constexpr int ZROW = kHaloCap;                 // index of the all-zero halo row
-  static_assert(NTASK % 256 == 0, "W staging assumes whole tasks per thread");
-
-  __shared__ __attribute__((aligned(16))) unsigned char s_halo[(kHaloCap + 1) * ROWB];
-  __shared__ __attribute__((aligned(16))) unsigned char s_w[2][COLS * LDWB];
-  __shared__ uint16_t s_ll[kHaloMaxK][kHaloTR];
-  __shared__ int32_t s_u[kHaloCap];
-  __shared__ int32_t s_cnt;
-  // the hash set lives in the halo buffer until the halo is loaded
-  int32_t* s_hkey = reinterpret_cast<int32_t*>(s_halo);
-  uint16_t* s_hid = reinterpret_cast<uint16_t*>(s_halo + kHashSlots * 4);
-
-  const int64_t per = gridDim.x / 8;
-  const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
-  if (tile >= ntiles) return;
-
-  const int64_t n_rows = hdr->n_out;
-  const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid % kWave;
-  const int lr = lane % 16, lg = lane / 16;
-  const int64_t p0 = tile * kHaloTR;
-  constexpr uint32_t kOOB = 0x80000000u;
-  const __amdgpu_buffer_rsrc_t xr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<TIn*>(x), 0, static_cast<int>(x_bytes),
-                                        static_cast<int>(kBufDword3));
-
-  // ---- phase 1: gather-map entries of the tile -> de-duplicated local ids
-  for (int q = tid; q < kHashSlots; q += 256) s_hkey[q] = 0;
-  if (tid == 0) s_cnt = 0;
-  const int pme = tid % kHaloTR;                        // this thread's tile position
-  const int64_t pos = p0 + pme;
-  const int32_t myrow = pos < n_rows ? perm[pos] : -1;
-  constexpr int EPT = (kHaloMaxK + 1) / 2;              // offsets per thread (2 threads/row)
-  int32_t ge[EPT];
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int i = tid / kHaloTR + 2 * q;
-    ge[q] = (i < K && myrow >= 0) ? gmap[static_cast<int64_t>(i) * n_cap + pos] : 0;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int32_t g = ge[q];
-    if (g == 0) continue;
-    uint32_t h = (static_cast<uint32_t>(g) * 2654435761u) >> 21;
-    for (int probe = 0; probe < kHashSlots; ++probe) {
-      const int32_t old = atomicCAS(&s_hkey[h], 0, g);
-      if (old == 0) {
-        const int id = atomicAdd(&s_cnt, 1);
-        s_hid[h] = static_cast<uint16_t>(id < kHaloCap ? id : kHaloCap);
-        if (id < kHaloCap) s_u[id] = g - 1;
-        break;
-      }
-      if (old == g) break;
-      h = (h + 1) & (kHashSlots - 1);
-    }
-  }
-  __syncthreads();
-  const int count = s_cnt;
-  const bool fits = count <= cap;
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int i = tid / kHaloTR + 2 * q;
-    if (i >= K) continue;
-    const int32_t g = ge[q];
-    uint16_t ll = ZROW;
-    if (g != 0 && fits) {
-      uint32_t h = (static_cast<uint32_t>(g) * 2654435761u) >> 21;
-      while (s_hkey[h] != g) h = (h + 1) & (kHashSlots - 1);
-      ll = s_hid[h];
-    }
-    s_ll[i][pme] = ll;
-  }
-  __syncthreads();
-
-  // ---- phase 2: halo rows -> LDS (16-byte chunk c of row r stored at chunk
-  // c ^ (r & 7), so that the 16 rows an A-operand load reads spread over the
-  // banks); row ZROW is all zeros
-  if (fits) {
-    constexpr int PER = (kHaloCap * 8 + 255) / 256;
-    u32x4 v[PER];
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int c = tid + q * 256;
-      const int r = c / 8;
-      const uint32_t off = r < count ? static_cast<uint32_t>(s_u[r]) * ROWB + (c % 8) * 16 : kOOB;
-      v[q] = buf_load16(xr, off);
-    }
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int c = tid + q * 256;
-      const int r = c / 8;
-      if (r < count)
-        *reinterpret_cast<u32x4*>(&s_halo[r * ROWB + (((c % 8) ^ (r & 7)) * 16)]) = v[q];
-    }
-    if (tid < 8)
-      *reinterpret_cast<u32x4*>(&s_halo[ZROW * ROWB + tid * 16]) = u32x4{0u, 0u, 0u, 0u};
-  }
-  __syncthreads();
-
-  // ---- phase 3: offsets x column chunks on the matrix cores
-  typedef u32x4 WRegs[TPT][KPT];
-  for (int col0 = 0; col0 < C_out; col0 += COLS) {
-    auto w_load = [&](int i, WRegs& wr) {
-      if (i >= K) return;
-#pragma unroll
-      for (int q = 0; q < TPT; ++q) {
-        const int t = tid + q * 256;
-        const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
-        const TIn* src =
-            w + (static_cast<int64_t>(i) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
-#pragma unroll
-        for (int r = 0; r < KPT; ++r)
-          wr[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
-      }
-    };
-    // LDS row of output column n: (n % NCB) * 16 + n / NCB, so that the 16
-    // lanes reading one column block touch 16 consecutive padded rows
-    auto w_store = [&](int i, const WRegs& wr) {
-      if (i >= K) return;
-      unsigned char* dst = s_w[i & 1];
-#pragma unroll
-      for (int q = 0; q < TPT; ++q) {
-        const int t = tid + q * 256;
-        const int kt = t % (CIN / KPT), nt = t / (CIN / KPT);
-        if constexpr (ESZ == 2) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int n = nt * 8 + j;
-            const uint32_t a = wr[q][0][j / 2], b = wr[q][1][j / 2];
-            const uint32_t val = (j & 1) ? ((a >> 16) | (b & 0xffff0000u))
-                                         : ((a & 0xffffu) | (b << 16));
-            *reinterpret_cast<uint32_t*>(&dst[((n % NCB) * 16 + n / NCB) * LDWB + kt * 4]) = val;
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int n = nt * 4 + j;
-            *reinterpret_cast<uint32_t*>(&dst[((n % NCB) * 16 + n / NCB) * LDWB + kt * 4]) =
-                wr[q][0][j];
-          }
-        }
-      }
-    };
-
-    f32x4 acc[RB][NCB];
-#pragma unroll
-    for (int b = 0; b < RB; ++b)
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) acc[b][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // A operands of offset i for this wave's blocks, read from the LDS halo
-    // (they do not depend on W, so offset i+1's are read while offset i's
-    // MFMAs run); bit b of the result marks blocks with at least one row.
-    typedef u32x4 ARegs[RB][NCH];
-    auto a_read = [&](int i, ARegs& a) -> uint32_t {
-      uint32_t pres = 0;
-      if (i >= K) return 0;
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const int L = s_ll[i][wave * 32 + b * 16 + lr];
-        if (__ballot(L != ZROW) != 0) pres |= 1u << b;
-#pragma unroll
-        for (int ch = 0; ch < NCH; ++ch)
-          a[b][ch] = *reinterpret_cast<const u32x4*>(
-              &s_halo[L * ROWB + (((ch * 4 + lg) ^ (L & 7)) * 16)]);
-      }
-      return pres;
-    };
-    auto mma = [&](int i, const ARegs& a, uint32_t pres) {
-      const unsigned char* sw = s_w[i & 1];
-      u32x4 bw[NCH][NCB];
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-          bw[ch][cb] = *reinterpret_cast<const u32x4*>(
-              &sw[(cb * 16 + lr) * LDWB + ch * 64 + lg * 16]);
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-        for (int b = 0; b < RB; ++b) {
-          if (!(pres & (1u << b))) continue;    // all 16 rows lack offset i
-#pragma unroll
-          for (int cb = 0; cb < NCB; ++cb)
-            acc[b][cb] = MT<TIn>::mma(a[b][ch], bw[ch][cb], acc[b][cb]);
-        }
-    };
-    // Direct gathers, for a tile whose halo does not fit in LDS.
-    auto a_gather = [&](int i, ARegs& a) -> uint32_t {
-      uint32_t pres = 0;
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        const int64_t ps = p0 + wave * 32 + b * 16 + lr;
-        const int32_t g = ps < n_rows ? gmap[static_cast<int64_t>(i) * n_cap + ps] - 1 : -1;
-        if (__ballot(g >= 0) != 0) pres |= 1u << b;
-#pragma unroll
-        for (int ch = 0; ch < NCH; ++ch)
-          a[b][ch] = buf_load16(xr, g >= 0 ? static_cast<uint32_t>(g) * ROWB + ch * 64 + lg * 16
-                                           : kOOB);
-      }
-      return pres;
-    };
-
-    WRegs w0, w1, w2;
-    w_load(0, w0);
-    w_load(1, w1);
-    w_store(0, w0);
-    __syncthreads();
-    if (fits) {
-      ARegs a0, a1;
-      uint32_t q0 = a_read(0, a0), q1 = 0;
-      // step i: W^(i+2) fetched, A(i+1) read from LDS, MFMAs of offset i,
-      // W^(i+1) published for the next step
-      auto step = [&](int i, ARegs& aU, uint32_t qU, ARegs& aN, uint32_t& qN, WRegs& wN,
-                      WRegs& wF) {
-        if (i >= K) return;
-        w_load(i + 2, wF);
-        qN = a_read(i + 1, aN);
-        mma(i, aU, qU);
-        w_store(i + 1, wN);
-        __syncthreads();
-      };
-      if constexpr (KT > 0) {
-#pragma unroll
-        for (int i = 0; i < KT; i += 6) {
-          step(i, a0, q0, a1, q1, w1, w2);
-          step(i + 1, a1, q1, a0, q0, w2, w0);
-          step(i + 2, a0, q0, a1, q1, w0, w1);
-          step(i + 3, a1, q1, a0, q0, w1, w2);
-          step(i + 4, a0, q0, a1, q1, w2, w0);
-          step(i + 5, a1, q1, a0, q0, w0, w1);
-        }
-      } else {
-        for (int i = 0; i < K; i += 6) {
-          step(i, a0, q0, a1, q1, w1, w2);
-          step(i + 1, a1, q1, a0, q0, w2, w0);
-          step(i + 2, a0, q0, a1, q1, w0, w1);
-          step(i + 3, a1, q1, a0, q0, w1, w2);
-          step(i + 4, a0, q0, a1, q1, w2, w0);
-          step(i + 5, a1, q1, a0, q0, w0, w1);
-        }
-      }
-    } else {
-      // rare: gathers waited for in place
-      auto dstep = [&](int i, WRegs& wN, WRegs& wF) {
-        if (i >= K) return;
-        w_load(i + 2, wF);
-        ARegs a;
-        const uint32_t q = a_gather(i, a);
-        mma(i, a, q);
-        w_store(i + 1, wN);
-        __syncthreads();
-      };
-      for (int i = 0; i < K; i += 3) {
-        dstep(i, w1, w2);
-        dstep(i + 1, w2, w0);
-        dstep(i + 2, w0, w1);
-      }
-    }
-
-    // ---- epilogue: bias, one rounding, NCB adjacent columns per lane-row
-    float bv[NCB];
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t ps = p0 + wave * 32 + b * 16 + lg * 4 + v;
-        if (ps < n_rows) {
-          const int64_t row = perm[ps];
-          float o[NCB];
-#pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
-          OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
-        }
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Dispatch
 // ---------------------------------------------------------------------------
 // Row blocks per wave: fewer when the input rows are wide, so that the two
@@ -746,52 +445,10 @@ void launch_mfma_ncb(spconv_rulebook rb, const void* x, uint32_t x_bytes, const 
     launch_mfma<TIn, NCH, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
 }
 
-// Rows a tile's halo may hold; the test-only SPCONV_TEST_HALO_CAP lowers it
-// to exercise the direct-gather fallback of tiles whose halo does not fit.
-int halo_cap() {
-  if (const char* e = std::getenv("SPCONV_TEST_HALO_CAP")) {
-    const int v = std::atoi(e);
-    if (v >= 0 && v < kHaloCap) return v;
-  }
-  return kHaloCap;
-}
-
-template <typename TIn, int NCB, typename TOut>
-void launch_halo(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
-                 const float* bias, void* y, int C_out, hipStream_t stream) {
-  const int64_t ntiles = (rb->n_cap + kHaloTR - 1) / kHaloTR;
-  const int64_t per = (ntiles + 7) / 8;
-  auto kern = rb->K == 27 ? k_fwd_halo<TIn, NCB, TOut, 27> : k_fwd_halo<TIn, NCB, TOut, 0>;
-  kern<<<static_cast<unsigned>(8 * per), 256, 0, stream>>>(
-      rb->gmap, rb->n_cap, rb->hdr, static_cast<int>(rb->K), rb->perm,
-      static_cast<const TIn*>(x), x_bytes, static_cast<const TIn*>(w), bias,
-      static_cast<TOut*>(y), C_out, ntiles, halo_cap());
-}
-
-// Halo path: one 128-byte input row (bf16 x 64 or fp32 x 32), at most 27
-// offsets, C_out a multiple of 64 (columns are walked in chunks of 64).
-template <typename TOut>
-bool try_halo(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
-              void* y, int C_in, int C_out, hipStream_t stream) {
-  if (!rb->perm || rb->K > kHaloMaxK || C_out % 64 != 0) return false;
-  const uint64_t xb = static_cast<uint64_t>(rb->n_in) * 128;
-  if (xb >= 0x7fffffffull) return false;
-  if (in_dt == SPCONV_BF16 && C_in == 64)
-    launch_halo<uint16_t, 4, TOut>(rb, x, static_cast<uint32_t>(xb), w, bias, y, C_out, stream);
-  else if (in_dt == SPCONV_F32 && C_in == 32)
-    launch_halo<float, 4, TOut>(rb, x, static_cast<uint32_t>(xb), w, bias, y, C_out, stream);
-  else
-    return false;
-  return true;
-}
-
 template <typename TOut>
 bool try_mfma(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
               void* y, int C_in, int C_out, hipStream_t stream) {
   if (C_out % 16 != 0) return false;
-  if (force_halo_path() &&
-      try_halo<TOut>(rb, in_dt, x, w, bias, y, C_in, C_out, stream))
-    return true;
   const uint64_t xb = static_cast<uint64_t>(rb->n_in) * C_in * (in_dt == SPCONV_BF16 ? 2 : 4);
   // buffer ranges are kept below 2^31 bytes (inputs and one offset's map row)
   if (xb >= 0x7fffffffull || static_cast<uint64_t>(rb->n_cap) * 4 >= 0x7fffffffull) return false;

@@ -22,6 +22,7 @@ constexpr int kMaxK = 1024;          // filter offsets per layer
 constexpr uint64_t kEmpty = ~0ull;   // empty hash slot
 constexpr int kBlock = 256;          // rows per rule-book block (4 waves)
 
+
 // ---------------------------------------------------------------------------
 // Order-preserving site codec: coordinate j occupies `bits[j]` bits at
 // `shift[j]`, coordinate 0 (sample) in the high bits, so integer order of
@@ -159,7 +160,8 @@ struct spconv_rulebook_s {
   spc::DeviceHeader* hdr;
   int32_t* out_coords;         // [n_cap][D]
   int32_t* gmap;               // [K][n_cap] 1 + input row per (offset, schedule position); 0 = none
-  int32_t* blk_cnt;            // [K][4 nblk] per-wave pair counts, then bases
+  int32_t* blk_cnt;            // [K][nblk] per-block pair counts, then bases
+  uint32_t* wpre;              // [K][nblk] per-wave prefixes inside a block (bytes)
   int64_t* totals;             // [K] k_i
   int64_t* pair_off;           // [K+1]
   int32_t* pairs;              // [K * n_cap][2]

@@ -5,8 +5,9 @@
 // Dense grid (grids of up to 2^29 cells and at most ~64 cells per site):
 //   every cell of the grid holds 1 + row (0 = empty), cells laid out along
 //   the Z-order curve of the sites.
-//   k_zero_u32 + k_grid_scatter   clear, then CAS 1 + r into r's cell
-//                                 (range errors, duplicates)
+//   k_zero_u32 + k_grid_scatter   clear, then store 1 + r into r's cell
+//                                 (range errors; duplicates by CAS, or for
+//                                 VSC by the occupied-cell count)
 //   k_grid_bits / k_bitscan / k_grid_emit
 //                                 occupancy bitmap, its prefix counts, and
 //                                 the rows in cell order = the Z-order
@@ -106,6 +107,25 @@ __device__ void fill_offsets(const OffsetTable& ot, int16_t (*s_off)[kMaxD]) {
   }
 }
 
+// Per-block pair counts.  During a probe every wave leaves its count for
+// offset i in s_cnt[i][wave]; at the end the block writes, per offset, its
+// total (scanned later into the block's base) and the exclusive prefixes of
+// waves 1..3 packed in bytes 0..2 (each at most 192).
+__device__ void publish_counts(const uint8_t (*s_cnt)[kBlock / kWave], int K,
+                               int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre,
+                               int64_t nblk) {
+  __syncthreads();
+  for (int i = threadIdx.x; i < K; i += kBlock) {
+    const uint32_t c0 = s_cnt[i][0], c1 = s_cnt[i][1], c2 = s_cnt[i][2], c3 = s_cnt[i][3];
+    blk_cnt[i * nblk + blockIdx.x] = static_cast<int32_t>(c0 + c1 + c2 + c3);
+    wpre[i * nblk + blockIdx.x] = c0 | ((c0 + c1) << 8) | ((c0 + c1 + c2) << 16);
+  }
+}
+
+__device__ __forceinline__ uint32_t wave_prefix(uint32_t packed, int wave) {
+  return wave ? (packed >> (8 * (wave - 1))) & 0xffu : 0u;
+}
+
 __global__ void k_fill_u64(uint64_t* __restrict__ p, uint64_t v, uint64_t n) {
   uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
   for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n;
@@ -196,8 +216,10 @@ template <bool WIDE, bool SC, int D>
 __global__ __launch_bounds__(kBlock) void k_probe(
     const uint64_t* __restrict__ rowkeys, const int32_t* __restrict__ perm,
     const DeviceHeader* __restrict__ hdr, int64_t n_cap, Codec crow, Codec cin, Table t,
-    OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, int64_t nw) {
+    OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt,
+    uint32_t* __restrict__ wpre, int64_t nblk) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
+  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
   fill_offsets(ot, s_off);
   __syncthreads();
 
@@ -266,14 +288,14 @@ __global__ __launch_bounds__(kBlock) void k_probe(
       if (inb[u] && r[u] == -2) row = find_from<WIDE>(t, bk[u], key[u]);
       if (p < n_cap) gmap[i * n_cap + p] = row + 1;   // 0 = no active input
       const uint64_t m = __ballot(row >= 0);
-      if (lane_id() == 0)
-        blk_cnt[i * nw + blockIdx.x * (kBlock / kWave) + wave] = __popcll(m);
+      if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
   }
+  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk);
 }
 
-// One block per offset: exclusive scan of its per-wave counts, in place; total
-// into totals[i].
+// One block per offset: exclusive scan of its per-block counts, in place;
+// total into totals[i].
 __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, int64_t nblk,
                                                  int64_t* __restrict__ totals) {
   int32_t* c = blk_cnt + blockIdx.x * nblk;
@@ -301,14 +323,15 @@ __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, 
 }
 
 // Compaction of the gather map into the per-offset pair lists: every wave
-// writes its pairs of offset i at pair_off[i] + (exclusive count of the waves
-// before it) + (set lanes before it in its ballot), so R_i comes out in
-// schedule (Z-order) order without any further sorting.
+// writes its pairs of offset i at pair_off[i] + (pairs of the blocks before
+// it) + (pairs of the waves before it in its block) + (set lanes before it in
+// its ballot), so R_i comes out in schedule (Z-order) order without any
+// further sorting.
 __global__ __launch_bounds__(kBlock) void k_compact(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ wave_base,
+    const int32_t* __restrict__ blk_base, const uint32_t* __restrict__ wpre,
     const int64_t* __restrict__ totals, int K, int64_t n_cap,
-    const DeviceHeader* __restrict__ hdr, int64_t nw, int2* __restrict__ pairs,
+    const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ int64_t s_off[kMaxK + 1];
   // pair_off = exclusive prefix of totals (K <= 1024, 4 per thread).
@@ -337,12 +360,13 @@ __global__ __launch_bounds__(kBlock) void k_compact(
   const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   const bool valid = p < n_rows;
   const int32_t y = valid ? perm[p] : 0;
-  const int64_t wslot = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+  const int wave = threadIdx.x / kWave;
   for (int i = 0; i < K; ++i) {
     const int32_t row = valid ? gmap[i * n_cap + p] - 1 : -1;
     const uint64_t m = __ballot(row >= 0);
+    const int64_t q = i * nblk + blockIdx.x;
     if (row >= 0) {
-      const int64_t pos = s_off[i] + wave_base[i * nw + wslot] + prefix_popc(m);
+      const int64_t pos = s_off[i] + blk_base[q] + wave_prefix(wpre[q], wave) + prefix_popc(m);
       pairs[pos] = make_int2(row, y);
     }
   }
@@ -392,9 +416,11 @@ __global__ __launch_bounds__(kBlock) void k_bitsum(const uint32_t* __restrict__ 
   if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
 }
 
-// Single block: exclusive scan of the block sums; n_out = total.
+// Single block: exclusive scan of the block sums; n_out = total.  A total
+// other than `expect` (when >= 0) flags duplicate sites.
 __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum, int64_t nb,
-                                                    DeviceHeader* __restrict__ hdr) {
+                                                    DeviceHeader* __restrict__ hdr,
+                                                    int64_t expect) {
   int64_t carry = 0;
   for (int64_t base = 0; base < nb; base += 4 * kBlock) {
     uint32_t v[4];
@@ -415,7 +441,10 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
     }
     carry += tot;
   }
-  if (threadIdx.x == 0) hdr->n_out = carry;
+  if (threadIdx.x == 0) {
+    hdr->n_out = carry;
+    if (expect >= 0 && carry != expect) atomicOr(&hdr->status, kStDup);
+  }
 }
 
 // Emit the marked output sites in rank order: coordinates and packed keys.
@@ -512,11 +541,14 @@ __device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* 
   return cell;
 }
 
-// Place input row r at its cell: grid[cell] = r + 1 by compare-and-swap
-// from 0 (empty); finding the cell taken means a duplicate site.  Lanes of
-// a wave hit distinct words, so the swaps do not contend.  Optionally copies
-// the coordinates (VSC output sites) and writes packed keys (SC marking).
-// With `count` set, only the first *count (<= N) rows exist.
+// Place input row r at its cell: grid[cell] = r + 1 (0 = empty).  With CAS,
+// by compare-and-swap from 0, and a cell found taken is a duplicate site.
+// Without it a plain store; duplicates then leave fewer occupied cells than
+// rows, which the schedule's count reveals (k_bitscan's `expect`).
+// Optionally copies the coordinates (VSC output sites) and writes packed
+// keys (SC marking).  With `count` set, only the first *count (<= N) rows
+// exist.
+template <bool CAS>
 __global__ __launch_bounds__(kBlock) void k_grid_scatter(
     const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
     GridGeom g, uint32_t* __restrict__ grid, int32_t* __restrict__ copy_out, Codec ckey,
@@ -536,7 +568,10 @@ __global__ __launch_bounds__(kBlock) void k_grid_scatter(
     return;
   }
   if (keys_out) keys_out[r] = pack_site(ckey, x);
-  if (atomicCAS(&grid[grid_cell(g, x)], 0u, static_cast<uint32_t>(r + 1)) != 0u)
+  const uint32_t cell = grid_cell(g, x);
+  if (!CAS)
+    grid[cell] = static_cast<uint32_t>(r + 1);
+  else if (atomicCAS(&grid[cell], 0u, static_cast<uint32_t>(r + 1)) != 0u)
     atomicOr(status, kStDup);
 }
 
@@ -602,9 +637,10 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
     const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
     const DeviceHeader* __restrict__ hdr, int64_t n_cap, GridGeom g, OffsetTable ot,
     const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
-    int32_t* __restrict__ blk_cnt, int64_t nw) {
+    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
   __shared__ uint32_t s_dil[kMaxK][kMaxD];
+  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
   for (int i = threadIdx.x; i < ot.K; i += blockDim.x) {
     int rem = i;
     for (int j = ot.D - 1; j >= 0; --j) {
@@ -658,10 +694,10 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
       const int32_t e = (valid && i == ot.centre) ? y + 1 : static_cast<int32_t>(gv[u]);
       if (p < n_cap) gmap[i * n_cap + p] = e;   // 1 + input row, 0 = none
       const uint64_t m = __ballot(e != 0);
-      if (lane_id() == 0)
-        blk_cnt[i * nw + blockIdx.x * (kBlock / kWave) + wave] = __popcll(m);
+      if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
   }
+  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk);
 }
 
 // ---------------------------------------------------------------------------
@@ -822,22 +858,20 @@ int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Co
 
 // Per-offset pair counts -> k_i and pair_off; gather map -> pair lists.
 void launch_scan_compact(spconv_rulebook rb) {
-  const int64_t nw = rb->nblk * (kBlock / kWave);
-  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, nw,
+  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
                                                                   rb->totals);
   k_compact<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
-      rb->gmap, rb->perm, rb->blk_cnt, rb->totals, static_cast<int>(rb->K), rb->n_cap, rb->hdr,
-      nw, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+      rb->gmap, rb->perm, rb->blk_cnt, rb->wpre, rb->totals, static_cast<int>(rb->K), rb->n_cap,
+      rb->hdr, rb->nblk, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
 }
 
 void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
                                const Codec& cin, const Transient& tr) {
   const OffsetTable ot = make_offsets(rb);
   const unsigned g = static_cast<unsigned>(rb->nblk);
-  const int64_t nw = rb->nblk * (kBlock / kWave);     // waves (count slots) per offset
   auto launch = [&](auto kern) {
     kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->n_cap, crow, cin,
-                                       tr.table, ot, rb->gmap, rb->blk_cnt, nw);
+                                       tr.table, ot, rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
   const bool sc = rb->kind == SPCONV_SC;
 #define SPC_PROBE(W, S)                                      \
@@ -925,34 +959,36 @@ GridBufs take_grid(Carver* cv, uint64_t cells) {
   return b;
 }
 
-// Clear the grid and scatter rows [0, N) (or [0, *count)) into it.
+// Clear the grid and scatter rows [0, N) (or [0, *count)) into it; `cas`
+// detects duplicates at the scatter, otherwise the schedule's count does.
 void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
                          const int64_t* count, const GridGeom& g, uint64_t cells,
                          const GridBufs& b, int32_t* copy_out, const Codec& ckey,
-                         uint64_t* keys_out) {
+                         uint64_t* keys_out, bool cas) {
   launch_zero(b.grid, cells, rb->stream);
-  k_grid_scatter<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out,
-                                                         ckey, keys_out, &rb->hdr->status);
+  auto kern = cas ? k_grid_scatter<true> : k_grid_scatter<false>;
+  kern<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out, ckey,
+                                               keys_out, &rb->hdr->status);
 }
 
 // Z-order schedule from the grid; also sets n_out to the number of occupied
-// cells.
-void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells) {
+// cells, flagging duplicates when that is not `expect` (>= 0).
+void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
+                          int64_t expect) {
   k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
                                                                         b.bitmap, b.bsum);
-  k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr);
-  k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.bitmap, b.nwords,
-                                                                        b.bsum, b.grid, rb->perm);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect);
+  k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
+      b.bitmap, b.nwords, b.bsum, b.grid, rb->perm);
 }
 
 void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const GridGeom& g,
                        const GridBufs& b, uint64_t cells) {
   const OffsetTable ot = make_offsets(rb);
-  const int64_t nw = rb->nblk * (kBlock / kWave);
   auto launch = [&](auto kern) {
     kern<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
         rows_sites, rb->perm, rb->hdr, rb->n_cap, g, ot, b.grid, static_cast<uint32_t>(cells),
-        rb->gmap, rb->blk_cnt, nw);
+        rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
   const bool sc = rb->kind == SPCONV_SC;
 #define SPC_PROBE(S)                                         \
@@ -977,8 +1013,9 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
   }
   Carver cv{static_cast<char*>(mem)};
   const GridBufs b = take_grid(&cv, cells);
-  launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr);
-  launch_grid_schedule(rb, b, cells);
+  launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr,
+                      false);
+  launch_grid_schedule(rb, b, cells, N);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
   if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -1014,17 +1051,17 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
   Extents E{};
   for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
-  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys);
+  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys, true);
   k_fill_u32<<<grid_for(static_cast<int64_t>(lwords)), kBlock, 0, rb->stream>>>(lex, 0u, lwords);
   const OffsetTable ot = make_offsets(rb);
   k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, cin, ot, E, lex);
   k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
-  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1);
   k_sc_emit<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
                                                                      rb->out_coords, nullptr);
   launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
-                      cout, nullptr);
-  launch_grid_schedule(rb, bo, cells_out);
+                      cout, nullptr, false);
+  launch_grid_schedule(rb, bo, cells_out, -1);
   launch_probe_grid(rb, rb->out_coords, gi, bi, cells_in);
   if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -1091,7 +1128,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     const OffsetTable ot = make_offsets(rb);
     k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(tr.keys, N, cin, ot, E, bitmap);
     k_bitsum<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(bitmap, nwords, bsum);
-    k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr);
+    k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1);
     k_sc_emit<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
     launch_schedule(rb, out_keys, cout, &cv);

@@ -450,27 +450,40 @@ def test_non_contiguous_coords_through_python_api():
     np.testing.assert_array_equal(pairs.cpu().numpy(), ref.pairs)
 
 
-@pytest.mark.parametrize("dtype,ci", [("bf16", 64), ("f32", 32)])
-def test_halo_overflow_fallback(monkeypatch, dtype, ci):
-    """Halo kernel (opt-in): tiles whose input halo exceeds the LDS budget
-    gather directly instead."""
-    monkeypatch.setenv("SPCONV_FORCE_PATH", "halo")
-    coords = inputs.surfaces(1, 40, 5.0, 16.0, seed=23, target=4000)
-    size = [1, 40, 40, 40]
-    y_ref, yo, absb, _, _ = compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1],
-                                          ci, 64, dtype=dtype, what="halo path")
-    for cap in ("100", "0"):
-        monkeypatch.setenv("SPCONV_TEST_HALO_CAP", cap)
-        y, _, _, _, _ = compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], ci, 64,
-                                      dtype=dtype, what=f"halo cap {cap}")
-        # both routes sum the same products in the same order
-        np.testing.assert_array_equal(y, y_ref)
+@pytest.mark.parametrize("path", ["mfma", "vec"])
+def test_matrix_core_shapes_both_paths(monkeypatch, path):
+    """Matrix-core shapes, through the matrix-core kernel and the vector path
+    (SPCONV_FORCE_PATH=vec): wide outputs walk column chunks; SC layers,
+    generic filter sizes and f = 1 included."""
+    if path == "vec":
+        monkeypatch.setenv("SPCONV_FORCE_PATH", "vec")
+    coords = inputs.surfaces(2, 40, 5.0, 16.0, seed=24, target=4000)
+    size = [2, 40, 40, 40]
+    compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], 64, 128,
+                  dtype="bf16", what=f"{path} C_out 128")
+    compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], 32, 64,
+                  what=f"{path} f32")
+    compare_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], 64, 64,
+                  dtype="bf16", out_dtype="f32", what=f"{path} bf16->f32")
+    compare_layer(spc.VSC, coords, size, [1, 1, 3, 3], [1, 1, 1, 1], 64, 64,
+                  dtype="bf16", what=f"{path} 1x3x3")
+    compare_layer(spc.VSC, coords, size, [1, 5, 5, 5], [1, 1, 1, 1], 64, 64,
+                  dtype="bf16", what=f"{path} 5^3")
+    compare_layer(spc.VSC, coords, size, [1, 1, 1, 1], [1, 1, 1, 1], 32, 64,
+                  what=f"{path} f=1")
+    compare_layer(spc.SC, coords, size, [1, 2, 2, 2], [1, 2, 2, 2], 64, 64,
+                  dtype="bf16", what=f"{path} SC 2/2")
+    compare_layer(spc.SC, coords, size, [1, 3, 3, 3], [1, 2, 2, 2], 32, 128,
+                  what=f"{path} SC 3/2 f32")
 
 
-def test_halo_path_forced_sc_and_wide_out(monkeypatch):
-    monkeypatch.setenv("SPCONV_FORCE_PATH", "halo")
-    coords = inputs.surfaces(1, 40, 5.0, 16.0, seed=24, target=4000)
-    compare_layer(spc.VSC, coords, [1, 40, 40, 40], [1, 3, 3, 3], [1, 1, 1, 1], 64, 128,
-                  dtype="bf16", what="forced halo C_out 128")
-    compare_layer(spc.SC, coords, [1, 40, 40, 40], [1, 3, 3, 3], [1, 2, 2, 2], 32, 64,
-                  what="forced halo SC f32")
+@pytest.mark.parametrize("path", ["hash", "grid"])
+def test_forward_on_both_rulebook_paths(monkeypatch, path):
+    """The forward walks the schedule and gather map of either rule-book
+    path."""
+    monkeypatch.setenv("SPCONV_RULEBOOK", path)
+    coords = inputs.surfaces(3, 36, 4.0, 14.0, seed=25, target=3000)
+    compare_layer(spc.VSC, coords, [3, 36, 36, 36], [1, 3, 3, 3], [1, 1, 1, 1], 64, 64,
+                  dtype="bf16", what=f"forward {path}")
+    compare_layer(spc.SC, coords, [3, 36, 36, 36], [1, 2, 2, 2], [1, 2, 2, 2], 64, 64,
+                  dtype="bf16", what=f"forward SC {path}")
