@@ -73,9 +73,11 @@ enum {
 
 typedef struct spconv_rulebook_s* spconv_rulebook;
 
-/* Build the rule book of one layer (Section 4: hash the active sites, then
- * list for every filter offset the (input row, output row) pairs; VSC
- * re-uses the input site set as its output set).
+/* Build the rule book of one layer (Section 4: map the active sites to rows,
+ * then list for every filter offset the (input row, output row) pairs; VSC
+ * re-uses the input site set as its output set).  The site map is a dense
+ * index grid when the grid is small enough, else a hash table; the result
+ * does not depend on which.
  *
  *   kind          SPCONV_VSC or SPCONV_SC
  *   D             coordinates per site, 2..4 (sample index + d spatial)
