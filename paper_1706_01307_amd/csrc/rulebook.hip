@@ -141,10 +141,17 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, uint64_t n) {
 }
 
 // Zero n 32-bit words at a 16-byte aligned p: 16-byte stores, then the tail.
-__global__ void k_zero_u32(uint32_t* __restrict__ p, uint64_t n) {
+// With hdr set, also initialises the build's header (status 0, n_out).
+__global__ void k_zero_u32(uint32_t* __restrict__ p, uint64_t n, DeviceHeader* hdr,
+                           int64_t n_out) {
   const uint64_t n4 = n / 4;
   const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
   const uint64_t t = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x;
+  if (hdr && t == 0) {
+    hdr->status = 0;
+    hdr->pad = 0;
+    hdr->n_out = n_out;
+  }
   uint4* q = reinterpret_cast<uint4*>(p);
   for (uint64_t i = t; i < n4; i += stride) q[i] = make_uint4(0u, 0u, 0u, 0u);
   if (t < n - 4 * n4) p[4 * n4 + t] = 0u;
@@ -334,6 +341,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(
     const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ int64_t s_off[kMaxK + 1];
+  __shared__ uint32_t s_wp[kMaxK];
   // pair_off = exclusive prefix of totals (K <= 1024, 4 per thread).
   {
     int64_t v[4], sum = 0;
@@ -356,18 +364,33 @@ __global__ __launch_bounds__(kBlock) void k_compact(
   __syncthreads();
   if (blockIdx.x == 0)
     for (int k = threadIdx.x; k <= K; k += kBlock) pair_off[k] = s_off[k];
+  __syncthreads();
+  // this block's start inside every R_i, and its waves' packed prefixes
+  for (int k = threadIdx.x; k < K; k += kBlock) {
+    const int64_t q = static_cast<int64_t>(k) * nblk + blockIdx.x;
+    s_off[k] += blk_base[q];
+    s_wp[k] = wpre[q];
+  }
+  __syncthreads();
   const int64_t n_rows = hdr->n_out;
   const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   const bool valid = p < n_rows;
   const int32_t y = valid ? perm[p] : 0;
   const int wave = threadIdx.x / kWave;
-  for (int i = 0; i < K; ++i) {
-    const int32_t row = valid ? gmap[i * n_cap + p] - 1 : -1;
-    const uint64_t m = __ballot(row >= 0);
-    const int64_t q = i * nblk + blockIdx.x;
-    if (row >= 0) {
-      const int64_t pos = s_off[i] + blk_base[q] + wave_prefix(wpre[q], wave) + prefix_popc(m);
-      pairs[pos] = make_int2(row, y);
+  constexpr int U = 4;                  // gather-map loads in flight
+  for (int i0 = 0; i0 < K; i0 += U) {
+    int32_t row[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      row[u] = (valid && i0 + u < K) ? gmap[(i0 + u) * n_cap + p] - 1 : -1;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u;
+      const uint64_t m = __ballot(row[u] >= 0);
+      if (row[u] >= 0) {
+        const int64_t pos = s_off[i] + wave_prefix(s_wp[i], wave) + prefix_popc(m);
+        pairs[pos] = make_int2(row[u], y);
+      }
     }
   }
 }
@@ -722,11 +745,12 @@ inline unsigned grid_for(int64_t n, int per = kBlock) {
   return static_cast<unsigned>(g < 1 ? 1 : g);
 }
 
-void launch_zero(uint32_t* p, uint64_t n, hipStream_t stream) {
+void launch_zero(uint32_t* p, uint64_t n, hipStream_t stream, DeviceHeader* hdr = nullptr,
+                 int64_t n_out = 0) {
   const uint64_t n4 = n / 4;
   uint64_t blocks = (n4 + 4 * kBlock - 1) / (4 * kBlock);   // 4 stores per thread
   blocks = blocks < 1 ? 1 : (blocks > 65536 ? 65536 : blocks);
-  k_zero_u32<<<static_cast<unsigned>(blocks), kBlock, 0, stream>>>(p, n);
+  k_zero_u32<<<static_cast<unsigned>(blocks), kBlock, 0, stream>>>(p, n, hdr, n_out);
 }
 
 OffsetTable make_offsets(spconv_rulebook rb) {
@@ -961,11 +985,12 @@ GridBufs take_grid(Carver* cv, uint64_t cells) {
 
 // Clear the grid and scatter rows [0, N) (or [0, *count)) into it; `cas`
 // detects duplicates at the scatter, otherwise the schedule's count does.
+// init_n >= 0 also initialises the header with n_out = init_n.
 void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
                          const int64_t* count, const GridGeom& g, uint64_t cells,
                          const GridBufs& b, int32_t* copy_out, const Codec& ckey,
-                         uint64_t* keys_out, bool cas) {
-  launch_zero(b.grid, cells, rb->stream);
+                         uint64_t* keys_out, bool cas, int64_t init_n = -1) {
+  launch_zero(b.grid, cells, rb->stream, init_n >= 0 ? rb->hdr : nullptr, init_n);
   auto kern = cas ? k_grid_scatter<true> : k_grid_scatter<false>;
   kern<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out, ckey,
                                                keys_out, &rb->hdr->status);
@@ -1005,7 +1030,6 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
 int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
                    uint64_t cells) {
   const int64_t N = rb->n_in;
-  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
   void* mem = nullptr;
   if (hipMallocAsync(&mem, grid_bytes(cells) + 256, rb->stream) != hipSuccess) {
     (void)hipGetLastError();
@@ -1014,7 +1038,7 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
   Carver cv{static_cast<char*>(mem)};
   const GridBufs b = take_grid(&cv, cells);
   launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr,
-                      false);
+                      false, N);
   launch_grid_schedule(rb, b, cells, N);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
   if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
@@ -1034,7 +1058,6 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   for (int j = 0; j < rb->D; ++j) lex_cells *= static_cast<uint64_t>(rb->out_size[j]);
   const uint64_t lwords = (lex_cells + 31) / 32;
   const int64_t lnbw = static_cast<int64_t>((lwords + 4 * kBlock - 1) / (4 * kBlock));
-  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, 0);
   const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out) + align_up(lwords * 4, 256) +
                        align_up(static_cast<size_t>(lnbw) * 4, 256) +
                        align_up(static_cast<size_t>(N) * 8, 256) + 256;
@@ -1051,7 +1074,7 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
   Extents E{};
   for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
-  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys, true);
+  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys, true, 0);
   k_fill_u32<<<grid_for(static_cast<int64_t>(lwords)), kBlock, 0, rb->stream>>>(lex, 0u, lwords);
   const OffsetTable ot = make_offsets(rb);
   k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, cin, ot, E, lex);
