@@ -152,6 +152,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
     }
   }
   rb->nblk = (rb->n_cap + kBlock - 1) / kBlock;
+  rb->gstride = rb->nblk * kBlock;
 
   // One persistent allocation: header, output sites, gather map, counts,
   // offsets and the pair lists (sized for the worst case K * n_cap so the
@@ -160,7 +161,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   const size_t Kz = static_cast<size_t>(K);
   size_t bytes = 256;
   bytes += align_up(n_cap * D * 4, 256);
-  bytes += align_up(Kz * n_cap * 4, 256);
+  bytes += align_up(Kz * static_cast<size_t>(rb->gstride) * 4, 256);
   bytes += align_up(Kz * static_cast<size_t>(rb->nblk) * 4 * 2, 256);
   bytes += align_up(Kz * 8, 256);
   bytes += align_up((Kz + 1) * 8, 256);
@@ -181,7 +182,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   };
   rb->hdr = reinterpret_cast<DeviceHeader*>(take(256));
   rb->out_coords = reinterpret_cast<int32_t*>(take(n_cap * D * 4));
-  rb->gmap = reinterpret_cast<int32_t*>(take(Kz * n_cap * 4));
+  rb->gmap = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->gstride) * 4));
   rb->blk_cnt = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->nblk) * 4 * 2));
   rb->wpre = reinterpret_cast<uint32_t*>(rb->blk_cnt + Kz * static_cast<size_t>(rb->nblk));
   rb->totals = reinterpret_cast<int64_t*>(take(Kz * 8));

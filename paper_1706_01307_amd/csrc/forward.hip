@@ -70,7 +70,7 @@ template <> struct ElemIO<uint16_t> {
 // ---------------------------------------------------------------------------
 template <typename TIn, typename TOut>
 __global__ __launch_bounds__(256) void k_fwd_vec(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t n_cap,
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
     const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
     int C_out) {
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void k_fwd_vec(
     const int col = static_cast<int>(idx - p * C_out);
     float acc = 0.0f;
     for (int i = 0; i < K; ++i) {
-      const int32_t g = gmap[i * n_cap + p] - 1;
+      const int32_t g = gmap[i * gstride + p] - 1;
       if (g < 0) continue;
       const int64_t xb = static_cast<int64_t>(g) * C_in;
       const int64_t wb = static_cast<int64_t>(i) * C_in * C_out + col;
@@ -189,7 +189,7 @@ struct WImage {
 // into the other LDS buffer.  One barrier per offset publishes W^(i+1).
 template <typename TIn, int NCH, int NCB, int RB, typename TOut, int KT, bool SKIP = false>
 __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t n_cap,
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K_arg,
     const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
     const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles) {
@@ -288,11 +288,11 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   // offset past the map's range reads 0, so rows past the end and offsets
   // past K need no branch (a load under a divergent branch would force a
   // full wait for every load in flight).
-  const uint32_t gmap_bytes = static_cast<uint32_t>(n_cap * 4);
+  const uint32_t gmap_bytes = static_cast<uint32_t>(gstride * 4);
   auto g_load = [&](int i, GRegs& g) {
     const int ic = i < K ? i : 0;
     const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<int32_t*>(gmap + static_cast<int64_t>(ic) * n_cap), 0,
+        const_cast<int32_t*>(gmap + static_cast<int64_t>(ic) * gstride), 0,
         static_cast<int>(gmap_bytes), static_cast<int>(kBufDword3));
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
@@ -424,11 +424,11 @@ void launch_mfma(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void
   const int64_t per = (ntiles + 7) / 8;
   dim3 grid(static_cast<unsigned>(8 * per), static_cast<unsigned>(C_out / (NCB * 16)));
   // 3^3 filters on Z-ordered tiles: whole 16-row blocks often lack an
-  // offset, so the unrolled kernel skips their gathers and products
+  // offset, so the unrolled kernel skips their products
   auto kern = rb->K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true>
                           : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0>;
   kern<<<grid, 256, 0, stream>>>(
-      rb->gmap, rb->perm, rb->n_cap, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x), x_bytes,
+      rb->gmap, rb->perm, rb->gstride, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x), x_bytes,
       static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_out, ntiles);
 }
 
@@ -451,7 +451,7 @@ bool try_mfma(spconv_rulebook rb, int in_dt, const void* x, const void* w, const
   if (C_out % 16 != 0) return false;
   const uint64_t xb = static_cast<uint64_t>(rb->n_in) * C_in * (in_dt == SPCONV_BF16 ? 2 : 4);
   // buffer ranges are kept below 2^31 bytes (inputs and one offset's map row)
-  if (xb >= 0x7fffffffull || static_cast<uint64_t>(rb->n_cap) * 4 >= 0x7fffffffull) return false;
+  if (xb >= 0x7fffffffull || static_cast<uint64_t>(rb->gstride) * 4 >= 0x7fffffffull) return false;
   const uint32_t x_bytes = static_cast<uint32_t>(xb);
   if (in_dt == SPCONV_BF16) {
     switch (C_in) {
@@ -480,7 +480,7 @@ void launch_vec(spconv_rulebook rb, const void* x, const void* w, const float* b
   if (blocks > 65536) blocks = 65536;
   if (blocks < 1) blocks = 1;
   k_fwd_vec<TIn, TOut><<<static_cast<unsigned>(blocks), 256, 0, stream>>>(
-      rb->gmap, rb->perm, rb->n_cap, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x),
+      rb->gmap, rb->perm, rb->gstride, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x),
       static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_in, C_out);
 }
 

@@ -159,7 +159,8 @@ struct spconv_rulebook_s {
   // carved device pointers
   spc::DeviceHeader* hdr;
   int32_t* out_coords;         // [n_cap][D]
-  int32_t* gmap;               // [K][n_cap] 1 + input row per (offset, schedule position); 0 = none
+  int32_t* gmap;               // [K][gstride] 1 + input row per (offset, schedule position); 0 = none
+  int64_t gstride;             // gather-map row length: nblk * kBlock (entries past n_out are 0)
   int32_t* blk_cnt;            // [K][nblk] per-block pair counts, then bases
   uint32_t* wpre;              // [K][nblk] per-wave prefixes inside a block (bytes)
   int64_t* totals;             // [K] k_i

@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kBlock) void k_insert(
 template <bool WIDE, bool SC, int D>
 __global__ __launch_bounds__(kBlock) void k_probe(
     const uint64_t* __restrict__ rowkeys, const int32_t* __restrict__ perm,
-    const DeviceHeader* __restrict__ hdr, int64_t n_cap, Codec crow, Codec cin, Table t,
+    const DeviceHeader* __restrict__ hdr, int64_t gstride, Codec crow, Codec cin, Table t,
     OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt,
     uint32_t* __restrict__ wpre, int64_t nblk) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(kBlock) void k_probe(
       if (i >= ot.K) break;
       int32_t row = inb[u] ? r[u] : ((valid && i == ot.centre) ? y : -1);
       if (inb[u] && r[u] == -2) row = find_from<WIDE>(t, bk[u], key[u]);
-      if (p < n_cap) gmap[i * n_cap + p] = row + 1;   // 0 = no active input
+      if (p < gstride) gmap[i * gstride + p] = row + 1;   // 0 = no input
       const uint64_t m = __ballot(row >= 0);
       if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, 
 __global__ __launch_bounds__(kBlock) void k_compact(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ blk_base, const uint32_t* __restrict__ wpre,
-    const int64_t* __restrict__ totals, int K, int64_t n_cap,
+    const int64_t* __restrict__ totals, int K, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ int64_t s_off[kMaxK + 1];
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(
     int32_t row[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      row[u] = (valid && i0 + u < K) ? gmap[(i0 + u) * n_cap + p] - 1 : -1;
+      row[u] = (valid && i0 + u < K) ? gmap[(i0 + u) * gstride + p] - 1 : -1;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int i = i0 + u;
@@ -658,7 +658,7 @@ constexpr uint32_t kOOB = 0x80000000u;         // byte offset past every buffer:
 template <bool SC, int D>
 __global__ __launch_bounds__(kBlock) void k_probe_grid(
     const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
-    const DeviceHeader* __restrict__ hdr, int64_t n_cap, GridGeom g, OffsetTable ot,
+    const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g, OffsetTable ot,
     const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
     int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
@@ -715,7 +715,7 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
       const int i = i0 + u;
       if (i >= ot.K) break;
       const int32_t e = (valid && i == ot.centre) ? y + 1 : static_cast<int32_t>(gv[u]);
-      if (p < n_cap) gmap[i * n_cap + p] = e;   // 1 + input row, 0 = none
+      if (p < gstride) gmap[i * gstride + p] = e;   // 1 + input row, 0 = none
       const uint64_t m = __ballot(e != 0);
       if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
@@ -885,7 +885,7 @@ void launch_scan_compact(spconv_rulebook rb) {
   k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
                                                                   rb->totals);
   k_compact<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
-      rb->gmap, rb->perm, rb->blk_cnt, rb->wpre, rb->totals, static_cast<int>(rb->K), rb->n_cap,
+      rb->gmap, rb->perm, rb->blk_cnt, rb->wpre, rb->totals, static_cast<int>(rb->K), rb->gstride,
       rb->hdr, rb->nblk, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
 }
 
@@ -894,7 +894,7 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
   const OffsetTable ot = make_offsets(rb);
   const unsigned g = static_cast<unsigned>(rb->nblk);
   auto launch = [&](auto kern) {
-    kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->n_cap, crow, cin,
+    kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->gstride, crow, cin,
                                        tr.table, ot, rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
   const bool sc = rb->kind == SPCONV_SC;
@@ -1012,7 +1012,7 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
   const OffsetTable ot = make_offsets(rb);
   auto launch = [&](auto kern) {
     kern<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
-        rows_sites, rb->perm, rb->hdr, rb->n_cap, g, ot, b.grid, static_cast<uint32_t>(cells),
+        rows_sites, rb->perm, rb->hdr, rb->gstride, g, ot, b.grid, static_cast<uint32_t>(cells),
         rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
   const bool sc = rb->kind == SPCONV_SC;
