@@ -3,7 +3,7 @@
 Workload (default): 8 voxelised surfaces on a 128^3 grid, ~100k active sites
 each (~900k in total), VSC 3^3, 64 -> 64 planes, bf16 features and weights,
 fp32 accumulation, bf16 output, fp32 bias.  A step is one pass of the whole
-hot path on resident inputs: build the rule book (hash, neighbour probe,
+hot path on resident inputs: build the rule book (site map, neighbour probe,
 per-offset compaction) and run the forward multiply-add.
 
 Prints one JSON line:
@@ -11,6 +11,10 @@ Prints one JSON line:
   roofline   the forward kernel (the dominant one) against the bf16 dense
              matrix-core peak, from HIP events around each forward launch
   cpu_baseline  the oracle on one sample of the same workload, host cores
+
+Other modes (not the benchmark line): --workload with a multi-layer stack
+(VSC levels joined by SC) times the whole stack; --peaks measures a plain
+device copy and a library bf16 GEMM as achievable-peak references.
 """
 from __future__ import annotations
 
@@ -46,6 +50,8 @@ def _args():
                    help="samples of the batch the oracle baseline runs on")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one plain device copy of this many MiB (counter calibration)")
+    p.add_argument("--peaks", action="store_true",
+                   help="measure a device copy and a bf16 library GEMM instead")
     return p.parse_args()
 
 
@@ -100,9 +106,15 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lib = _lib.load()
     dev = torch.device("cuda:0")
+    if a.peaks:
+        measure_peaks(torch, dev)
+        return
     wl = inputs.make_workload(a.workload, variant=a.variant)
+    if len(wl.layers) > 1:
+        run_stack(a, wl, torch, dev, lib, _lib, inputs)
+        return
     layer = wl.layers[0]
-    assert layer.kind == "vsc" and len(wl.layers) == 1, "bench times a single VSC layer"
+    assert layer.kind == "vsc", "bench times a single VSC layer or a stack"
     N, D = len(wl.coords), wl.d + 1
     K = layer.f ** wl.d
     Cin, Cout = layer.c_in, layer.c_out
@@ -193,8 +205,10 @@ def main():
     esz = 2 if bf16 else 4
     fwd_bytes = N * Cin * esz + N * Cout * esz + 4 * K * N + K * Cin * Cout * esz + 4 * Cout
 
+    headline = a.workload == "surf128x8_vsc3_c64_bf16"
     out = {
-        "metric": "VSC layer active sites/sec + effective TFLOP/s (3^3, C=64, 128^3 surfaces)",
+        "metric": ("VSC layer active sites/sec + effective TFLOP/s (3^3, C=64, 128^3 surfaces)"
+                   if headline else "VSC layer active sites/sec + effective TFLOP/s"),
         "value": N / (ms_per_step * 1e-3),
         "unit": "active sites/s",
         "n_gpus": 1,
@@ -219,6 +233,141 @@ def main():
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, bias, a.cpu_samples)
     print(json.dumps(out), flush=True)
+
+
+def measure_peaks(torch, dev):
+    """Achievable references on this GPU: a 1 GiB device-to-device copy
+    (HBM read + write) and an 8192^3 bf16 GEMM through the vendor library."""
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+    nb = 1 << 30
+    src = torch.ones(nb // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    t_copy = timed(lambda: dst.copy_(src), 20)
+    del src, dst
+    n = 8192
+    a = torch.randn((n, n), dtype=torch.bfloat16, device=dev).contiguous()
+    b = torch.randn((n, n), dtype=torch.bfloat16, device=dev).contiguous()
+    t_mm = timed(lambda: torch.matmul(a, b), 10)
+    print(json.dumps({
+        "copy_GBps": 2 * nb / t_copy / 1e9, "copy_bytes": nb,
+        "bf16_gemm_TFLOPs": 2 * n ** 3 / t_mm / 1e12, "gemm_shape": [n, n, n],
+        "spec": {"hbm_GBps": PEAKS["hbm"], "bf16_TFLOPs": PEAKS["bf16"]}}), flush=True)
+
+
+def run_stack(a, wl, torch, dev, lib, _lib, inputs):
+    """A stack of layers: VSC levels joined by strided SC layers.  One VSC
+    rule book per level serves all its VSC layers (Section 4: layers on the
+    same sites share it); each SC build waits once (the next level needs its
+    output count on the host) and its output sites feed the next build in
+    place.  A step = every build + every forward + releases."""
+    D = wl.d + 1
+    bf16 = wl.dtype == "bf16"
+    esz = 2 if bf16 else 4
+    tdt = torch.bfloat16 if bf16 else torch.float32
+    dt_code = _lib.BF16 if bf16 else _lib.F32
+    N0 = len(wl.coords)
+    ct = torch.from_numpy(np.ascontiguousarray(wl.coords)).to(dev).contiguous()
+    params = []
+    for j, L in enumerate(wl.layers):
+        K = L.f ** wl.d
+        wf = inputs.normal_f32((K, L.c_in, L.c_out), std=1.0 / np.sqrt(K * L.c_in), seed=100 + j)
+        bf = inputs.normal_f32((L.c_out,), std=0.1, seed=200 + j)
+        if bf16:
+            wt = torch.from_numpy(inputs.to_bf16_bits(wf).view(np.int16)).view(torch.bfloat16).to(dev)
+        else:
+            wt = torch.from_numpy(wf).to(dev)
+        params.append((wt, torch.from_numpy(bf).to(dev)))
+    xf = inputs.normal_f32((N0, wl.layers[0].c_in), seed=11)
+    if bf16:
+        x0 = torch.from_numpy(inputs.to_bf16_bits(xf).view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        x0 = torch.from_numpy(xf).to(dev)
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    info = []
+
+    def step(record=False):
+        coords, N = ctypes.c_void_p(ct.data_ptr()), N0
+        size = np.array(wl.spatial_size, np.int32)
+        x, rb, handles = x0, None, []
+        for j, L in enumerate(wl.layers):
+            wt, bt = params[j]
+            f = np.array([1] + [L.f] * wl.d, np.int32)
+            s = np.array([1] + [L.s] * wl.d, np.int32)
+            if L.kind == "vsc":
+                if rb is None:
+                    rb = ctypes.c_void_p()
+                    _lib.check(lib.spconv_build_rulebook(_lib.VSC, D, coords, N, size.ctypes.data,
+                                                         f.ctypes.data, s.ctypes.data,
+                                                         _lib.BUILD_ASYNC, sp, ctypes.byref(rb)),
+                               "build")
+                    handles.append(rb)
+                y = torch.empty((N, L.c_out), dtype=tdt, device=dev)
+                _lib.check(lib.spconv_vsc_forward(rb, dt_code, ctypes.c_void_p(x.data_ptr()),
+                                                  ctypes.c_void_p(wt.data_ptr()),
+                                                  ctypes.c_void_p(bt.data_ptr()), dt_code,
+                                                  ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out,
+                                                  sp), "vsc forward")
+                k_pairs = None
+            else:
+                h = ctypes.c_void_p()
+                _lib.check(lib.spconv_build_rulebook(_lib.SC, D, coords, N, size.ctypes.data,
+                                                     f.ctypes.data, s.ctypes.data, 0, sp,
+                                                     ctypes.byref(h)), "build")
+                handles.append(h)
+                n_out, osz = ctypes.c_int64(), np.zeros(D, np.int32)
+                _lib.check(lib.spconv_rulebook_query(h, None, ctypes.byref(n_out), None,
+                                                     osz.ctypes.data, None), "query")
+                y = torch.empty((n_out.value, L.c_out), dtype=tdt, device=dev)
+                _lib.check(lib.spconv_sc_forward(h, dt_code, ctypes.c_void_p(x.data_ptr()),
+                                                 ctypes.c_void_p(wt.data_ptr()),
+                                                 ctypes.c_void_p(bt.data_ptr()), dt_code,
+                                                 ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out,
+                                                 sp), "sc forward")
+                oc = ctypes.c_void_p()
+                _lib.check(lib.spconv_rulebook_out_coords(h, ctypes.byref(oc)), "out coords")
+                coords, N, size, rb = oc, n_out.value, osz, None
+            if record:
+                off = np.zeros(L.f ** wl.d + 1, np.int64)
+                _lib.check(lib.spconv_rulebook_query(handles[-1], None, None, None, None,
+                                                     off.ctypes.data), "query")
+                info.append({"layer": j, "kind": L.kind, "n_in": int(x.shape[0]),
+                             "n_out": int(y.shape[0]), "c_in": L.c_in, "c_out": L.c_out,
+                             "sum_k": int(off[-1])})
+            x = y
+        for h in handles:
+            lib.spconv_rulebook_destroy(h)
+        return x
+
+    step(record=True)                     # sizes and pair counts (untimed)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / a.steps
+    flops = sum(2.0 * r["sum_k"] * r["c_in"] * r["c_out"] for r in info)
+    print(json.dumps({
+        "metric": "layer-stack forward active input sites/sec (all builds + forwards)",
+        "value": N0 / (ms * 1e-3), "unit": "active sites/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "variant": a.variant, "batch": wl.batch,
+                   "grid": wl.size, "active_sites": N0, "layers": info},
+        "effective_tflops": flops / (ms * 1e-3) / 1e12,
+        "bytes_features": int(sum(r["n_in"] * r["c_in"] * esz + r["n_out"] * r["c_out"] * esz
+                                  for r in info))}), flush=True)
 
 
 if __name__ == "__main__":

@@ -426,16 +426,12 @@ __global__ __launch_bounds__(kBlock) void k_sc_mark(
   }
 }
 
-// Popcount of 1024 bitmap words per block.
+// Popcount of 256 bitmap words per block (one word per thread).
 __global__ __launch_bounds__(kBlock) void k_bitsum(const uint32_t* __restrict__ bitmap,
                                                    uint64_t nwords, uint32_t* __restrict__ bsum) {
-  const uint64_t base = blockIdx.x * 4ull * kBlock + 4ull * threadIdx.x;
-  uint32_t v = 0;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-    if (base + u < nwords) v += __popc(bitmap[base + u]);
+  const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
   uint32_t tot;
-  block_excl_scan<uint32_t>(v, &tot);
+  block_excl_scan<uint32_t>(w < nwords ? __popc(bitmap[w]) : 0u, &tot);
   if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
 }
 
@@ -471,36 +467,27 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
 }
 
 // Emit the marked output sites in rank order: coordinates and packed keys.
+// One bitmap word (32 cells) per thread, 256 words per block.
 __global__ __launch_bounds__(kBlock) void k_sc_emit(
     const uint32_t* __restrict__ bitmap, uint64_t nwords, const uint32_t* __restrict__ bbase,
     Codec cout, Extents E, int32_t* __restrict__ out_coords,
     uint64_t* __restrict__ out_keys) {
-  const uint64_t base = blockIdx.x * 4ull * kBlock + 4ull * threadIdx.x;
-  uint32_t w[4];
-  uint32_t v = 0;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    w[u] = base + u < nwords ? bitmap[base + u] : 0u;
-    v += __popc(w[u]);
-  }
+  const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
+  uint32_t word = w < nwords ? bitmap[w] : 0u;
   uint32_t tot;
-  uint32_t rank = block_excl_scan<uint32_t>(v, &tot) + bbase[blockIdx.x];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    uint32_t word = w[u];
-    while (word) {
-      const int b = __builtin_ctz(word);
-      word &= word - 1;
-      uint32_t L = static_cast<uint32_t>((base + u) * 32 + b);
-      int32_t yv[kMaxD];
-      for (int j = cout.D - 1; j >= 0; --j) {
-        yv[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
-        L /= static_cast<uint32_t>(E.e[j]);
-      }
-      for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
-      if (out_keys) out_keys[rank] = pack_site(cout, yv);
-      ++rank;
+  uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
+  while (word) {
+    const int b = __builtin_ctz(word);
+    word &= word - 1;
+    uint32_t L = static_cast<uint32_t>(w * 32 + b);
+    int32_t yv[kMaxD];
+    for (int j = cout.D - 1; j >= 0; --j) {
+      yv[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
+      L /= static_cast<uint32_t>(E.e[j]);
     }
+    for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
+    if (out_keys) out_keys[rank] = pack_site(cout, yv);
+    ++rank;
   }
 }
 
@@ -1057,7 +1044,7 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   uint64_t lex_cells = 1;
   for (int j = 0; j < rb->D; ++j) lex_cells *= static_cast<uint64_t>(rb->out_size[j]);
   const uint64_t lwords = (lex_cells + 31) / 32;
-  const int64_t lnbw = static_cast<int64_t>((lwords + 4 * kBlock - 1) / (4 * kBlock));
+  const int64_t lnbw = static_cast<int64_t>((lwords + kBlock - 1) / kBlock);
   const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out) + align_up(lwords * 4, 256) +
                        align_up(static_cast<size_t>(lnbw) * 4, 256) +
                        align_up(static_cast<size_t>(N) * 8, 256) + 256;
@@ -1130,7 +1117,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
   uint64_t cells = 1;
   for (int j = 0; j < rb->D; ++j) cells *= static_cast<uint64_t>(rb->out_size[j]);
   const uint64_t nwords = (cells + 31) / 32;
-  const int64_t nbw = static_cast<int64_t>((nwords + 4 * kBlock - 1) / (4 * kBlock));
+  const int64_t nbw = static_cast<int64_t>((nwords + kBlock - 1) / kBlock);
   k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, 0);
   const size_t extra = align_up(nwords * 4, 256) + align_up(nbw * 4, 256) +
                        align_up(static_cast<size_t>(rb->n_cap) * 8, 256) +
