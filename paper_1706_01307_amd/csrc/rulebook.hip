@@ -113,13 +113,22 @@ __device__ void fill_offsets(const OffsetTable& ot, int16_t (*s_off)[kMaxD]) {
 // waves 1..3 packed in bytes 0..2 (each at most 192).
 __device__ void publish_counts(const uint8_t (*s_cnt)[kBlock / kWave], int K,
                                int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre,
-                               int64_t nblk) {
+                               int64_t nblk, int64_t blk) {
   __syncthreads();
   for (int i = threadIdx.x; i < K; i += kBlock) {
     const uint32_t c0 = s_cnt[i][0], c1 = s_cnt[i][1], c2 = s_cnt[i][2], c3 = s_cnt[i][3];
-    blk_cnt[i * nblk + blockIdx.x] = static_cast<int32_t>(c0 + c1 + c2 + c3);
-    wpre[i * nblk + blockIdx.x] = c0 | ((c0 + c1) << 8) | ((c0 + c1 + c2) << 16);
+    blk_cnt[i * nblk + blk] = static_cast<int32_t>(c0 + c1 + c2 + c3);
+    wpre[i * nblk + blk] = c0 | ((c0 + c1) << 8) | ((c0 + c1 + c2) << 16);
   }
+}
+
+// XCD-aware block order for kernels whose neighbouring blocks share data:
+// workgroup b runs on XCD b % 8, so XCD x gets the contiguous block range
+// [x * per, (x + 1) * per) and its L2 holds that stretch of the schedule's
+// neighbourhood.  The grid must be launched with 8 * per workgroups.
+__device__ __forceinline__ int64_t xcd_block() {
+  const int64_t per = gridDim.x / 8;
+  return static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
 }
 
 __device__ __forceinline__ uint32_t wave_prefix(uint32_t packed, int wave) {
@@ -225,6 +234,8 @@ __global__ __launch_bounds__(kBlock) void k_probe(
     const DeviceHeader* __restrict__ hdr, int64_t gstride, Codec crow, Codec cin, Table t,
     OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt,
     uint32_t* __restrict__ wpre, int64_t nblk) {
+  const int64_t blk = xcd_block();
+  if (blk >= nblk) return;
   __shared__ int16_t s_off[kMaxK][kMaxD];
   __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
   fill_offsets(ot, s_off);
@@ -232,7 +243,7 @@ __global__ __launch_bounds__(kBlock) void k_probe(
 
   // thread = schedule position p; its output row is perm[p]
   const int64_t n_rows = hdr->n_out;
-  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const int64_t p = blk * kBlock + threadIdx.x;
   const bool valid = p < n_rows;
   const int wave = threadIdx.x / kWave;
   const int32_t y = valid ? perm[p] : 0;
@@ -298,7 +309,7 @@ __global__ __launch_bounds__(kBlock) void k_probe(
       if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
   }
-  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk);
+  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk, blk);
 }
 
 // One block per offset: exclusive scan of its per-block counts, in place;
@@ -648,6 +659,8 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
     const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g, OffsetTable ot,
     const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
     int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
+  const int64_t blk = xcd_block();
+  if (blk >= nblk) return;
   __shared__ int16_t s_off[kMaxK][kMaxD];
   __shared__ uint32_t s_dil[kMaxK][kMaxD];
   __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
@@ -664,7 +677,7 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
   __syncthreads();
 
   const int64_t n_rows = hdr->n_out;
-  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  const int64_t p = blk * kBlock + threadIdx.x;
   const bool valid = p < n_rows;
   const int wave = threadIdx.x / kWave;
   const int32_t y = valid ? perm[p] : 0;
@@ -707,7 +720,7 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
       if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
     }
   }
-  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk);
+  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk, blk);
 }
 
 // ---------------------------------------------------------------------------
@@ -879,7 +892,7 @@ void launch_scan_compact(spconv_rulebook rb) {
 void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
                                const Codec& cin, const Transient& tr) {
   const OffsetTable ot = make_offsets(rb);
-  const unsigned g = static_cast<unsigned>(rb->nblk);
+  const unsigned g = static_cast<unsigned>(8 * ((rb->nblk + 7) / 8));
   auto launch = [&](auto kern) {
     kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->gstride, crow, cin,
                                        tr.table, ot, rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
@@ -998,7 +1011,7 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
                        const GridBufs& b, uint64_t cells) {
   const OffsetTable ot = make_offsets(rb);
   auto launch = [&](auto kern) {
-    kern<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
+    kern<<<static_cast<unsigned>(8 * ((rb->nblk + 7) / 8)), kBlock, 0, rb->stream>>>(
         rows_sites, rb->perm, rb->hdr, rb->gstride, g, ot, b.grid, static_cast<uint32_t>(cells),
         rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
