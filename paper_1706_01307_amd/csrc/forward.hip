@@ -4,20 +4,21 @@
 // output site).
 //
 // The kernels are output-stationary: a workgroup owns a tile of output rows
-// and keeps their fp32 accumulators in registers while it walks the offsets
-// in ascending order.  For offset i it gathers the input rows G[i][y] of its
-// output rows (the gather map built with the rule book; -1 = no active
-// input, read as zeros) and multiplies them by W^i.  Every output element is
-// written once, by one lane, after a fixed-order sum: no atomics, bitwise
-// reproducible.
+// (consecutive positions of the rule book's Z-order schedule, so the tile is
+// spatially compact) and keeps their fp32 accumulators in registers while it
+// walks the offsets in ascending order.  For offset i it gathers the input
+// rows G[i][p] of its positions (the gather map built with the rule book;
+// 1 + input row, 0 = no active input, read as zeros) and multiplies them by
+// W^i.  Every output element is written once, by one lane, after a
+// fixed-order sum: no atomics, bitwise reproducible.
 //
 //   k_fwd_mfma  dense contraction on the matrix cores: v_mfma 16x16x32 bf16
-//               or 16x16x4 f32.  W^i is staged into LDS transposed (one
-//               padded row per output column) and double-buffered across
-//               offsets; gathered rows go straight from memory to registers
-//               through buffer loads whose hardware range check returns zero
-//               for absent neighbours; a 16-row block whose 16 rows all lack
-//               offset i skips that offset's MFMAs.
+//               or 16x16x4 f32.  W^i is staged into LDS transposed (one row
+//               per output column, XOR-swizzled chunks) and double-buffered
+//               across offsets; gathered rows go straight from memory to
+//               registers through buffer loads whose hardware range check
+//               returns zero for absent neighbours; with 3^3 filters a 16-row
+//               block whose 16 rows all lack offset i skips its MFMAs.
 //   k_fwd_vec   any channel count: one lane per (output row, output column),
 //               fp32 FMA chain.  The low-channel path (e.g. 1 input plane).
 #include <cstdlib>
