@@ -2,7 +2,9 @@
 
 A ctypes wrapper around ``oracle.cpp``, the plain std::map CPU statement of
 the paper's sparse convolutions (Section 3 for the layer definitions,
-Section 4 for the rule book and the forward multiply-add).  Only the test
+including sparse max / average pooling and the deconvolution DC, Section 4
+for the rule book and the forward multiply-add), plus the derivatives of
+those sums that training needs (input, weight and bias gradients).  Only the test
 suite, the smoke check and the benchmark's CPU-baseline leg import this
 package; the product path never does.  It shares no code with the HIP
 library.
@@ -22,7 +24,8 @@ _SRC = os.path.join(_HERE, "oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 OK, EINVAL, EDUP, ERANGE = 0, -1, -2, -3
-VSC, SC = 0, 1
+VSC, SC, DC = 0, 1, 2
+POOL_MAX, POOL_AVG = 0, 1
 F32, BF16 = 0, 1
 
 
@@ -55,6 +58,14 @@ def _load():
     lib.ref_forward.restype = I32
     lib.ref_forward_rows.argtypes = [P, I32, P, P, P, I32, I32, P, P, P]
     lib.ref_forward_rows.restype = I32
+    lib.ref_pool.argtypes = [P, I32, I32, P, I32, P, P]
+    lib.ref_pool.restype = I32
+    lib.ref_dc_forward.argtypes = [P, I32, P, P, P, I32, I32, P, P, P]
+    lib.ref_dc_forward.restype = I32
+    lib.ref_backward_data.argtypes = [P, I32, I32, P, P, I32, I32, P, P]
+    lib.ref_backward_data.restype = I32
+    lib.ref_backward_weight.argtypes = [P, I32, I32, P, P, I32, I32, P, P, P, P]
+    lib.ref_backward_weight.restype = I32
     lib.ref_round.argtypes = [P, I64, I32, P]
     lib.ref_round.restype = I32
     lib.ref_free.argtypes = [P]
@@ -140,6 +151,64 @@ class Rulebook:
         if st != OK:
             raise OracleError(st)
         return y[rows], absb[rows]
+
+    def pool(self, x, mode, dt=F32):
+        """Sparse MP / AP (SC rule book): (y, absb), float64 [n_out, C]."""
+        lib = _load()
+        x = np.ascontiguousarray(x)
+        C = x.shape[1]
+        y = np.zeros((self.n_out, C), np.float64)
+        absb = np.zeros((self.n_out, C), np.float64)
+        st = lib.ref_pool(self._h, mode, dt, _ptr(x), C, _ptr(y), _ptr(absb))
+        if st != OK:
+            raise OracleError(st)
+        return y, absb
+
+    def dc_forward(self, x, w, bias=None, in_dt=F32, x_absb=None):
+        """DC on this SC rule book: x [n_out, C_in] -> (y, absb) [n_in, C_out]."""
+        lib = _load()
+        x = np.ascontiguousarray(x)
+        w = np.ascontiguousarray(w)
+        C_in, C_out = w.shape[1], w.shape[2]
+        y = np.zeros((self.n_in, C_out), np.float64)
+        absb = np.zeros((self.n_in, C_out), np.float64)
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        xa = None if x_absb is None else np.ascontiguousarray(x_absb, dtype=np.float64)
+        st = lib.ref_dc_forward(self._h, in_dt, _ptr(x), _ptr(w), _ptr(b), C_in, C_out,
+                                _ptr(y), _ptr(absb), _ptr(xa))
+        if st != OK:
+            raise OracleError(st)
+        return y, absb
+
+    def backward_data(self, op, dy, w, dt=F32):
+        """Input gradient of op (VSC, SC or DC) given dy: (dx, absb) float64."""
+        lib = _load()
+        dy = np.ascontiguousarray(dy)
+        w = np.ascontiguousarray(w)
+        C_in, C_out = w.shape[1], w.shape[2]
+        rows = self.n_out if op == DC else self.n_in
+        dx = np.zeros((rows, C_in), np.float64)
+        absb = np.zeros((rows, C_in), np.float64)
+        st = lib.ref_backward_data(self._h, op, dt, _ptr(dy), _ptr(w), C_in, C_out,
+                                   _ptr(dx), _ptr(absb))
+        if st != OK:
+            raise OracleError(st)
+        return dx, absb
+
+    def backward_weight(self, op, x, dy, C_in, C_out, dt=F32):
+        """(dw [K, C_in, C_out], db [C_out], absb_w, absb_b), all float64."""
+        lib = _load()
+        x = np.ascontiguousarray(x)
+        dy = np.ascontiguousarray(dy)
+        dw = np.zeros((self.K, C_in, C_out), np.float64)
+        aw = np.zeros_like(dw)
+        db = np.zeros(C_out, np.float64)
+        ab = np.zeros(C_out, np.float64)
+        st = lib.ref_backward_weight(self._h, op, dt, _ptr(x), _ptr(dy), C_in, C_out,
+                                     _ptr(dw), _ptr(db), _ptr(aw), _ptr(ab))
+        if st != OK:
+            raise OracleError(st)
+        return dw, db, aw, ab
 
     def __del__(self):
         h = getattr(self, "_h", None)

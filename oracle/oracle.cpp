@@ -18,7 +18,17 @@
 //   * rule book R = (R_i), R_i a list of (input row, output row) pairs per
 //     filter offset i (Section 4);
 //   * forward: output matrix starts at zero; for every pair of R_i add the
-//     input row times W^i to the output row (Section 4).
+//     input row times W^i to the output row (Section 4);
+//   * max-pooling MP(f,s) and average-pooling AP(f,s) are variants of
+//     SC(.,.,f,s): MP takes the maximum of the zero vector and the input
+//     vectors of the receptive field, AP f^-d times the sum of the active
+//     input vectors (Section 3);
+//   * deconvolution DC(.,.,f,s) inverts SC(.,.,f,s): its active output sites
+//     are the SC input sites and every connection is reversed (Section 3);
+//   * the backward pass (the networks of Section 5 are trained with SGD) is
+//     the derivative of the forward sums: input gradients run every pair in
+//     the opposite direction with W^i transposed, weight gradients sum
+//     input-row x output-gradient-row outer products over R_i.
 //
 // Readings where the paper is silent (each one is listed in the design notes):
 //   * coordinate 0 is the sample index, with f[0] = s[0] = 1, so samples never
@@ -31,7 +41,11 @@
 //     output site: sample index first, then the coordinates' bits level by
 //     level from the most significant, dimension 1 first within a level;
 //   * the bias (optional) is added once at every active output site;
-//   * accumulation is in double, rounded once to the output type (RNE).
+//   * accumulation is in double, rounded once to the output type (RNE);
+//   * MP and AP run on an SC rule book; f^-d is 1 / prod_j f_j over the
+//     spatial dimensions (non-square filters); MP compares with IEEE maxNum
+//     (a NaN input is ignored), so its result is never NaN;
+//   * DC runs on an SC rule book (DC is defined as the inverse of SC).
 #include <algorithm>
 #include <array>
 #include <cmath>
@@ -44,7 +58,8 @@
 namespace {
 
 enum { OK = 0, EINVAL_ = -1, EDUP_ = -2, ERANGE_ = -3 };
-enum { VSC = 0, SC = 1 };
+enum { VSC = 0, SC = 1, DC = 2 };
+enum { POOL_MAX = 0, POOL_AVG = 1 };
 enum { F32 = 0, BF16 = 1 };
 
 using Site = std::array<int32_t, 4>;   // unused trailing entries are 0
@@ -306,6 +321,156 @@ int ref_forward_rows(void* h, int in_dt, const void* x, const void* w,
         }
       }
     }
+  return OK;
+}
+
+// Sparse pooling on an SC rule book.
+//   mode   POOL_MAX (MP) or POOL_AVG (AP)
+//   x      host [n_in][C] of dt (fp32 or bf16 bits)
+//   y      host double [n_out][C]; absb host double [n_out][C] or NULL (AP:
+//          sum |x| / K, the tolerance scale; MP: |y|)
+int ref_pool(void* h, int mode, int dt, const void* x, int C, double* y, double* absb) {
+  if (!h || C < 1 || (dt != F32 && dt != BF16) || (mode != POOL_MAX && mode != POOL_AVG))
+    return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (rb->kind != SC) return EINVAL_;
+  for (int64_t r = 0; r < rb->n_out * C; ++r) {
+    y[r] = 0.0;                        // MP: the zero vector; AP: empty sum
+    if (absb) absb[r] = 0.0;
+  }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i])
+      for (int c = 0; c < C; ++c) {
+        const double v = load(dt, x, pr[0] * C + c);
+        double& o = y[pr[1] * C + c];
+        if (mode == POOL_MAX) {
+          o = std::fmax(o, v);
+        } else {
+          o += v;
+          if (absb) absb[pr[1] * C + c] += std::fabs(v);
+        }
+      }
+  if (mode == POOL_AVG) {
+    const double k = static_cast<double>(rb->K);   // prod_j f_j, f_0 = 1
+    for (int64_t r = 0; r < rb->n_out * C; ++r) {
+      y[r] /= k;
+      if (absb) absb[r] /= k;
+    }
+  } else if (absb) {
+    for (int64_t r = 0; r < rb->n_out * C; ++r) absb[r] = std::fabs(y[r]);
+  }
+  return OK;
+}
+
+// DC forward on an SC rule book: output rows are the SC input rows.
+//   x     host [n_out][C_in] of dt (features on the SC output sites)
+//   w     host [K][C_in][C_out] of dt; bias host fp32 [C_out] or NULL
+//   y     host double [n_in][C_out]: bias + sum_i sum_{(a,b) in R_i} x[b] W^i
+//         into row a;  absb / x_absb as for ref_forward
+int ref_dc_forward(void* h, int dt, const void* x, const void* w, const float* bias,
+                   int C_in, int C_out, double* y, double* absb, const double* x_absb) {
+  if (!h || C_in < 1 || C_out < 1 || (dt != F32 && dt != BF16)) return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (rb->kind != SC) return EINVAL_;
+  for (int64_t r = 0; r < rb->n_in; ++r)
+    for (int n = 0; n < C_out; ++n) {
+      const double b = bias ? static_cast<double>(bias[n]) : 0.0;
+      y[r * C_out + n] = b;
+      if (absb) absb[r * C_out + n] = std::fabs(b);
+    }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i]) {
+      const int64_t src = pr[1], dst = pr[0];       // the SC pair read backwards
+      for (int c = 0; c < C_in; ++c) {
+        const double xv = load(dt, x, src * C_in + c);
+        const double xa = x_absb ? x_absb[src * C_in + c] : std::fabs(xv);
+        for (int n = 0; n < C_out; ++n) {
+          const double wv = load(dt, w, (i * C_in + c) * C_out + n);
+          y[dst * C_out + n] += xv * wv;
+          if (absb) absb[dst * C_out + n] += xa * std::fabs(wv);
+        }
+      }
+    }
+  return OK;
+}
+
+// Gradient with respect to the layer input, given the gradient dy of its
+// output and the weights w [K][C_in][C_out] (dt).
+//   op VSC / SC (rule book of that kind): dx [n_in][C_in],
+//      dx[a] = sum_i sum_{(a,b) in R_i} dy[b] (W^i)^T, dy [n_out][C_out]
+//   op DC (SC rule book): dx [n_out][C_in],
+//      dx[b] = sum_i sum_{(a,b) in R_i} dy[a] (W^i)^T, dy [n_in][C_out]
+//   dx, absb: host double; absb = sum |dy| |w| (the tolerance scale) or NULL
+int ref_backward_data(void* h, int op, int dt, const void* dy, const void* w, int C_in,
+                      int C_out, double* dx, double* absb) {
+  if (!h || C_in < 1 || C_out < 1 || (dt != F32 && dt != BF16)) return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (op == DC ? rb->kind != SC : op != rb->kind) return EINVAL_;
+  const int64_t rows = op == DC ? rb->n_out : rb->n_in;
+  for (int64_t r = 0; r < rows * C_in; ++r) {
+    dx[r] = 0.0;
+    if (absb) absb[r] = 0.0;
+  }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i]) {
+      const int64_t src = op == DC ? pr[0] : pr[1];   // row of dy
+      const int64_t dst = op == DC ? pr[1] : pr[0];   // row of dx
+      for (int n = 0; n < C_out; ++n) {
+        const double g = load(dt, dy, src * C_out + n);
+        for (int c = 0; c < C_in; ++c) {
+          const double wv = load(dt, w, (i * C_in + c) * C_out + n);
+          dx[dst * C_in + c] += g * wv;
+          if (absb) absb[dst * C_in + c] += std::fabs(g) * std::fabs(wv);
+        }
+      }
+    }
+  return OK;
+}
+
+// Gradients of the weights and the bias, given the layer input x and the
+// output gradient dy (both dt).
+//   op VSC / SC: x [n_in][C_in], dy [n_out][C_out],
+//      dw[i][c][n] = sum_{(a,b) in R_i} x[a][c] dy[b][n]
+//   op DC (SC rule book): x [n_out][C_in], dy [n_in][C_out],
+//      dw[i][c][n] = sum_{(a,b) in R_i} x[b][c] dy[a][n]
+//   db[n] = sum of dy[.][n] over all output rows (NULL: skipped)
+//   dw / db / absb_w / absb_b: host double; absb_* (sum of |terms|) or NULL
+int ref_backward_weight(void* h, int op, int dt, const void* x, const void* dy, int C_in,
+                        int C_out, double* dw, double* db, double* absb_w, double* absb_b) {
+  if (!h || C_in < 1 || C_out < 1 || (dt != F32 && dt != BF16)) return EINVAL_;
+  auto* rb = static_cast<Rulebook*>(h);
+  if (op == DC ? rb->kind != SC : op != rb->kind) return EINVAL_;
+  const int64_t nw = rb->K * C_in * C_out;
+  for (int64_t k = 0; k < nw; ++k) {
+    dw[k] = 0.0;
+    if (absb_w) absb_w[k] = 0.0;
+  }
+  for (int64_t i = 0; i < rb->K; ++i)
+    for (const auto& pr : rb->R[i]) {
+      const int64_t xr = op == DC ? pr[1] : pr[0];
+      const int64_t gr = op == DC ? pr[0] : pr[1];
+      for (int c = 0; c < C_in; ++c) {
+        const double xv = load(dt, x, xr * C_in + c);
+        for (int n = 0; n < C_out; ++n) {
+          const double g = load(dt, dy, gr * C_out + n);
+          dw[(i * C_in + c) * C_out + n] += xv * g;
+          if (absb_w) absb_w[(i * C_in + c) * C_out + n] += std::fabs(xv) * std::fabs(g);
+        }
+      }
+    }
+  if (db) {
+    const int64_t out_rows = op == DC ? rb->n_in : rb->n_out;
+    for (int n = 0; n < C_out; ++n) {
+      double s = 0.0, a = 0.0;
+      for (int64_t r = 0; r < out_rows; ++r) {
+        const double g = load(dt, dy, r * C_out + n);
+        s += g;
+        a += std::fabs(g);
+      }
+      db[n] = s;
+      if (absb_b) absb_b[n] = a;
+    }
+  }
   return OK;
 }
 
