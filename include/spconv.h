@@ -63,12 +63,21 @@ typedef enum {
 
 typedef enum { SPCONV_F32 = 0, SPCONV_BF16 = 1 } spconv_dtype;
 typedef enum { SPCONV_VSC = 0, SPCONV_SC = 1 } spconv_kind;
+/* Layer operations for the gradients: the two convolutions and the
+ * deconvolution DC(.,.,f,s), which runs on the rule book of the
+ * SC(.,.,f,s) it inverts (Section 3). */
+typedef enum { SPCONV_OP_VSC = 0, SPCONV_OP_SC = 1, SPCONV_OP_DC = 2 } spconv_op;
+/* Sparse pooling (Section 3: MP(f,s) and AP(f,s), variants of SC). */
+typedef enum { SPCONV_POOL_MAX = 0, SPCONV_POOL_AVG = 1 } spconv_pool_mode;
 
 /* Build flags. */
 enum {
   /* Return as soon as the work is enqueued.  Device-detected errors
    * (EDUP, ERANGE, ECAP) are then reported by spconv_rulebook_status. */
-  SPCONV_BUILD_ASYNC = 1
+  SPCONV_BUILD_ASYNC = 1,
+  /* SC only: also build the transposed rule book (every pair reversed),
+   * which spconv_dc_forward and the SC input gradient walk. */
+  SPCONV_BUILD_TRANSPOSE = 2
 };
 
 typedef struct spconv_rulebook_s* spconv_rulebook;
@@ -86,7 +95,8 @@ typedef struct spconv_rulebook_s* spconv_rulebook;
  *   spatial_size  host int32 [D], grid extent; spatial_size[0] = batch size
  *   f, s          host int32 [D], filter size and stride; f[0] = s[0] = 1;
  *                 VSC needs every f_j odd and every s_j = 1
- *   flags         0 (wait for the device result) or SPCONV_BUILD_ASYNC
+ *   flags         0 (wait for the device result), SPCONV_BUILD_ASYNC, and for
+ *                 SC optionally SPCONV_BUILD_TRANSPOSE (OR-ed)
  *   stream        hipStream_t as void*
  *   out           receives the handle; NULL on any error
  *
@@ -149,6 +159,68 @@ int spconv_vsc_forward(spconv_rulebook rb, int in_dt, const void* x,
 int spconv_sc_forward(spconv_rulebook rb, int in_dt, const void* x,
                       const void* w, const float* bias, int out_dt, void* y,
                       int C_in, int C_out, void* stream);
+
+/* Sparse max- or average-pooling (Section 3: MP(f,s) takes the maximum of
+ * the zero vector and the input vectors of the receptive field, AP(f,s)
+ * f^-d times the sum of the active input vectors; both are variants of
+ * SC(.,.,f,s) and run on its rule book).
+ *   rb      a rule book of kind SPCONV_SC (its f and s are the pooling's)
+ *   mode    SPCONV_POOL_MAX or SPCONV_POOL_AVG
+ *   dt      dtype of x and y (SPCONV_F32 or SPCONV_BF16)
+ *   x       device [n_in][C];  y  device [n_out][C], fully overwritten
+ * MP compares with IEEE maxNum (a NaN input is ignored) and is exact; AP
+ * sums in fp32 in ascending offset order and divides once by prod_j f_j
+ * (f^-d for non-square fields), rounded once to dt.  Asynchronous, allocates
+ * nothing.  Errors: EINVAL (kind, dtype, mode, C < 1, NULL, alignment). */
+int spconv_pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y,
+                        int C, void* stream);
+
+/* Deconvolution DC(.,.,f,s) (Section 3: the inverse of SC(.,.,f,s); its
+ * active output sites are the SC input sites, every connection reversed):
+ * y[a] = bias + sum_i sum_{(a,b) in R_i} x[b] W^i.
+ *   rb      the SC(.,.,f,s) rule book, built with SPCONV_BUILD_TRANSPOSE
+ *   x       device [n_out][C_in] (features on the SC output sites)
+ *   w       device [K][C_in][C_out]; bias fp32 [C_out] or NULL
+ *   y       device [n_in][C_out] (rows in the SC input order), overwritten
+ * Accumulation, rounding and determinism as spconv_vsc_forward.
+ * Errors: EINVAL (kind, no transposed book, dtype, C < 1, NULL). */
+int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
+                      const float* bias, int out_dt, void* y, int C_in, int C_out,
+                      void* stream);
+
+/* Gradient with respect to the input of a layer (the networks of Section 5
+ * are trained by SGD): every pair runs in the opposite direction with W^i
+ * transposed.  C_in, C_out and w ([K][C_in][C_out]) are the layer's.
+ *   op SPCONV_OP_VSC (VSC book):  dy [n_out][C_out] -> dx [n_in][C_in]
+ *   op SPCONV_OP_SC  (SC book built with SPCONV_BUILD_TRANSPOSE):
+ *                                 dy [n_out][C_out] -> dx [n_in][C_in]
+ *   op SPCONV_OP_DC  (SC book):   dy [n_in][C_out]  -> dx [n_out][C_in]
+ * dt is the dtype of dy and w, out_dt that of dx.  fp32 accumulation in a
+ * fixed order, rounded once; deterministic; asynchronous; allocates nothing.
+ * Errors: EINVAL (op / book mismatch, missing transposed book, dtype, NULL). */
+int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, const void* w,
+                         int out_dt, void* dx, int C_in, int C_out, void* stream);
+
+/* Workspace bytes spconv_backward_weight needs for this book, op and shape
+ * (waits for the build).  Errors: EINVAL. */
+int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C_out,
+                                     size_t* bytes);
+
+/* Gradients of the weights and the bias of a layer:
+ *   dw[i][c][n] = sum_{(a,b) in R_i} x[a][c] dy[b][n]        (VSC, SC)
+ *   dw[i][c][n] = sum_{(a,b) in R_i} x[b][c] dy[a][n]        (DC)
+ *   db[n]       = sum over the layer's output rows of dy[.][n]
+ *   x, dy     device, dtype dt, shaped as the layer's input and output
+ *             gradient (see spconv_backward_data)
+ *   dw        device fp32 [K][C_in][C_out], overwritten; db fp32 [C_out] or NULL
+ *   workspace device scratch of at least spconv_backward_weight_workspace
+ *             bytes, owned by the caller (its contents are overwritten)
+ * Each R_i is summed in fixed chunks, and the chunks in ascending order:
+ * deterministic, no atomics.  Asynchronous; allocates nothing.
+ * Errors: EINVAL (op / book mismatch, dtype, NULL, workspace too small). */
+int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy,
+                           float* dw, float* db, int C_in, int C_out, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* Release a rule book (stream-ordered on its build stream).  NULL is a
  * no-op. */

@@ -16,12 +16,14 @@ import ctypes
 import numpy as np
 
 from . import _lib
-from ._lib import (BF16, BUILD_ASYNC, EDUP, EINVAL, ENOMEM, ERANGE, ECAP, EHIP, F32,
-                   OK, SC, VSC, SpconvError)
+from ._lib import (BF16, BUILD_ASYNC, BUILD_TRANSPOSE, EDUP, EINVAL, ENOMEM, ERANGE, ECAP,
+                   EHIP, F32, OK, OP_DC, OP_SC, OP_VSC, POOL_AVG, POOL_MAX, SC, VSC,
+                   SpconvError)
 
-__all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "Rulebook", "build_rulebook",
-           "vsc_forward", "sc_forward", "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE",
-           "ENOMEM", "ECAP", "EHIP"]
+__all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "BUILD_TRANSPOSE", "OP_VSC", "OP_SC",
+           "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "vsc_forward",
+           "sc_forward", "dc_forward", "pool_forward", "backward_data", "backward_weight",
+           "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE", "ENOMEM", "ECAP", "EHIP"]
 
 
 def _torch():
@@ -125,13 +127,16 @@ class Rulebook:
             pass
 
 
-def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, stream=None):
+def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, transpose=False,
+                   stream=None):
     """Build the rule book of one SC / VSC layer on the GPU.
 
     coords: int32 cuda tensor [N, D] (column 0 = sample index).
     spatial_size, f, s: length-D integer sequences, f[0] = s[0] = 1.
     sync=False enqueues the build and returns at once; device-detected
     errors are then reported by Rulebook.status().
+    transpose=True (SC only) also builds the reversed pairs that dc_forward
+    and the SC input gradient need.
     """
     torch = _torch()
     lib = _lib.load()
@@ -146,7 +151,9 @@ def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, stream=N
     st_ptr = _stream_ptr(stream)
     st = lib.spconv_build_rulebook(kind, D, coords.data_ptr() if coords.shape[0] else None,
                                    coords.shape[0], size.ctypes.data, fa.ctypes.data,
-                                   sa.ctypes.data, 0 if sync else BUILD_ASYNC, st_ptr,
+                                   sa.ctypes.data,
+                                   (0 if sync else BUILD_ASYNC) | (BUILD_TRANSPOSE if transpose else 0),
+                                   st_ptr,
                                    ctypes.byref(h))
     _lib.check(st, "spconv_build_rulebook")
     return Rulebook(h, kind, D, st_ptr)
@@ -187,3 +194,93 @@ def vsc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
 def sc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
     """SC forward on an SC rule book (output rows = rb.n_out)."""
     return _forward(_lib.load().spconv_sc_forward, SC, rb, x, w, bias, out_dtype, out, stream)
+
+
+def dc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
+    """Deconvolution DC on the SC rule book it inverts (built with
+    transpose=True): x [n_out, C_in] on the SC output sites -> [n_in, C_out]
+    on the SC input sites."""
+    torch = _torch()
+    if rb.kind != SC:
+        raise ValueError("DC runs on an SC rule book")
+    C_in, C_out = int(w.shape[1]), int(w.shape[2])
+    if w.dtype != x.dtype:
+        raise TypeError("x and w must share a dtype")
+    out_dtype = x.dtype if out_dtype is None else out_dtype
+    x, w = x.contiguous(), w.contiguous()
+    if bias is not None:
+        bias = bias.contiguous()
+        if bias.dtype != torch.float32:
+            raise TypeError("bias must be float32")
+    if out is None:
+        out = torch.empty((rb.n_in, C_out), dtype=out_dtype, device=x.device)
+    if out.numel() == 0:
+        return out
+    st = _lib.load().spconv_dc_forward(
+        rb.handle, _dtype_code(x.dtype), x.data_ptr() if x.numel() else None, w.data_ptr(),
+        bias.data_ptr() if bias is not None else None, _dtype_code(out_dtype), out.data_ptr(),
+        C_in, C_out, _stream_ptr(stream))
+    _lib.check(st, "spconv_dc_forward")
+    return out
+
+
+def pool_forward(rb, x, mode=POOL_MAX, out=None, stream=None):
+    """Sparse MP / AP on an SC rule book: x [n_in, C] -> [n_out, C], same dtype."""
+    torch = _torch()
+    if rb.kind != SC:
+        raise ValueError("pooling runs on an SC rule book")
+    x = x.contiguous()
+    C = int(x.shape[1])
+    if out is None:
+        out = torch.empty((rb.n_out, C), dtype=x.dtype, device=x.device)
+    if out.numel() == 0:
+        return out
+    st = _lib.load().spconv_pool_forward(rb.handle, mode, _dtype_code(x.dtype),
+                                         x.data_ptr() if x.numel() else None, out.data_ptr(), C,
+                                         _stream_ptr(stream))
+    _lib.check(st, "spconv_pool_forward")
+    return out
+
+
+def backward_data(rb, op, dy, w, out_dtype=None, out=None, stream=None):
+    """Input gradient of a VSC / SC / DC layer (w [K, C_in, C_out] the layer's):
+    VSC, SC: dy [n_out, C_out] -> [n_in, C_in]; DC: dy [n_in, C_out] -> [n_out, C_in]."""
+    torch = _torch()
+    C_in, C_out = int(w.shape[1]), int(w.shape[2])
+    if w.dtype != dy.dtype:
+        raise TypeError("dy and w must share a dtype")
+    out_dtype = dy.dtype if out_dtype is None else out_dtype
+    dy, w = dy.contiguous(), w.contiguous()
+    rows = rb.n_out if op == OP_DC else rb.n_in
+    if out is None:
+        out = torch.empty((rows, C_in), dtype=out_dtype, device=dy.device)
+    if out.numel() == 0:
+        return out
+    st = _lib.load().spconv_backward_data(
+        rb.handle, op, _dtype_code(dy.dtype), dy.data_ptr() if dy.numel() else None,
+        w.data_ptr(), _dtype_code(out_dtype), out.data_ptr(), C_in, C_out, _stream_ptr(stream))
+    _lib.check(st, "spconv_backward_data")
+    return out
+
+
+def backward_weight(rb, op, x, dy, C_in, C_out, bias=True, stream=None):
+    """(dw float32 [K, C_in, C_out], db float32 [C_out] or None) of a layer."""
+    torch = _torch()
+    lib = _lib.load()
+    if x.dtype != dy.dtype:
+        raise TypeError("x and dy must share a dtype")
+    x, dy = x.contiguous(), dy.contiguous()
+    nbytes = ctypes.c_size_t()
+    _lib.check(lib.spconv_backward_weight_workspace(rb.handle, op, C_in, C_out,
+                                                     ctypes.byref(nbytes)),
+               "spconv_backward_weight_workspace")
+    ws = torch.empty(int(nbytes.value), dtype=torch.uint8, device=x.device)
+    dw = torch.empty((rb.K, C_in, C_out), dtype=torch.float32, device=x.device)
+    db = torch.empty(C_out, dtype=torch.float32, device=x.device) if bias else None
+    st = lib.spconv_backward_weight(
+        rb.handle, op, _dtype_code(x.dtype), x.data_ptr() if x.numel() else None,
+        dy.data_ptr() if dy.numel() else None, dw.data_ptr(),
+        db.data_ptr() if db is not None else None, C_in, C_out, ws.data_ptr(), ws.numel(),
+        _stream_ptr(stream))
+    _lib.check(st, "spconv_backward_weight")
+    return dw, db

@@ -15,8 +15,10 @@ LIB_PATH = os.path.join(HERE, "libspconv.so")
 
 OK, EINVAL, EDUP, ERANGE, ENOMEM, ECAP, EHIP = 0, -1, -2, -3, -4, -5, -6
 VSC, SC = 0, 1
+OP_VSC, OP_SC, OP_DC = 0, 1, 2
+POOL_MAX, POOL_AVG = 0, 1
 F32, BF16 = 0, 1
-BUILD_ASYNC = 1
+BUILD_ASYNC, BUILD_TRANSPOSE = 1, 2
 
 # Every symbol the header declares, with its ctypes signature.
 _P, _I, _I64, _U = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint
@@ -28,6 +30,11 @@ SIGNATURES = {
     "spconv_rulebook_out_coords": (_I, [_P, ctypes.POINTER(_P)]),
     "spconv_vsc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
     "spconv_sc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
+    "spconv_pool_forward": (_I, [_P, _I, _I, _P, _P, _I, _P]),
+    "spconv_dc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
+    "spconv_backward_data": (_I, [_P, _I, _I, _P, _P, _I, _P, _I, _I, _P]),
+    "spconv_backward_weight_workspace": (_I, [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_size_t)]),
+    "spconv_backward_weight": (_I, [_P, _I, _I, _P, _P, _P, _P, _I, _I, _P, ctypes.c_size_t, _P]),
     "spconv_rulebook_destroy": (None, [_P]),
     "spconv_status_string": (ctypes.c_char_p, [_I]),
 }

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspconv.so")
-SOURCES = ["abi.hip", "rulebook.hip", "forward.hip", "sort.hip"]
+SOURCES = ["abi.hip", "rulebook.hip", "forward.hip", "forward_w0.hip", "forward_w1.hip",
+           "forward_w2.hip", "ops.hip", "sort.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -102,8 +102,11 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   if (kind != SPCONV_VSC && kind != SPCONV_SC) return SPCONV_EINVAL;
   if (D < 2 || D > kMaxD || N < 0 || N >= 0x7fffffffll) return SPCONV_EINVAL;
   if (N > 0 && (!coords || (reinterpret_cast<uintptr_t>(coords) & 3))) return SPCONV_EINVAL;
-  if (!spatial_size || !f || !s || (flags & ~static_cast<unsigned>(SPCONV_BUILD_ASYNC)))
+  if (!spatial_size || !f || !s ||
+      (flags & ~static_cast<unsigned>(SPCONV_BUILD_ASYNC | SPCONV_BUILD_TRANSPOSE)))
     return SPCONV_EINVAL;
+  const bool transpose = (flags & SPCONV_BUILD_TRANSPOSE) != 0;
+  if (transpose && kind != SPCONV_SC) return SPCONV_EINVAL;
   if (f[0] != 1 || s[0] != 1) return SPCONV_EINVAL;
   int64_t K = 1;
   for (int j = 0; j < D; ++j) {
@@ -167,6 +170,8 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   bytes += align_up((Kz + 1) * 8, 256);
   bytes += align_up(Kz * n_cap * 8, 256);
   bytes += align_up(n_cap * 4, 256);
+  const size_t tbytes = transpose ? transpose_bytes(N, K) : 0;
+  bytes += tbytes;
   if (hipMallocAsync(&rb->mem, bytes, rb->stream) != hipSuccess) {
     (void)hipGetLastError();
     delete rb;
@@ -189,8 +194,10 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   rb->pair_off = reinterpret_cast<int64_t*>(take((Kz + 1) * 8));
   rb->pairs = reinterpret_cast<int32_t*>(take(Kz * n_cap * 8));
   rb->perm = reinterpret_cast<int32_t*>(take(n_cap * 4));
+  char* tmem = transpose ? take(tbytes) : nullptr;
 
   int st = kind == SPCONV_VSC ? build_vsc(rb, coords) : build_sc(rb, coords);
+  if (st == SPCONV_OK && transpose) st = build_transpose(rb, coords, tmem);
   if (st != SPCONV_OK) {
     release(rb);
     return st;
@@ -294,6 +301,94 @@ int spconv_sc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
                       const float* bias, int out_dt, void* y, int C_in, int C_out,
                       void* stream) {
   return forward_common(rb, SPCONV_SC, in_dt, x, w, bias, out_dt, y, C_in, C_out, stream);
+}
+
+static bool dtype_ok(int dt) { return dt == SPCONV_F32 || dt == SPCONV_BF16; }
+static bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
+
+int spconv_pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y, int C,
+                        void* stream) {
+  if (!rb || rb->kind != SPCONV_SC || !dtype_ok(dt) || C < 1) return SPCONV_EINVAL;
+  if (mode != SPCONV_POOL_MAX && mode != SPCONV_POOL_AVG) return SPCONV_EINVAL;
+  if (rb->n_cap > 0 && (!y || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
+  if (misaligned(x) || misaligned(y)) return SPCONV_EINVAL;
+  return pool_forward(rb, mode, dt, x, y, C, static_cast<hipStream_t>(stream));
+}
+
+int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
+                      const float* bias, int out_dt, void* y, int C_in, int C_out,
+                      void* stream) {
+  if (!rb || rb->kind != SPCONV_SC || !rb->t_gmap) return SPCONV_EINVAL;
+  if (!dtype_ok(in_dt) || !dtype_ok(out_dt) || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
+  if (rb->n_in > 0 && (!y || !w || (rb->n_cap > 0 && !x))) return SPCONV_EINVAL;
+  if (misaligned(x) || misaligned(w) || misaligned(y) ||
+      (reinterpret_cast<uintptr_t>(bias) & 3))
+    return SPCONV_EINVAL;
+  return forward_view(transpose_view(rb), 0, in_dt, x, w, bias, out_dt, y, C_in, C_out,
+                      static_cast<hipStream_t>(stream));
+}
+
+// The book, view and weight mode an input gradient runs on.
+static int data_grad_view(spconv_rulebook rb, int op, FwdView* v, int* wmode) {
+  if (!rb) return SPCONV_EINVAL;
+  switch (op) {
+    case SPCONV_OP_VSC:
+      if (rb->kind != SPCONV_VSC) return SPCONV_EINVAL;
+      *v = view_of(rb);              // VSC pairs are symmetric: flip the offsets
+      *wmode = 1;
+      return SPCONV_OK;
+    case SPCONV_OP_SC:
+      if (rb->kind != SPCONV_SC || !rb->t_gmap) return SPCONV_EINVAL;
+      *v = transpose_view(rb);       // SC pairs reversed
+      *wmode = 2;
+      return SPCONV_OK;
+    case SPCONV_OP_DC:
+      if (rb->kind != SPCONV_SC) return SPCONV_EINVAL;
+      *v = view_of(rb);              // DC's reversed pairs reversed again
+      *wmode = 2;
+      return SPCONV_OK;
+    default:
+      return SPCONV_EINVAL;
+  }
+}
+
+int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, const void* w,
+                         int out_dt, void* dx, int C_in, int C_out, void* stream) {
+  FwdView v;
+  int wmode = 0;
+  int st = data_grad_view(rb, op, &v, &wmode);
+  if (st != SPCONV_OK) return st;
+  if (!dtype_ok(dt) || !dtype_ok(out_dt) || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
+  if (v.n_cap > 0 && (!dx || !w || (v.n_src > 0 && !dy))) return SPCONV_EINVAL;
+  if (misaligned(dy) || misaligned(w) || misaligned(dx)) return SPCONV_EINVAL;
+  // the kernels' input channels are the layer's output channels
+  return forward_view(v, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in,
+                      static_cast<hipStream_t>(stream));
+}
+
+int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C_out,
+                                     size_t* bytes) {
+  if (!rb || !bytes || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
+  if (op == SPCONV_OP_DC ? rb->kind != SPCONV_SC : op != rb->kind) return SPCONV_EINVAL;
+  *bytes = backward_weight_workspace(rb, C_in, C_out, op);
+  return SPCONV_OK;
+}
+
+int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy,
+                           float* dw, float* db, int C_in, int C_out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (!rb || C_in < 1 || C_out < 1 || !dtype_ok(dt) || !dw) return SPCONV_EINVAL;
+  if (op == SPCONV_OP_DC ? rb->kind != SPCONV_SC : op != rb->kind) return SPCONV_EINVAL;
+  if (!workspace || workspace_bytes < backward_weight_workspace(rb, C_in, C_out, op))
+    return SPCONV_EINVAL;
+  if (rb->n_cap > 0 && (!x || !dy)) return SPCONV_EINVAL;
+  if (misaligned(x) || misaligned(dy) || misaligned(workspace) ||
+      (reinterpret_cast<uintptr_t>(dw) & 3) || (reinterpret_cast<uintptr_t>(db) & 3))
+    return SPCONV_EINVAL;
+  const int st = sync_rulebook(rb);    // the bias gradient needs n_out on the host
+  if (st != SPCONV_OK) return st;
+  return backward_weight(rb, op, dt, x, dy, dw, db, C_in, C_out, workspace,
+                         static_cast<hipStream_t>(stream));
 }
 
 void spconv_rulebook_destroy(spconv_rulebook rb) { release(rb); }

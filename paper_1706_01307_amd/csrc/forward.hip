@@ -1,513 +1,41 @@
-// Forward multiply-add of SC / VSC on gfx950 (Section 4 of the paper: zero
-// the output, then for every offset i and pair j add input row R_i(j,1)
-// times W^i into output row R_i(j,2); Table 1: a*m*n multiply-adds per active
-// output site).
-//
-// The kernels are output-stationary: a workgroup owns a tile of output rows
-// (consecutive positions of the rule book's Z-order schedule, so the tile is
-// spatially compact) and keeps their fp32 accumulators in registers while it
-// walks the offsets in ascending order.  For offset i it gathers the input
-// rows G[i][p] of its positions (the gather map built with the rule book;
-// 1 + input row, 0 = no active input, read as zeros) and multiplies them by
-// W^i.  Every output element is written once, by one lane, after a
-// fixed-order sum: no atomics, bitwise reproducible.
-//
-//   k_fwd_mfma  dense contraction on the matrix cores: v_mfma 16x16x32 bf16
-//               or 16x16x4 f32.  W^i is staged into LDS transposed (one row
-//               per output column, XOR-swizzled chunks) and double-buffered
-//               across offsets; gathered rows go straight from memory to
-//               registers through buffer loads whose hardware range check
-//               returns zero for absent neighbours; with 3^3 filters a 16-row
-//               block whose 16 rows all lack offset i skips its MFMAs.
-//   k_fwd_vec   any channel count: one lane per (output row, output column),
-//               fp32 FMA chain.  The low-channel path (e.g. 1 input plane).
+// Dispatch of the output-stationary multiply-add kernels (kernels in
+// forward_kernels.h, one object file per weight mode).
 #include <cstdlib>
 #include <cstring>
 
 #include "internal.h"
 
 namespace spc {
-namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kWave = 64;
-
-// Test knob: SPCONV_FORCE_PATH=vec runs the vector path for shapes the
-// matrix-core kernel covers.
-bool force_vector_path() {
-  const char* e = std::getenv("SPCONV_FORCE_PATH");
-  return e && std::strcmp(e, "vec") == 0;
+FwdView view_of(spconv_rulebook rb) {
+  FwdView v;
+  v.gmap = rb->gmap;
+  v.perm = rb->perm;
+  v.gstride = rb->gstride;
+  v.hdr = rb->hdr;
+  v.n_cap = rb->n_cap;
+  v.K = rb->K;
+  v.n_src = rb->n_in;
+  return v;
 }
 
-constexpr uint32_t kBufDword3 = 0x00020000u;   // gfx9 raw buffer descriptor word 3
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const void* w,
+                 const float* bias, int out_dt, void* y, int C_in, int C_out,
+                 hipStream_t stream) {
+  if (v.n_cap == 0) return SPCONV_OK;
+  FwdCall c{v, x, 0u, w, bias, y, C_out, stream};
+  switch (wmode) {
+    case 0: forward_run_w0(c, in_dt, out_dt, C_in); break;
+    case 1: forward_run_w1(c, in_dt, out_dt, C_in); break;
+    case 2: forward_run_w2(c, in_dt, out_dt, C_in); break;
+    default: return SPCONV_EINVAL;
+  }
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
-
-// fp32 -> bf16, round to nearest even; NaN stays NaN.
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
-
-template <typename T> struct ElemIO;
-template <> struct ElemIO<float> {
-  __device__ static float load(const float* p, int64_t i) { return p[i]; }
-  __device__ static void store(float* p, int64_t i, float v) { p[i] = v; }
-};
-template <> struct ElemIO<uint16_t> {
-  __device__ static float load(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
-  __device__ static void store(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
-};
-
-// ---------------------------------------------------------------------------
-// Generic (vector ALU) path
-// ---------------------------------------------------------------------------
-template <typename TIn, typename TOut>
-__global__ __launch_bounds__(256) void k_fwd_vec(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
-    const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
-    const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
-    int C_out) {
-  const int64_t n_rows = hdr->n_out;
-  const int64_t total = n_rows * C_out;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-  for (int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; idx < total;
-       idx += stride) {
-    const int64_t p = idx / C_out;                 // schedule position
-    const int col = static_cast<int>(idx - p * C_out);
-    float acc = 0.0f;
-    for (int i = 0; i < K; ++i) {
-      const int32_t g = gmap[i * gstride + p] - 1;
-      if (g < 0) continue;
-      const int64_t xb = static_cast<int64_t>(g) * C_in;
-      const int64_t wb = static_cast<int64_t>(i) * C_in * C_out + col;
-      for (int c = 0; c < C_in; ++c)
-        acc = fmaf(ElemIO<TIn>::load(x, xb + c), ElemIO<TIn>::load(w, wb + c * C_out), acc);
-    }
-    if (bias) acc += bias[col];
-    ElemIO<TOut>::store(y, static_cast<int64_t>(perm[p]) * C_out + col, acc);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Matrix-core path
-// ---------------------------------------------------------------------------
-// Element traits: a lane moves 16 bytes per k-chunk; KC real k per chunk
-// across the 4 lane groups of a 16x16 MFMA.
-template <typename T> struct MT;
-template <> struct MT<uint16_t> {          // bf16
-  static constexpr int KC = 32;            // 8 bf16 per lane x 4 groups
-  static constexpr int T = 8;              // transpose tile (elements per 16 B)
-  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-  }
-};
-template <> struct MT<float> {             // fp32
-  static constexpr int KC = 16;            // 4 fp32 per lane x 4 groups
-  static constexpr int T = 4;
-  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
-    // The 4 elements of a lane's 16-byte chunk are consumed by 4 MFMA steps;
-    // step e pairs A[r][16ch + 4g + e] with B[16ch + 4g + e][c] in every lane
-    // group g, so the 4 steps cover the chunk's 16 k exactly once.
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[e]), __uint_as_float(b[e]), c,
-                                               0, 0, 0);
-    return c;
-  }
-};
-
-template <typename TOut, int NCB> struct OutStore;
-template <int NCB> struct OutStore<float, NCB> {
-  __device__ static void store(float* p, const float* v) {
-    if constexpr (NCB == 4) {
-      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-    } else if constexpr (NCB == 2) {
-      *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
-    } else {
-      p[0] = v[0];
-    }
-  }
-};
-template <int NCB> struct OutStore<uint16_t, NCB> {
-  __device__ static void store(uint16_t* p, const float* v) {
-    if constexpr (NCB == 4) {
-      uint2 u;
-      u.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-      u.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-      *reinterpret_cast<uint2*>(p) = u;
-    } else if constexpr (NCB == 2) {
-      *reinterpret_cast<uint32_t*>(p) =
-          f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-    } else {
-      p[0] = f32_to_bf16(v[0]);
-    }
-  }
-};
-
-__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-}
-
-// LDS image of W^i transposed: one row per output column of the chunk, ROWB
-// bytes of k.  Rows whose length is a multiple of 128 bytes store 16-byte
-// chunk c at c ^ (row & 7) (measured conflict-free for the fragment reads,
-// where 16 lanes read one chunk of 16 consecutive rows; a 16-byte pad per
-// row, used for other lengths, leaves a 2-way conflict).
-template <int ROWB>
-struct WImage {
-  static constexpr bool kSwz = ROWB % 128 == 0;
-  static constexpr int kRowBytes = kSwz ? ROWB : ROWB + 16;
-  __device__ static int at(int row, int byte) {
-    if constexpr (kSwz)
-      return row * kRowBytes + ((((byte >> 4) ^ (row & 7)) << 4) | (byte & 15));
-    else
-      return row * kRowBytes + byte;
-  }
-};
-
-// Tile of the output handled by one workgroup: 4 waves x RB blocks of 16 rows,
-// NCB blocks of 16 columns (the whole workgroup shares one column chunk).
-//
-// Lane layout (16x16 MFMA): lane l = 16 g + r.  A operand: row r of the
-// 16-row block, k-chunk bytes [16 g, 16 g + 16).  B operand: output column
-// r * NCB + cb of the chunk (so a lane ends up owning NCB adjacent columns),
-// same k bytes.  Result: lane l holds rows 4 g + v (v = 0..3), columns
-// r * NCB + cb.
-//
-// Pipeline over the offsets (iteration i): G(i+3) and W^(i+2) are fetched,
-// gathered rows A(i+2) are issued (their gather-map entries G(i+2) arrived
-// one iteration earlier), the MFMAs of offset i run on A(i) and the LDS copy
-// of W^i, and W^(i+1) (fetched one iteration earlier) is written transposed
-// into the other LDS buffer.  One barrier per offset publishes W^(i+1).
-template <typename TIn, int NCH, int NCB, int RB, typename TOut, int KT, bool SKIP = false>
-__global__ __launch_bounds__(256, 2) void k_fwd_mfma(
-    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
-    const DeviceHeader* __restrict__ hdr, int K_arg,
-    const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
-    const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles) {
-  // KT > 0: the offset count is a compile-time constant and the offset loop
-  // is unrolled completely (no loop-carried register hazards).
-  const int K = KT > 0 ? KT : K_arg;
-  constexpr int KC = MT<TIn>::KC;
-  constexpr int CIN = NCH * KC;
-  constexpr int COLS = NCB * 16;
-  constexpr int ESZ = static_cast<int>(sizeof(TIn));
-  constexpr int ROWB = CIN * ESZ;                 // bytes of one input row
-  constexpr int LDWB = WImage<ROWB>::kRowBytes;   // LDS row of W^T (bytes)
-  // W^T staging tasks: bf16 takes 2 k-rows x 8 columns (packed in pairs),
-  // fp32 1 k-row x 4 columns; each task is one 16-byte load per k-row.
-  constexpr int KPT = ESZ == 2 ? 2 : 1;           // k-rows per task
-  constexpr int NPT = 16 / ESZ;                   // columns per task
-  constexpr int NTASK = (CIN / KPT) * (COLS / NPT);
-  constexpr int TPT = (NTASK + 255) / 256;        // tasks per thread
-  constexpr int WAVE_ROWS = RB * 16;
-  constexpr int TILE_ROWS = 4 * WAVE_ROWS;
-
-  __shared__ __attribute__((aligned(16))) unsigned char s_w[2][COLS * LDWB];
-
-  // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
-  // contiguous range of tiles so neighbouring tiles share that XCD's L2.
-  const int64_t per = gridDim.x / 8;
-  const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
-  if (tile >= ntiles) return;
-
-  const int64_t n_rows = hdr->n_out;
-  const int col0 = blockIdx.y * COLS;
-  const int wave = threadIdx.x / kWave;
-  const int lane = threadIdx.x % kWave;
-  const int lr = lane % 16, lg = lane / 16;
-  const int64_t row0 = tile * TILE_ROWS + wave * WAVE_ROWS;
-
-  const __amdgpu_buffer_rsrc_t xr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<TIn*>(x), 0, static_cast<int>(x_bytes),
-                                        static_cast<int>(kBufDword3));
-  constexpr uint32_t kOOB = 0x80000000u;   // past any x_bytes < 2^31: reads as zero
-
-  // ---- W^i -> registers.  Task t = (k-row group kt, column group nt) with nt
-  // fastest, so consecutive lanes read one k-row of the chunk end to end.
-  typedef u32x4 WRegs[TPT][KPT];
-  constexpr int NGRP = COLS / NPT;                // column groups per k-row
-  auto w_load = [&](int i, WRegs& wr) {
-    if (i >= K) return;
-#pragma unroll
-    for (int q = 0; q < TPT; ++q) {
-      // tasks beyond NTASK (only when NTASK is not a multiple of 256) re-read
-      // task 0 and are never stored
-      const int t0 = threadIdx.x + q * 256;
-      const int t = (NTASK % 256 == 0 || t0 < NTASK) ? t0 : 0;
-      const int kt = t / NGRP, nt = t % NGRP;
-      const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
-#pragma unroll
-      for (int r = 0; r < KPT; ++r)
-        wr[q][r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
-    }
-  };
-  // ---- registers -> LDS, transposed: one LDS row per column n holding
-  // W^i[k][n] for all k.  Column n = NCB r + cb (lane r's cb-th column) sits
-  // in LDS row 16 cb + r, so the lanes that read one fragment chunk together
-  // read 16 consecutive rows (spread over the banks by WImage).
-  auto w_row = [](int n) { return (n % NCB) * 16 + n / NCB; };
-  auto w_store = [&](int i, const WRegs& wr) {
-    if (i >= K) return;
-    unsigned char* dst = s_w[i & 1];
-#pragma unroll
-    for (int q = 0; q < TPT; ++q) {
-      const int t = threadIdx.x + q * 256;
-      if (NTASK % 256 == 0 || t < NTASK) {
-        const int kt = t / NGRP, nt = t % NGRP;
-        if constexpr (ESZ == 2) {
-          // pack (W[2kt][n], W[2kt+1][n]) into one 32-bit LDS word per column
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const uint32_t a = wr[q][0][j / 2], b = wr[q][1][j / 2];
-            const uint32_t v = (j & 1) ? ((a >> 16) | (b & 0xffff0000u))
-                                       : ((a & 0xffffu) | (b << 16));
-            *reinterpret_cast<uint32_t*>(&dst[WImage<ROWB>::at(w_row(nt * 8 + j), kt * 4)]) = v;
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<uint32_t*>(&dst[WImage<ROWB>::at(w_row(nt * 4 + j), kt * 4)]) =
-                wr[q][0][j];
-        }
-      }
-    }
-  };
-
-  // ---- gather-map entries of this wave's rows: G[i][row0 + 16 b + r]
-  typedef int32_t GRegs[RB];
-  // Gather-map entries (1 + input row, 0 = none) through buffer loads: an
-  // offset past the map's range reads 0, so rows past the end and offsets
-  // past K need no branch (a load under a divergent branch would force a
-  // full wait for every load in flight).
-  const uint32_t gmap_bytes = static_cast<uint32_t>(gstride * 4);
-  auto g_load = [&](int i, GRegs& g) {
-    const int ic = i < K ? i : 0;
-    const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<int32_t*>(gmap + static_cast<int64_t>(ic) * gstride), 0,
-        static_cast<int>(gmap_bytes), static_cast<int>(kBufDword3));
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      const int64_t row = row0 + b * 16 + lr;
-      const uint32_t off = (i < K && row < n_rows) ? static_cast<uint32_t>(row) * 4u : kOOB;
-      g[b] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(gr, off, 0, 0)) - 1;
-    }
-  };
-  // ---- gathered rows; returns the blocks (bit b) with at least one row
-  typedef u32x4 ARegs[RB][NCH];
-  auto a_load = [&](const GRegs& g, ARegs& a) -> uint32_t {
-    uint32_t pres = 0;
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      const uint32_t base = g[b] >= 0 ? static_cast<uint32_t>(g[b]) * ROWB + lg * 16 : kOOB;
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
-        a[b][ch] = buf_load16(xr, base == kOOB ? kOOB : base + ch * 64);
-      if (__ballot(g[b] >= 0) != 0) pres |= 1u << b;
-    }
-    return pres;
-  };
-
-  f32x4 acc[RB][NCB];
-#pragma unroll
-  for (int b = 0; b < RB; ++b)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[b][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  auto mma = [&](int i, const ARegs& a, uint32_t pres) {
-    const unsigned char* sw = s_w[i & 1];
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      u32x4 bw[NCB];                               // W^i fragments of chunk ch
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-        bw[cb] = *reinterpret_cast<const u32x4*>(
-            &sw[WImage<ROWB>::at(cb * 16 + lr, ch * 64 + lg * 16)]);
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        if (SKIP && !(pres & (1u << b))) continue;   // all 16 rows lack offset i
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-          acc[b][cb] = MT<TIn>::mma(a[b][ch], bw[cb], acc[b][cb]);
-      }
-    }
-  };
-
-  // Three rotating register sets (offsets i, i+1, i+2 modulo 3).
-  GRegs g0, g1, g2;
-  ARegs a0, a1, a2;
-  WRegs w0, w1, w2;
-  uint32_t p0 = 0, p1 = 0, p2 = 0;
-
-  // prologue: W^0 into LDS, W^1 in registers, A(0), A(1), G(2) in flight
-  g_load(0, g0);
-  g_load(1, g1);
-  g_load(2, g2);
-  w_load(0, w0);
-  w_load(1, w1);
-  p0 = a_load(g0, a0);
-  p1 = a_load(g1, a1);
-  w_store(0, w0);
-  __syncthreads();
-
-  // iteration i uses set (i mod 3): A(i) in aU, G(i+2) in gF -> A(i+2) into aF,
-  // G(i+3) into gU; W^(i+1) stored from wN, W^(i+2) loaded into wF.
-  auto step = [&](int i, ARegs& aU, uint32_t& pU, ARegs& aF, uint32_t& pF, GRegs& gU,
-                  GRegs& gF, WRegs& wN, WRegs& wF) {
-    if (i >= K) return;
-    // issue order matters: the in-order load counter lets a later wait for
-    // G(i+3) or W^(i+2) leave the gathered rows issued after them in flight
-    g_load(i + 3, gU);
-    w_load(i + 2, wF);
-    pF = a_load(gF, aF);
-    mma(i, aU, pU);
-    w_store(i + 1, wN);
-    __syncthreads();
-  };
-  if constexpr (KT > 0) {
-#pragma unroll
-    for (int i = 0; i < KT; i += 3) {
-      step(i, a0, p0, a2, p2, g0, g2, w1, w2);
-      step(i + 1, a1, p1, a0, p0, g1, g0, w2, w0);
-      step(i + 2, a2, p2, a1, p1, g2, g1, w0, w1);
-    }
-  } else {
-    for (int i = 0; i < K; i += 3) {
-      step(i, a0, p0, a2, p2, g0, g2, w1, w2);
-      step(i + 1, a1, p1, a0, p0, g1, g0, w2, w0);
-      step(i + 2, a2, p2, a1, p1, g2, g1, w0, w1);
-    }
-  }
-
-  // ---- epilogue: bias, round once, store NCB adjacent columns per lane-row
-  float bv[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
-#pragma unroll
-  for (int b = 0; b < RB; ++b) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
-      if (pos < n_rows) {
-        const int64_t row = perm[pos];
-        float o[NCB];
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
-        OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Dispatch
-// ---------------------------------------------------------------------------
-// Row blocks per wave: fewer when the input rows are wide, so that the two
-// register sets of gathered rows (current and next offset) still fit.
-template <int NCH>
-constexpr int rows_blocks() { return NCH <= 2 ? 4 : (NCH <= 4 ? 2 : 1); }
-
-template <typename TIn, int NCH, int NCB, typename TOut>
-void launch_mfma(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
-                 const float* bias, void* y, int C_out, hipStream_t stream) {
-  constexpr int RB = rows_blocks<NCH>();
-  constexpr int kTileRows = 4 * RB * 16;
-  const int64_t ntiles = (rb->n_cap + kTileRows - 1) / kTileRows;
-  const int64_t per = (ntiles + 7) / 8;
-  dim3 grid(static_cast<unsigned>(8 * per), static_cast<unsigned>(C_out / (NCB * 16)));
-  // 3^3 filters on Z-ordered tiles: whole 16-row blocks often lack an
-  // offset, so the unrolled kernel skips their products
-  auto kern = rb->K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true>
-                          : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0>;
-  kern<<<grid, 256, 0, stream>>>(
-      rb->gmap, rb->perm, rb->gstride, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x), x_bytes,
-      static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_out, ntiles);
-}
-
-template <typename TIn, int NCH, typename TOut>
-void launch_mfma_ncb(spconv_rulebook rb, const void* x, uint32_t x_bytes, const void* w,
-                     const float* bias, void* y, int C_out, hipStream_t stream) {
-  // wide fp32 rows leave no registers for 4 column blocks
-  constexpr bool four = !(sizeof(TIn) == 4 && NCH >= 6);
-  if (four && C_out % 64 == 0)
-    launch_mfma<TIn, NCH, four ? 4 : 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
-  else if (C_out % 32 == 0)
-    launch_mfma<TIn, NCH, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
-  else
-    launch_mfma<TIn, NCH, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream);
-}
-
-template <typename TOut>
-bool try_mfma(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
-              void* y, int C_in, int C_out, hipStream_t stream) {
-  if (C_out % 16 != 0) return false;
-  const uint64_t xb = static_cast<uint64_t>(rb->n_in) * C_in * (in_dt == SPCONV_BF16 ? 2 : 4);
-  // buffer ranges are kept below 2^31 bytes (inputs and one offset's map row)
-  if (xb >= 0x7fffffffull || static_cast<uint64_t>(rb->gstride) * 4 >= 0x7fffffffull) return false;
-  const uint32_t x_bytes = static_cast<uint32_t>(xb);
-  if (in_dt == SPCONV_BF16) {
-    switch (C_in) {
-      case 32: launch_mfma_ncb<uint16_t, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-      case 64: launch_mfma_ncb<uint16_t, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-      case 96: launch_mfma_ncb<uint16_t, 3, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-      case 128: launch_mfma_ncb<uint16_t, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-      default: return false;
-    }
-  }
-  switch (C_in) {
-    case 16: launch_mfma_ncb<float, 1, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-    case 32: launch_mfma_ncb<float, 2, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-    case 64: launch_mfma_ncb<float, 4, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-    case 96: launch_mfma_ncb<float, 6, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-    case 128: launch_mfma_ncb<float, 8, TOut>(rb, x, x_bytes, w, bias, y, C_out, stream); return true;
-    default: return false;
-  }
-}
-
-template <typename TIn, typename TOut>
-void launch_vec(spconv_rulebook rb, const void* x, const void* w, const float* bias, void* y,
-                int C_in, int C_out, hipStream_t stream) {
-  const int64_t total = rb->n_cap * C_out;
-  int64_t blocks = (total + 255) / 256;
-  if (blocks > 65536) blocks = 65536;
-  if (blocks < 1) blocks = 1;
-  k_fwd_vec<TIn, TOut><<<static_cast<unsigned>(blocks), 256, 0, stream>>>(
-      rb->gmap, rb->perm, rb->gstride, rb->hdr, static_cast<int>(rb->K), static_cast<const TIn*>(x),
-      static_cast<const TIn*>(w), bias, static_cast<TOut*>(y), C_in, C_out);
-}
-
-
-}  // namespace
 
 int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w, const float* bias,
             int out_dt, void* y, int C_in, int C_out, hipStream_t stream) {
-  if (rb->n_cap == 0) return SPCONV_OK;
-  bool done = false;
-  if (!force_vector_path()) {
-    done = out_dt == SPCONV_F32
-               ? try_mfma<float>(rb, in_dt, x, w, bias, y, C_in, C_out, stream)
-               : try_mfma<uint16_t>(rb, in_dt, x, w, bias, y, C_in, C_out, stream);
-  }
-  if (!done) {
-    if (in_dt == SPCONV_F32 && out_dt == SPCONV_F32)
-      launch_vec<float, float>(rb, x, w, bias, y, C_in, C_out, stream);
-    else if (in_dt == SPCONV_F32)
-      launch_vec<float, uint16_t>(rb, x, w, bias, y, C_in, C_out, stream);
-    else if (out_dt == SPCONV_F32)
-      launch_vec<uint16_t, float>(rb, x, w, bias, y, C_in, C_out, stream);
-    else
-      launch_vec<uint16_t, uint16_t>(rb, x, w, bias, y, C_in, C_out, stream);
-  }
-  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+  return forward_view(view_of(rb), 0, in_dt, x, w, bias, out_dt, y, C_in, C_out, stream);
 }
 
 }  // namespace spc

@@ -168,6 +168,13 @@ struct spconv_rulebook_s {
   int32_t* pairs;              // [K * n_cap][2]
   int32_t* perm;               // [n_cap] schedule: output rows in Z-order of their sites
   int64_t nblk;                // ceil(n_cap / kBlock)
+  // transposed rule book (SC built with SPCONV_BUILD_TRANSPOSE), or NULL:
+  // the SC input rows ordered by offset class, and for every (offset, position
+  // in that order) 1 + the SC output row paired with that input row
+  spc::DeviceHeader* t_hdr;    // n_out = n_in
+  int32_t* t_perm;             // [n_in]
+  int32_t* t_gmap;             // [K][t_gstride]
+  int64_t t_gstride;
   // host state after synchronisation
   bool synced;
   int status;
@@ -186,10 +193,51 @@ bool radix_sort_pairs(uint64_t* keys, int32_t* vals, uint64_t* keys_tmp, int32_t
                       const DeviceHeader* hdr, int64_t n_cap, int key_bits, void* scratch,
                       hipStream_t stream);
 
-// Forward (forward.hip).
+// Forward (forward.hip).  A view names the gather map the output-stationary
+// kernels walk: for output position p (rows perm[p], p < hdr->n_out <= n_cap)
+// and offset i, gmap[i * gstride + p] = 1 + source row (0: none); n_src rows
+// of the source features.
+struct FwdView {
+  const int32_t* gmap;
+  const int32_t* perm;
+  int64_t gstride;
+  const DeviceHeader* hdr;
+  int64_t n_cap;
+  int64_t K;
+  int64_t n_src;
+};
+FwdView view_of(spconv_rulebook rb);
+struct FwdCall {
+  FwdView v;
+  const void* x;
+  uint32_t x_bytes;
+  const void* w;
+  const float* bias;
+  void* y;
+  int C_out;
+  hipStream_t stream;
+};
+void forward_run_w0(const FwdCall& c, int in_dt, int out_dt, int C_in);
+void forward_run_w1(const FwdCall& c, int in_dt, int out_dt, int C_in);
+void forward_run_w2(const FwdCall& c, int in_dt, int out_dt, int C_in);
+// wmode 0: W^i = w[i] ([K][C_in][C_out]); 1: w[K-1-i]^T; 2: w[i]^T (w given
+// as [K][C_out][C_in] of the layer whose gradient this is).
+int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const void* w,
+                 const float* bias, int out_dt, void* y, int C_in, int C_out,
+                 hipStream_t stream);
 int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
             const float* bias, int out_dt, void* y, int C_in, int C_out,
             hipStream_t stream);
+
+// Pooling, transposed rule book, weight gradients (ops.hip).
+int pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y, int C,
+                 hipStream_t stream);
+size_t transpose_bytes(int64_t n_in, int64_t K);
+int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem);
+FwdView transpose_view(spconv_rulebook rb);
+size_t backward_weight_workspace(spconv_rulebook rb, int C_in, int C_out, int op);
+int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy, float* dw,
+                    float* db, int C_in, int C_out, void* ws, hipStream_t stream);
 
 // Host helpers (abi.cpp).
 Codec make_codec(int D, const int32_t* size);

@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 9, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -79,3 +79,27 @@ def test_other_host_errors():
     assert lib.spconv_rulebook_status(None) == _lib.EINVAL
     assert lib.spconv_rulebook_query(None, None, None, None, None, None) == _lib.EINVAL
     lib.spconv_rulebook_destroy(None)
+
+
+def test_new_entry_points_reject_bad_arguments_on_the_host():
+    """Pooling, DC and gradient entry points: NULL books and bad flags fail
+    before any device work."""
+    lib = _lib.load()
+    E = _lib.EINVAL
+    assert lib.spconv_pool_forward(None, 0, 0, None, None, 4, None) == E
+    assert lib.spconv_dc_forward(None, 0, None, None, None, 0, None, 1, 1, None) == E
+    assert lib.spconv_backward_data(None, 0, 0, None, None, 0, None, 1, 1, None) == E
+    nbytes = ctypes.c_size_t()
+    assert lib.spconv_backward_weight_workspace(None, 0, 1, 1, ctypes.byref(nbytes)) == E
+    assert lib.spconv_backward_weight(None, 0, 0, None, None, None, None, 1, 1, None, 0,
+                                      None) == E
+    # the transposed book exists for SC only; unknown flag bits are rejected
+    size = np.asarray([1, 4, 4], np.int32)
+    f = np.asarray([1, 3, 3], np.int32)
+    s = np.asarray([1, 1, 1], np.int32)
+    h = ctypes.c_void_p()
+    for kind, flags in ((0, _lib.BUILD_TRANSPOSE), (1, 4), (0, 8)):
+        st = lib.spconv_build_rulebook(kind, 3, ctypes.c_void_p(16), 1, size.ctypes.data,
+                                       f.ctypes.data, s.ctypes.data, flags, None,
+                                       ctypes.byref(h))
+        assert st == E and h.value is None

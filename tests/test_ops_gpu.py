@@ -1,0 +1,224 @@
+"""GPU parity of sparse pooling, DC and the gradients against the oracle.
+
+* MP is exact (a maximum of the zero vector and input values), so it is
+  compared bit for bit; AP and everything with products use the features
+  bound of the forward tests: per element |g - o| <= rtol * S and normwise
+  ||g - o|| <= rtol ||o||, with rtol 1e-5 (fp32) / 2e-2 (bf16 in or out).
+* Weight and bias gradients sum up to k_i products per entry in fp32, in
+  chunks of 4096 pairs whose partial sums are then added in order; their
+  tolerance is RTOL_GRAD = 1e-4, ~25x the typical sqrt(n) * 2^-24 error of a
+  4096-term fp32 sum (the worst case n * 2^-24 is 2.4e-4).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import paper_1706_01307_amd as spc  # noqa: E402
+from paper_1706_01307_amd import inputs  # noqa: E402
+from tests.test_parity_gpu import (RTOL_BF16, RTOL_F32, _bf16_tensor, _t,  # noqa: E402
+                                   _to_np, check_features)
+
+pytestmark = pytest.mark.gpu
+
+RTOL_GRAD = 1e-4
+OP = {"vsc": (spc.OP_VSC, oracle.VSC), "sc": (spc.OP_SC, oracle.SC), "dc": (spc.OP_DC, oracle.DC)}
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+
+
+def _feats(n, C, dtype, seed, std=1.0):
+    f = inputs.normal_f32((n, C), std=std, seed=seed)
+    return inputs.to_bf16_bits(f) if dtype == "bf16" else f
+
+
+def _dev(a, dtype):
+    return _bf16_tensor(a) if dtype == "bf16" else _t(a)
+
+
+def _odt(dtype):
+    return oracle.BF16 if dtype == "bf16" else oracle.F32
+
+
+def _pen(n_grids, seed):
+    return inputs.pen_strokes(n_grids, 64, seed=seed), [n_grids, 64, 64]
+
+
+def _surf(n, size, seed):
+    c = inputs.surfaces(n, size, size / 8, size * 0.45, seed=seed, variant="literal")
+    return c, [n, size, size, size]
+
+
+def _sites(case):
+    if case == "pen":
+        return _pen(16, 3)
+    if case == "surf":
+        return _surf(2, 48, 5)
+    raise ValueError(case)
+
+
+# ---------------------------------------------------------------------------
+# Pooling
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case,f,s,C,dtype", [
+    ("pen", [1, 2, 2], [1, 2, 2], 32, "f32"),
+    ("pen", [1, 3, 3], [1, 2, 2], 5, "f32"),
+    ("pen", [1, 2, 3], [1, 2, 3], 16, "bf16"),
+    ("surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, "bf16"),
+    ("surf", [1, 3, 3, 3], [1, 2, 2, 2], 8, "f32"),
+])
+def test_pool_matches_oracle(case, f, s, C, dtype):
+    coords, size = _sites(case)
+    _say(f"[pool] {case} N={len(coords)} f={f} s={s} C={C} {dtype}")
+    x = _feats(len(coords), C, dtype, 41)
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, f, s)
+    ref = oracle.Rulebook(oracle.SC, coords, size, f, s)
+    xd = _dev(x, dtype)
+    mp = spc.pool_forward(rb, xd, spc.POOL_MAX)
+    ap = spc.pool_forward(rb, xd, spc.POOL_AVG)
+    torch.cuda.synchronize()
+    mo, _ = ref.pool(x, oracle.POOL_MAX, _odt(dtype))
+    ao, absb = ref.pool(x, oracle.POOL_AVG, _odt(dtype))
+    want = oracle.round_to(mo, _odt(dtype))
+    got = mp.view(torch.int16).cpu().numpy().view(np.uint16) if dtype == "bf16" else mp.cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    check_features(_to_np(ap), ao, absb, RTOL_F32 if dtype == "f32" else RTOL_BF16, "AP")
+
+
+def test_pool_max_ignores_nan_and_empty_input():
+    coords, size = _pen(2, 9)
+    x = _feats(len(coords), 8, "f32", 3)
+    x[5, 2] = np.nan
+    x[17, :] = np.nan
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2], [1, 2, 2])
+    got = spc.pool_forward(rb, _t(x), spc.POOL_MAX).cpu().numpy()
+    ref = oracle.Rulebook(oracle.SC, coords, size, [1, 2, 2], [1, 2, 2])
+    want = ref.pool(x, oracle.POOL_MAX)[0].astype(np.float32)
+    assert not np.isnan(got).any()
+    np.testing.assert_array_equal(got, want)
+    empty = spc.build_rulebook(spc.SC, _t(np.zeros((0, 3), np.int32)), size, [1, 2, 2], [1, 2, 2])
+    out = spc.pool_forward(empty, torch.zeros((0, 8), device="cuda"), spc.POOL_AVG)
+    assert out.shape == (0, 8)
+
+
+# ---------------------------------------------------------------------------
+# Deconvolution
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case,f,s,C_in,C_out,dtype", [
+    ("pen", [1, 2, 2], [1, 2, 2], 32, 32, "f32"),
+    ("pen", [1, 3, 3], [1, 2, 2], 1, 16, "f32"),
+    ("pen", [1, 3, 3], [1, 2, 2], 16, 16, "f32"),
+    ("surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 32, "bf16"),
+    ("surf", [1, 2, 2, 2], [1, 2, 2, 2], 64, 32, "bf16"),
+    ("surf", [1, 3, 3, 3], [1, 2, 2, 2], 32, 16, "f32"),
+])
+def test_dc_matches_oracle(case, f, s, C_in, C_out, dtype):
+    coords, size = _sites(case)
+    K = int(np.prod(f))
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, f, s, transpose=True)
+    ref = oracle.Rulebook(oracle.SC, coords, size, f, s)
+    _say(f"[dc] {case} N={len(coords)} -> {ref.n_out} f={f} s={s} C={C_in}->{C_out} {dtype}")
+    x = _feats(ref.n_out, C_in, dtype, 51)
+    wf = inputs.normal_f32((K, C_in, C_out), std=1.0 / np.sqrt(K * C_in), seed=52)
+    w = inputs.to_bf16_bits(wf) if dtype == "bf16" else wf
+    b = inputs.normal_f32((C_out,), std=0.1, seed=53)
+    y = spc.dc_forward(rb, _dev(x, dtype), _dev(w, dtype), _t(b))
+    yo, absb = ref.dc_forward(x, w, b, in_dt=_odt(dtype))
+    check_features(_to_np(y), yo, absb, RTOL_F32 if dtype == "f32" else RTOL_BF16, "DC")
+    y2 = spc.dc_forward(rb, _dev(x, dtype), _dev(w, dtype), _t(b))
+    assert torch.equal(y, y2)                    # bitwise reproducible
+
+
+def test_dc_needs_the_transposed_book():
+    coords, size = _pen(2, 4)
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2], [1, 2, 2])
+    x = torch.zeros((rb.n_out, 16), device="cuda")
+    w = torch.zeros((4, 16, 16), device="cuda")
+    with pytest.raises(spc.SpconvError):
+        spc.dc_forward(rb, x, w)
+    with pytest.raises(spc.SpconvError):
+        spc.backward_data(rb, spc.OP_SC, torch.zeros((rb.n_out, 16), device="cuda"), w)
+
+
+# ---------------------------------------------------------------------------
+# Gradients
+# ---------------------------------------------------------------------------
+
+GRAD_CASES = [
+    ("vsc", "pen", [1, 3, 3], None, 32, 32, "f32"),
+    ("vsc", "pen", [1, 3, 3], None, 1, 16, "f32"),
+    ("vsc", "surf", [1, 3, 3, 3], None, 32, 32, "bf16"),
+    ("vsc", "surf", [1, 3, 3, 3], None, 64, 64, "bf16"),
+    ("vsc", "surf", [1, 3, 3, 3], None, 16, 32, "f32"),
+    ("sc", "pen", [1, 2, 2], [1, 2, 2], 32, 32, "f32"),
+    ("sc", "pen", [1, 3, 3], [1, 2, 2], 16, 32, "bf16"),
+    ("sc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 64, "bf16"),
+    ("dc", "pen", [1, 2, 2], [1, 2, 2], 32, 16, "f32"),
+    ("dc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 64, 32, "bf16"),
+]
+
+
+def _grad_setup(op, case, f, s, C_in, C_out, dtype):
+    coords, size = _sites(case)
+    kind = spc.VSC if op == "vsc" else spc.SC
+    s = s or [1] * len(f)
+    rb = spc.build_rulebook(kind, _t(coords), size, f, s, transpose=(op == "sc"))
+    ref = oracle.Rulebook(kind, coords, size, f, s)
+    in_rows = ref.n_out if op == "dc" else ref.n_in
+    out_rows = ref.n_in if op == "dc" else ref.n_out
+    K = ref.K
+    x = _feats(in_rows, C_in, dtype, 61)
+    dy = _feats(out_rows, C_out, dtype, 62)
+    wf = inputs.normal_f32((K, C_in, C_out), std=1.0 / np.sqrt(K * C_in), seed=63)
+    w = inputs.to_bf16_bits(wf) if dtype == "bf16" else wf
+    return coords, rb, ref, x, dy, w
+
+
+@pytest.mark.parametrize("op,case,f,s,C_in,C_out,dtype", GRAD_CASES)
+def test_input_gradient_matches_oracle(op, case, f, s, C_in, C_out, dtype):
+    coords, rb, ref, x, dy, w = _grad_setup(op, case, f, s, C_in, C_out, dtype)
+    _say(f"[dx] {op} {case} N={len(coords)} f={f} C={C_in}->{C_out} {dtype}")
+    dx = spc.backward_data(rb, OP[op][0], _dev(dy, dtype), _dev(w, dtype))
+    dxo, absb = ref.backward_data(OP[op][1], dy, w, _odt(dtype))
+    check_features(_to_np(dx), dxo, absb, RTOL_F32 if dtype == "f32" else RTOL_BF16, "dx")
+    dx2 = spc.backward_data(rb, OP[op][0], _dev(dy, dtype), _dev(w, dtype))
+    assert torch.equal(dx, dx2)
+
+
+@pytest.mark.parametrize("op,case,f,s,C_in,C_out,dtype", GRAD_CASES)
+def test_weight_gradient_matches_oracle(op, case, f, s, C_in, C_out, dtype):
+    coords, rb, ref, x, dy, w = _grad_setup(op, case, f, s, C_in, C_out, dtype)
+    _say(f"[dw] {op} {case} N={len(coords)} f={f} C={C_in}->{C_out} {dtype}")
+    dw, db = spc.backward_weight(rb, OP[op][0], _dev(x, dtype), _dev(dy, dtype), C_in, C_out)
+    dwo, dbo, aw, ab = ref.backward_weight(OP[op][1], x, dy, C_in, C_out, _odt(dtype))
+    check_features(dw.cpu().numpy(), dwo, aw, RTOL_GRAD, "dw")
+    check_features(db.cpu().numpy(), dbo, ab, RTOL_GRAD, "db")
+    dw2, db2 = spc.backward_weight(rb, OP[op][0], _dev(x, dtype), _dev(dy, dtype), C_in, C_out)
+    assert torch.equal(dw, dw2) and torch.equal(db, db2)
+
+
+def test_gradient_op_must_match_the_book():
+    coords, size = _pen(2, 6)
+    vsc = spc.build_rulebook(spc.VSC, _t(coords), size, [1, 3, 3])
+    w = torch.zeros((9, 8, 8), device="cuda")
+    dy = torch.zeros((len(coords), 8), device="cuda")
+    for op in (spc.OP_SC, spc.OP_DC):
+        with pytest.raises(spc.SpconvError):
+            spc.backward_data(vsc, op, dy, w)
+        with pytest.raises(spc.SpconvError):
+            spc.backward_weight(vsc, op, dy, dy, 8, 8)
