@@ -14,7 +14,8 @@ Prints one JSON line:
 
 Other modes (not the benchmark line): --workload with a multi-layer stack
 (VSC levels joined by SC) times the whole stack; --peaks measures a plain
-device copy and a library bf16 GEMM as achievable-peak references.
+device copy and a library bf16 GEMM as achievable-peak references; --ops
+times sparse pooling, DC and the gradients (one JSON line per op).
 """
 from __future__ import annotations
 
@@ -52,6 +53,8 @@ def _args():
                    help="run one plain device copy of this many MiB (counter calibration)")
     p.add_argument("--peaks", action="store_true",
                    help="measure a device copy and a bf16 library GEMM instead")
+    p.add_argument("--ops", action="store_true",
+                   help="time pooling, DC and the gradients instead")
     return p.parse_args()
 
 
@@ -108,6 +111,9 @@ def main():
     dev = torch.device("cuda:0")
     if a.peaks:
         measure_peaks(torch, dev)
+        return
+    if a.ops:
+        run_ops(a, torch, dev, spc, inputs)
         return
     wl = inputs.make_workload(a.workload, variant=a.variant)
     if len(wl.layers) > 1:
@@ -368,6 +374,101 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
         "effective_tflops": flops / (ms * 1e-3) / 1e12,
         "bytes_features": int(sum(r["n_in"] * r["c_in"] * esz + r["n_out"] * r["c_out"] * esz
                                   for r in info))}), flush=True)
+
+
+def run_ops(a, torch, dev, spc, inputs):
+    """Pooling, DC and gradients on the workloads they belong to, one JSON
+    line each: the level-0 sites of the 4 x 256^3 encoder (2^3 stride-2 SC:
+    pooling, DC, the SC gradients) and the 8 x 128^3 headline VSC layer (its
+    input and weight gradients).  Each line gives the mean time per call from
+    HIP events on the stream the library runs on, and achieved / peak for the
+    bound that applies (algorithmic bytes or FLOPs per call)."""
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(a.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record(stream)
+        for _ in range(a.steps):
+            fn()
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / a.steps
+
+    def feats(n, c, seed):
+        f = inputs.normal_f32((n, c), seed=seed)
+        return torch.from_numpy(inputs.to_bf16_bits(f).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def weights(K, ci, co, seed):
+        f = inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci), seed=seed)
+        return torch.from_numpy(inputs.to_bf16_bits(f).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def emit(op, workload, ms, bound, achieved, unit, peak, extra):
+        print(json.dumps({"op": op, "workload": workload, "ms_per_call": ms,
+                          "calls": a.steps, "dtype": "bf16",
+                          "roofline": {"bound": bound, "achieved": achieved, "peak": peak,
+                                       "unit": unit, "frac": achieved / peak},
+                          **extra}), flush=True)
+
+    # ---- encoder level 0: 2^3 stride-2 SC on 4 x 256^3 surfaces
+    wl = inputs.make_workload("surf256x4_unet_enc_bf16", variant=a.variant)
+    ct = torch.from_numpy(np.ascontiguousarray(wl.coords)).to(dev)
+    n_in = len(wl.coords)
+    f2 = [1, 2, 2, 2]
+    rb = spc.build_rulebook(spc.SC, ct, wl.spatial_size, f2, f2, transpose=True)
+    n_out, K = rb.n_out, rb.K
+    sum_k = int(rb.pair_off[-1])
+    C = 32
+    x = feats(n_in, C, 21)
+    y = torch.empty((n_out, C), dtype=torch.bfloat16, device=dev)
+    for mode, name in ((spc.POOL_MAX, "max_pool_2x2x2_s2"), (spc.POOL_AVG, "avg_pool_2x2x2_s2")):
+        ms = timed(lambda: spc.pool_forward(rb, x, mode, out=y))
+        nbytes = n_in * C * 2 + n_out * C * 2 + 4 * K * n_out
+        emit(name, "surf256x4 level 0", ms, "hbm", nbytes / (ms * 1e-3) / 1e9, "GB/s",
+             PEAKS["hbm"], {"n_in": n_in, "n_out": n_out, "C": C, "algorithmic_bytes": nbytes})
+    # DC 2^3 stride 2 (decoder upsampling, 64 -> 32 planes), SC input gradient
+    ci, co = 64, 32
+    xd = feats(n_out, ci, 22)
+    wd = weights(K, ci, co, 23)
+    yd = torch.empty((n_in, co), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: spc.dc_forward(rb, xd, wd, out=yd))
+    fl = 2.0 * sum_k * ci * co
+    emit("dc_2x2x2_s2_c64_c32", "surf256x4 level 0", ms, "mfma", fl / (ms * 1e-3) / 1e12,
+         "TFLOP/s", PEAKS["bf16"], {"n_in": n_out, "n_out": n_in, "sum_k": sum_k})
+    wsc = weights(K, co, ci, 24)                 # SC(32 -> 64) weights
+    dysc = feats(n_out, ci, 25)
+    dxsc = torch.empty((n_in, co), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: spc.backward_data(rb, spc.OP_SC, dysc, wsc, out=dxsc))
+    emit("sc_input_grad_2x2x2_s2_c32_c64", "surf256x4 level 0", ms, "mfma",
+         fl / (ms * 1e-3) / 1e12, "TFLOP/s", PEAKS["bf16"], {"sum_k": sum_k})
+    xsc = feats(n_in, co, 26)
+    ms = timed(lambda: spc.backward_weight(rb, spc.OP_SC, xsc, dysc, co, ci))
+    emit("sc_weight_grad_2x2x2_s2_c32_c64", "surf256x4 level 0", ms, "mfma",
+         fl / (ms * 1e-3) / 1e12, "TFLOP/s", PEAKS["bf16"], {"sum_k": sum_k})
+    rb.close()
+    del x, y, xd, yd, dysc, dxsc, xsc
+
+    # ---- headline VSC layer: input and weight gradients
+    wl = inputs.make_workload("surf128x8_vsc3_c64_bf16", variant=a.variant)
+    ct = torch.from_numpy(np.ascontiguousarray(wl.coords)).to(dev)
+    N = len(wl.coords)
+    rb = spc.build_rulebook(spc.VSC, ct, wl.spatial_size, [1, 3, 3, 3])
+    sum_k = int(rb.pair_off[-1])
+    C = 64
+    w = weights(27, C, C, 31)
+    dy = feats(N, C, 32)
+    xv = feats(N, C, 33)
+    dx = torch.empty((N, C), dtype=torch.bfloat16, device=dev)
+    fl = 2.0 * sum_k * C * C
+    ms = timed(lambda: spc.backward_data(rb, spc.OP_VSC, dy, w, out=dx))
+    emit("vsc_input_grad_3x3x3_c64", "surf128x8", ms, "mfma", fl / (ms * 1e-3) / 1e12,
+         "TFLOP/s", PEAKS["bf16"], {"active_sites": N, "sum_k": sum_k})
+    ms = timed(lambda: spc.backward_weight(rb, spc.OP_VSC, xv, dy, C, C))
+    emit("vsc_weight_grad_3x3x3_c64", "surf128x8", ms, "mfma", fl / (ms * 1e-3) / 1e12,
+         "TFLOP/s", PEAKS["bf16"], {"active_sites": N, "sum_k": sum_k})
+    rb.close()
 
 
 if __name__ == "__main__":

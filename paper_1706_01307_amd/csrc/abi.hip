@@ -324,8 +324,12 @@ int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
   if (misaligned(x) || misaligned(w) || misaligned(y) ||
       (reinterpret_cast<uintptr_t>(bias) & 3))
     return SPCONV_EINVAL;
-  return forward_view(transpose_view(rb), 0, in_dt, x, w, bias, out_dt, y, C_in, C_out,
-                      static_cast<hipStream_t>(stream));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (rb->t_single && rb->n_in > 0) {
+    const int r = transpose_single(rb, 0, in_dt, x, w, bias, out_dt, y, C_in, C_out, st);
+    if (r != kNotSingle) return r;
+  }
+  return forward_view(transpose_view(rb), 0, in_dt, x, w, bias, out_dt, y, C_in, C_out, st);
 }
 
 // The book, view and weight mode an input gradient runs on.
@@ -356,14 +360,18 @@ int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, con
                          int out_dt, void* dx, int C_in, int C_out, void* stream) {
   FwdView v;
   int wmode = 0;
-  int st = data_grad_view(rb, op, &v, &wmode);
-  if (st != SPCONV_OK) return st;
+  const int vs = data_grad_view(rb, op, &v, &wmode);
+  if (vs != SPCONV_OK) return vs;
   if (!dtype_ok(dt) || !dtype_ok(out_dt) || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
   if (v.n_cap > 0 && (!dx || !w || (v.n_src > 0 && !dy))) return SPCONV_EINVAL;
   if (misaligned(dy) || misaligned(w) || misaligned(dx)) return SPCONV_EINVAL;
   // the kernels' input channels are the layer's output channels
-  return forward_view(v, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in,
-                      static_cast<hipStream_t>(stream));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (op == SPCONV_OP_SC && rb->t_single && rb->n_in > 0) {
+    const int r = transpose_single(rb, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in, st);
+    if (r != kNotSingle) return r;
+  }
+  return forward_view(v, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in, st);
 }
 
 int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C_out,

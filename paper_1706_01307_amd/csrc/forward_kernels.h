@@ -17,8 +17,9 @@
 //               per output column, XOR-swizzled chunks) and double-buffered
 //               across offsets; gathered rows go straight from memory to
 //               registers through buffer loads whose hardware range check
-//               returns zero for absent neighbours; with 3^3 filters a 16-row
-//               block whose 16 rows all lack offset i skips its MFMAs.
+//               returns zero for absent neighbours; a 16-row block whose 16
+//               rows all lack offset i skips its MFMAs (and, for filters
+//               other than 3^3, its gathers).
 //   k_fwd_vec   any channel count: one lane per (output row, output column),
 //               fp32 FMA chain.  The low-channel path (e.g. 1 input plane).
 #pragma once
@@ -204,7 +205,7 @@ struct WImage {
 // of W^i, and W^(i+1) (fetched one iteration earlier) is written transposed
 // into the other LDS buffer.  One barrier per offset publishes W^(i+1).
 template <typename TIn, int NCH, int NCB, int RB, typename TOut, int KT, bool SKIP = false,
-          int WT = 0>
+          int WT = 0, bool LSKIP = false>
 __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K_arg,
@@ -234,9 +235,10 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   // contiguous range of tiles so neighbouring tiles share that XCD's L2.
   const int64_t per = gridDim.x / 8;
   const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
-  if (tile >= ntiles) return;
-
   const int64_t n_rows = hdr->n_out;
+  // tiles past the device-side row count (the grid is sized for a bound)
+  if (tile >= ntiles || tile * TILE_ROWS >= n_rows) return;
+
   const int col0 = blockIdx.y * COLS;
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
@@ -354,10 +356,18 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       const uint32_t base = g[b] >= 0 ? static_cast<uint32_t>(g[b]) * ROWB + lg * 16 : kOOB;
+      const bool any = __ballot(g[b] >= 0) != 0;
+      if (!LSKIP || any) {
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
-        a[b][ch] = buf_load16(xr, base == kOOB ? kOOB : base + ch * 64);
-      if (__ballot(g[b] >= 0) != 0) pres |= 1u << b;
+        for (int ch = 0; ch < NCH; ++ch)
+          a[b][ch] = buf_load16(xr, base == kOOB ? kOOB : base + ch * 64);
+      } else {
+        // a block with no row at this offset: no loads (its products are
+        // skipped as well)
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) a[b][ch] = u32x4{0u, 0u, 0u, 0u};
+      }
+      if (any) pres |= 1u << b;
     }
     return pres;
   };
@@ -470,10 +480,12 @@ void launch_mfma(const Call& c) {
   const int64_t ntiles = (c.v.n_cap + kTileRows - 1) / kTileRows;
   const int64_t per = (ntiles + 7) / 8;
   dim3 grid(static_cast<unsigned>(8 * per), static_cast<unsigned>(c.C_out / (NCB * 16)));
-  // 3^3 filters on Z-ordered tiles: whole 16-row blocks often lack an
-  // offset, so the unrolled kernel skips their products
+  // Whole 16-row blocks that lack an offset skip their products.  3^3
+  // filters run the unrolled kernel; other filters (strided SC, DC and the
+  // SC input gradient, whose rows come ordered by offset class so that most
+  // blocks take one offset only) also skip the blocks' gathers.
   auto kern = c.v.K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
-                          : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, false, WT>;
+                          : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
   kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), c.x_bytes, static_cast<const TIn*>(c.w), c.bias,

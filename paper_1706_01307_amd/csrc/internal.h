@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <vector>
 
 #include "spconv.h"
 
@@ -175,6 +176,11 @@ struct spconv_rulebook_s {
   int32_t* t_perm;             // [n_in]
   int32_t* t_gmap;             // [K][t_gstride]
   int64_t t_gstride;
+  bool t_single;               // f = s: R_i also split into t_src / t_dst
+  int32_t* t_src;              // [sum k] 1 + SC output row, R_0 first
+  int32_t* t_dst;              // [sum k] SC input row
+  spc::DeviceHeader* t_hdrs;   // [K] n_out = k_i
+  std::vector<int64_t> h_pair_off;   // host copy of pair_off, filled on first use
   // host state after synchronisation
   bool synced;
   int status;
@@ -235,6 +241,10 @@ int pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y, i
 size_t transpose_bytes(int64_t n_in, int64_t K);
 int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem);
 FwdView transpose_view(spconv_rulebook rb);
+constexpr int kNotSingle = 1;
+int transpose_single(spconv_rulebook rb, int wmode, int in_dt, const void* x, const void* w,
+                     const float* bias, int out_dt, void* y, int C_in, int C_out,
+                     hipStream_t st);
 size_t backward_weight_workspace(spconv_rulebook rb, int C_in, int C_out, int op);
 int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy, float* dw,
                     float* db, int C_in, int C_out, void* ws, hipStream_t stream);

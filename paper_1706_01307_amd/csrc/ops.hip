@@ -19,12 +19,19 @@
 //                              whose input row sits at position q (each
 //                              (offset, input row) has at most one pair)
 // The output-stationary forward kernels then run DC and the input gradients
-// over this map.
+// over this map.  When f = s every SC input row has exactly one pair, and
+// the rule book also keeps R_i split into its two columns (source rows + 1,
+// destination rows) with a per-offset row count:
+//   k_split_pairs, k_offset_counts
+// so DC and the SC input gradient run one gather-multiply-store launch per
+// offset (the forward kernels with a single offset), with no empty offsets to
+// walk.
 //
 // Weight gradient dW^i = sum over the pairs of R_i of (input row)^T x (output
 // gradient row): R_i is cut into chunks of kChunk pairs; one workgroup forms
-// the fp32 partial product of a chunk for a 64x64 tile of dW^i (pairs staged
-// in LDS, 4x4 outputs per lane, pairs in list order), and a second kernel
+// the fp32 partial product of a chunk for a 64x64 tile of dW^i (bf16: on the
+// matrix cores, pairs gathered row-major into LDS and read back transposed;
+// fp32 and odd widths: vector ALU, 4x4 outputs per lane), and a second kernel
 // adds the chunks of every entry in ascending chunk order.  The bias
 // gradient sums the output-gradient rows in fixed row chunks the same way.
 // No atomics anywhere: results are bitwise reproducible.
@@ -183,6 +190,29 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t* __restrict__ a, int32
     a[r] = v;
 }
 
+// pairs (a, b) of the whole book -> src[e] = b + 1, dst[e] = a
+__global__ __launch_bounds__(256) void k_split_pairs(const int32_t* __restrict__ pairs,
+                                                     const int64_t* __restrict__ pair_off, int K,
+                                                     int32_t* __restrict__ src,
+                                                     int32_t* __restrict__ dst) {
+  const int64_t total = pair_off[K];
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += stride) {
+    src[e] = pairs[2 * e + 1] + 1;
+    dst[e] = pairs[2 * e];
+  }
+}
+
+__global__ void k_offset_counts(const int64_t* __restrict__ pair_off, int K,
+                                DeviceHeader* __restrict__ h) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < K) {
+    h[i].status = 0;
+    h[i].n_out = pair_off[i + 1] - pair_off[i];
+  }
+}
+
 __global__ void k_set_rows(DeviceHeader* h, int64_t n) {
   if (threadIdx.x == 0) {
     h->status = 0;
@@ -286,7 +316,159 @@ __global__ __launch_bounds__(256) void k_dw_partial(
   }
 }
 
-// dw[i][c][n] = sum over the chunks of R_i, in ascending chunk order.
+// Matrix-core partial products (bf16 inputs, fp32 accumulation): grid
+// (chunk, offset, 64x64 tile of dW^i).  Per step 128 pairs: their input rows
+// and gradient rows (this tile's 64 columns of each) are gathered into LDS
+// row-major, 8 lanes per 128-byte row; wave w multiplies pairs 32w..32w+31
+// of the step into its own 64x64 fp32 partial.  The contraction runs over
+// pairs, so an operand fragment holds one channel of 8 consecutive pairs: it
+// comes from the row-major tile through gfx950's transposing LDS read (16
+// lanes read 4 pairs x 16 channels, each lane receives one channel of the 4
+// pairs).  At the end of the chunk the 4 wave partials are added in wave
+// order through LDS.  Columns past C_in / C_out are zero.
+typedef short dw_s4 __attribute__((ext_vector_type(4)));
+typedef __bf16 dw_bf8 __attribute__((ext_vector_type(8)));
+typedef float dw_f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, int lane) {
+  // lanes 16q + j: pairs p0 + 8q + j/4 (+4 for the upper half), channels c0 + 4(j%4)..+3
+  const int j = lane & 15, q = lane >> 4;
+  const int row = p0 + 8 * q + (j >> 2), col = c0 + 4 * (j & 3);
+  typedef __attribute__((address_space(3))) dw_s4 lds_s4;
+  // generic -> LDS address-space conversion (the tile is a __shared__ array)
+  lds_s4* lo = (lds_s4*)(const_cast<uint16_t*>(tile) + row * 64 + col);
+  lds_s4* hi = (lds_s4*)(const_cast<uint16_t*>(tile) + (row + 4) * 64 + col);
+  const dw_s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lo);
+  const dw_s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(hi);
+  typedef short s8 __attribute__((ext_vector_type(8)));
+  const s8 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(dw_bf8, v);
+}
+
+template <bool DC>
+__global__ __launch_bounds__(256, 2) void k_dw_mfma(
+    const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ dy, int C_in, int C_out,
+    int maxchunks, float* __restrict__ part) {
+  constexpr int STEP = 128;
+  constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
+  // staging tiles; the final wave reduction reuses the same bytes
+  __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * STEP * 64];
+  __shared__ int32_t s_a[2][STEP], s_b[2][STEP];
+  uint16_t* s_x = s_buf;
+  uint16_t* s_g = s_buf + STEP * 64;
+  const int i = blockIdx.y, chunk = blockIdx.x;
+  const int ntn = (C_out + 63) / 64;
+  const int c0 = (blockIdx.z / ntn) * 64, n0 = (blockIdx.z % ntn) * 64;
+  const int64_t base = pair_off[i];
+  const int64_t k_i = pair_off[i + 1] - base;
+  const int64_t start = static_cast<int64_t>(chunk) * kChunk;
+  if (start >= k_i) return;
+  const int64_t end = start + kChunk < k_i ? start + kChunk : k_i;
+  const int nsteps = static_cast<int>((end - start + STEP - 1) / STEP);
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int cx = C_in - c0 < 64 ? C_in - c0 : 64;     // valid columns of this tile
+  const int cg = C_out - n0 < 64 ? C_out - n0 : 64;
+
+  // pair rows of step t -> s_a / s_b [t & 1] (input row, gradient row);
+  // DC reads its pairs backwards; -1 past the end of the chunk
+  auto rows_of = [&](int t) {
+    if (threadIdx.x < STEP) {
+      const int64_t e = start + static_cast<int64_t>(t) * STEP + threadIdx.x;
+      int32_t a = -1, b = -1;
+      if (t < nsteps && e < end) {
+        a = pairs[2 * (base + e)];
+        b = pairs[2 * (base + e) + 1];
+      }
+      s_a[t & 1][threadIdx.x] = DC ? b : a;
+      s_b[t & 1][threadIdx.x] = DC ? a : b;
+    }
+  };
+  uint4 vx[PASS], vg[PASS];
+  // gather the rows of step t into registers (8 lanes per 128-byte row)
+  auto gather = [&](int t) {
+    const int ch = (threadIdx.x % 8) * 8;
+#pragma unroll
+    for (int pass = 0; pass < PASS; ++pass) {
+      const int pp = pass * 32 + threadIdx.x / 8;
+      const int32_t ra = s_a[t & 1][pp], rg = s_b[t & 1][pp];
+      vx[pass] = uint4{0u, 0u, 0u, 0u};
+      vg[pass] = uint4{0u, 0u, 0u, 0u};
+      if (ra >= 0 && ch < cx)
+        vx[pass] = *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(ra) * C_in + c0 + ch);
+      if (rg >= 0 && ch < cg)
+        vg[pass] = *reinterpret_cast<const uint4*>(dy + static_cast<int64_t>(rg) * C_out + n0 + ch);
+    }
+  };
+  auto stage = [&]() {
+    const int ch = (threadIdx.x % 8) * 8;
+#pragma unroll
+    for (int pass = 0; pass < PASS; ++pass) {
+      const int pp = pass * 32 + threadIdx.x / 8;
+      *reinterpret_cast<uint4*>(&s_x[pp * 64 + ch]) = vx[pass];
+      *reinterpret_cast<uint4*>(&s_g[pp * 64 + ch]) = vg[pass];
+    }
+  };
+
+  dw_f4 acc[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[u][v] = dw_f4{0.f, 0.f, 0.f, 0.f};
+
+  // prologue: rows of steps 0 and 1, data of step 0 into LDS
+  rows_of(0);
+  rows_of(1);
+  __syncthreads();
+  gather(0);
+  stage();
+  __syncthreads();
+  for (int t = 0; t < nsteps; ++t) {
+    // next step's rows in flight while this one multiplies
+    if (t + 1 < nsteps) gather(t + 1);
+    const int p0 = wave * 32;
+    dw_bf8 fa[4], fb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) fa[u] = tr_frag(s_x, p0, u * 16, lane);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) fb[v] = tr_frag(s_g, p0, v * 16, lane);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[v], acc[u][v], 0, 0, 0);
+    __syncthreads();                          // tiles and s_a/s_b[t & 1] free
+    if (t + 1 < nsteps) {
+      stage();
+      rows_of(t + 2);
+    }
+    __syncthreads();
+  }
+  // wave partials -> LDS (one 16-row band of the tile at a time), summed in
+  // wave order; lane (r, g) holds rows 4g + e, column r of each 16x16 block
+  float (*s_red)[16][64 + 4] = reinterpret_cast<float (*)[16][64 + 4]>(s_buf);
+  float* out = part + (static_cast<int64_t>(i) * maxchunks + chunk) * C_in * C_out;
+  const int r = lane % 16, g = lane / 16;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s_red[wave][4 * g + e][v * 16 + r] = acc[u][v][e];
+    __syncthreads();
+    for (int t = threadIdx.x; t < 16 * 64; t += 256) {
+      const int rr = t / 64, cc = t % 64;
+      const float sum = ((s_red[0][rr][cc] + s_red[1][rr][cc]) + s_red[2][rr][cc]) + s_red[3][rr][cc];
+      const int c = c0 + u * 16 + rr, n = n0 + cc;
+      if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = sum;
+    }
+    __syncthreads();
+  }
+}
+
+// dw[i][c][n] = sum over the chunks of R_i: chunk ch goes to accumulator
+// ch mod 8, the 8 accumulators are added in order (a fixed order, so the
+// result is reproducible, with 8 loads in flight per lane).
 __global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ part,
                                                    const int64_t* __restrict__ pair_off, int K,
                                                    int C_in, int C_out, int maxchunks,
@@ -298,39 +480,88 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ par
   const int64_t rem = idx - i * per;
   const int64_t k_i = pair_off[i + 1] - pair_off[i];
   const int nch = static_cast<int>((k_i + kChunk - 1) / kChunk);
-  float s = 0.0f;
   const float* p = part + static_cast<int64_t>(i) * maxchunks * per + rem;
-  for (int ch = 0; ch < nch; ++ch) s += p[static_cast<int64_t>(ch) * per];
-  dw[idx] = s;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int ch = 0;
+  for (; ch + 8 <= nch; ch += 8) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
+  }
+  for (int j = 0; ch + j < nch; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
+  dw[idx] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
 }
 
-// Bias gradient, stage 1: per chunk of kRowChunk rows, 4 row phases x 64
-// columns per workgroup, phases combined in LDS in fixed order.
+// Bias gradient, stage 1: a chunk of `rows_per` rows per workgroup and up to
+// 32 groups of 16 bytes of columns (grid.y covers wider rows); lane (row
+// phase ph, column group cg) sums rows ph, ph + P, ... of the chunk, with P
+// the largest power of two that fits, then the phases are added in a fixed
+// tree through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, int64_t rows,
-                                                    int C_out, float* __restrict__ partb) {
-  __shared__ float s[4][64];
-  const int chunk = blockIdx.x, nb = blockIdx.y * 64;
-  const int ph = threadIdx.x / 64, n = nb + threadIdx.x % 64;
-  const int64_t r0 = static_cast<int64_t>(chunk) * kRowChunk;
-  const int64_t r1 = r0 + kRowChunk < rows ? r0 + kRowChunk : rows;
-  float acc = 0.0f;
-  if (n < C_out)
-    for (int64_t r = r0 + ph; r < r1; r += 4) acc += IO<T>::ld(dy, r * C_out + n);
-  s[ph][threadIdx.x % 64] = acc;
+                                                    int C_out, int64_t rows_per,
+                                                    float* __restrict__ partb) {
+  constexpr int V = IO<T>::kVec;
+  __shared__ float s[256][V + 1];
+  const int ngrp_all = (C_out + V - 1) / V;       // 16-byte column groups of a row
+  const int g0 = blockIdx.y * 32;
+  const int ngrp = ngrp_all - g0 < 32 ? ngrp_all - g0 : 32;
+  int nph = 1;
+  while (nph * 2 * ngrp <= 256) nph *= 2;         // row phases: a power of two
+  const int ph = threadIdx.x / ngrp, cgp = g0 + threadIdx.x % ngrp;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
+  const int64_t r1 = r0 + rows_per < rows ? r0 + rows_per : rows;
+  float acc[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) acc[e] = 0.0f;
+  const bool vec = C_out % V == 0;
+  if (ph < nph) {
+    for (int64_t r = r0 + ph; r < r1; r += nph) {
+      float v[V];
+      if (vec) {
+        IO<T>::ld16(dy, r * C_out + cgp * V, v);
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+          v[e] = cgp * V + e < C_out ? IO<T>::ld(dy, r * C_out + cgp * V + e) : 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < V; ++e) s[threadIdx.x][e] = acc[e];
   __syncthreads();
-  if (ph == 0 && n < C_out)
-    partb[static_cast<int64_t>(chunk) * C_out + n] =
-        ((s[0][threadIdx.x] + s[1][threadIdx.x]) + s[2][threadIdx.x]) + s[3][threadIdx.x];
+  for (int h = nph / 2; h >= 1; h >>= 1) {        // phase p absorbs phase p + h
+    if (ph < h) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) s[threadIdx.x][e] += s[threadIdx.x + h * ngrp][e];
+    }
+    __syncthreads();
+  }
+  if (ph == 0) {
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      const int n = cgp * V + e;
+      if (n < C_out) partb[static_cast<int64_t>(blockIdx.x) * C_out + n] = s[threadIdx.x][e];
+    }
+  }
 }
 
+// Bias gradient, stage 2: per column, chunk partials into 8 accumulators by
+// chunk mod 8, added in order.
 __global__ __launch_bounds__(256) void k_db_reduce(const float* __restrict__ partb, int nchunks,
                                                    int C_out, float* __restrict__ db) {
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= C_out) return;
-  float s = 0.0f;
-  for (int ch = 0; ch < nchunks; ++ch) s += partb[static_cast<int64_t>(ch) * C_out + n];
-  db[n] = s;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int ch = 0; ch < nchunks; ++ch) a[ch & 7] += partb[static_cast<int64_t>(ch) * C_out + n];
+  db[n] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+}
+
+// rows per bias-gradient chunk: at least kRowChunk, at most 256 chunks
+int64_t db_rows_per(int64_t rows) {
+  const int64_t by_cap = (rows + 255) / 256;
+  return by_cap > kRowChunk ? by_cap : kRowChunk;
 }
 
 int64_t dw_maxchunks(spconv_rulebook rb) { return (rb->n_cap + kChunk - 1) / kChunk; }
@@ -356,7 +587,8 @@ int pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y, i
 size_t transpose_bytes(int64_t n_in, int64_t K) {
   const int64_t tgstride = ((n_in + kBlock - 1) / kBlock) * kBlock;
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
-  return al(256) + al(static_cast<size_t>(n_in) * 4) + al(static_cast<size_t>(K * tgstride) * 4);
+  return al(256) + al(static_cast<size_t>(n_in) * 4) + al(static_cast<size_t>(K * tgstride) * 4) +
+         2 * al(static_cast<size_t>(n_in) * 4) + al(static_cast<size_t>(K) * sizeof(DeviceHeader));
 }
 
 int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
@@ -366,6 +598,15 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
   rb->t_perm = reinterpret_cast<int32_t*>(mem + al(256));
   rb->t_gstride = ((n + kBlock - 1) / kBlock) * kBlock;
   rb->t_gmap = reinterpret_cast<int32_t*>(mem + al(256) + al(static_cast<size_t>(n) * 4));
+  {
+    char* q = mem + al(256) + al(static_cast<size_t>(n) * 4) +
+              al(static_cast<size_t>(rb->K * rb->t_gstride) * 4);
+    rb->t_src = reinterpret_cast<int32_t*>(q);
+    rb->t_dst = reinterpret_cast<int32_t*>(q + al(static_cast<size_t>(n) * 4));
+    rb->t_hdrs = reinterpret_cast<DeviceHeader*>(q + 2 * al(static_cast<size_t>(n) * 4));
+  }
+  rb->t_single = true;               // f = s: one pair per SC input row
+  for (int j = 1; j < rb->D; ++j) rb->t_single = rb->t_single && rb->f[j] == rb->s[j];
   hipStream_t st = rb->stream;
   k_set_rows<<<1, 64, 0, st>>>(rb->t_hdr, n);
   k_fill_i32<<<grid_of(rb->K * rb->t_gstride), 256, 0, st>>>(rb->t_gmap, 0, rb->K * rb->t_gstride);
@@ -412,8 +653,54 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
   k_scatter_transpose<<<grid_of(rb->K * n), 256, 0, st>>>(rb->pairs, rb->pair_off,
                                                           static_cast<int>(rb->K), iperm,
                                                           rb->t_gmap, rb->t_gstride);
+  if (rb->t_single) {
+    k_split_pairs<<<grid_of(n), 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<int>(rb->K),
+                                              rb->t_src, rb->t_dst);
+    k_offset_counts<<<grid_of(rb->K), 256, 0, st>>>(rb->pair_off, static_cast<int>(rb->K),
+                                                    rb->t_hdrs);
+  }
   if (hipFreeAsync(tmem, st) != hipSuccess) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+// The transposed direction with f = s: one single-offset launch per R_i
+// (source rows pairs[.][1], destination rows pairs[.][0]), W^i sliced out of
+// w.  Needs the offsets' lengths on the host (the rule book is synchronised
+// once for that).  Returns kNotSingle, having launched nothing, when some
+// SC input row has no pair.
+int transpose_single(spconv_rulebook rb, int wmode, int in_dt, const void* x, const void* w,
+                     const float* bias, int out_dt, void* y, int C_in, int C_out,
+                     hipStream_t st) {
+  if (rb->h_pair_off.empty()) {
+    rb->h_pair_off.assign(static_cast<size_t>(rb->K + 1), 0);
+    if (hipMemcpyAsync(rb->h_pair_off.data(), rb->pair_off, (rb->K + 1) * sizeof(int64_t),
+                       hipMemcpyDeviceToHost, rb->stream) != hipSuccess ||
+        hipStreamSynchronize(rb->stream) != hipSuccess) {
+      (void)hipGetLastError();
+      rb->h_pair_off.clear();
+      return SPCONV_EHIP;
+    }
+  }
+  // rows near the far border may lack a pair (their output site falls off
+  // the SC grid); then not every destination row is written here
+  if (rb->h_pair_off[rb->K] != rb->n_in) return kNotSingle;
+  const size_t esz = in_dt == SPCONV_BF16 ? 2 : 4;
+  for (int64_t i = 0; i < rb->K; ++i) {
+    const int64_t off = rb->h_pair_off[i], k_i = rb->h_pair_off[i + 1] - off;
+    if (k_i == 0) continue;
+    FwdView v;
+    v.gmap = rb->t_src + off;
+    v.perm = rb->t_dst + off;
+    v.gstride = k_i;
+    v.hdr = rb->t_hdrs + i;
+    v.n_cap = k_i;
+    v.K = 1;
+    v.n_src = rb->n_cap;
+    const void* wi = static_cast<const char*>(w) + static_cast<size_t>(i) * C_in * C_out * esz;
+    const int r = forward_view(v, wmode, in_dt, x, wi, bias, out_dt, y, C_in, C_out, st);
+    if (r != SPCONV_OK) return r;
+  }
+  return SPCONV_OK;
 }
 
 FwdView transpose_view(spconv_rulebook rb) {
@@ -432,7 +719,7 @@ size_t backward_weight_workspace(spconv_rulebook rb, int C_in, int C_out, int op
   const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_cap;
   const int64_t nrc = (rows + kRowChunk - 1) / kRowChunk;
   return static_cast<size_t>(rb->K * dw_maxchunks(rb)) * C_in * C_out * 4 +
-         static_cast<size_t>(nrc > 0 ? nrc : 1) * C_out * 4 + 256;
+         static_cast<size_t>(nrc > 0 ? nrc : 1) * C_out * 4 + 256;  // nrc >= the chunk count
 }
 
 int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy, float* dw,
@@ -445,7 +732,13 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
     dim3 grid(static_cast<unsigned>(maxchunks), static_cast<unsigned>(rb->K),
               static_cast<unsigned>(tiles));
     const bool dc = op == SPCONV_OP_DC;
-    if (dt == SPCONV_F32) {
+    // matrix cores for bf16 rows of whole 16-byte chunks (C % 8 == 0 keeps
+    // every gathered 16-byte load inside its row)
+    if (dt == SPCONV_BF16 && C_in % 8 == 0 && C_out % 8 == 0) {
+      auto kern = dc ? k_dw_mfma<true> : k_dw_mfma<false>;
+      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<const uint16_t*>(x),
+                                 static_cast<const uint16_t*>(dy), C_in, C_out, maxchunks, part);
+    } else if (dt == SPCONV_F32) {
       auto kern = dc ? k_dw_partial<float, true> : k_dw_partial<float, false>;
       kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<const float*>(x),
                                  static_cast<const float*>(dy), C_in, C_out, maxchunks, part);
@@ -460,15 +753,19 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
                                                                C_out, maxchunks, dw);
   if (db) {
     const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_out;
-    const int nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
+    const int64_t rows_per = db_rows_per(rows);
+    const int nrc = static_cast<int>((rows + rows_per - 1) / rows_per);
     float* partb = part + static_cast<int64_t>(rb->K) * maxchunks * per;
     if (nrc > 0) {
-      dim3 g(static_cast<unsigned>(nrc), static_cast<unsigned>((C_out + 63) / 64));
+      const int vec = dt == SPCONV_F32 ? 4 : 8;
+      const int groups = (C_out + vec - 1) / vec;
+      dim3 g(static_cast<unsigned>(nrc), static_cast<unsigned>((groups + 31) / 32));
       if (dt == SPCONV_F32)
-        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out, partb);
+        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out,
+                                               rows_per, partb);
       else
         k_db_partial<uint16_t><<<g, 256, 0, st>>>(static_cast<const uint16_t*>(dy), rows, C_out,
-                                                  partb);
+                                                  rows_per, partb);
     }
     k_db_reduce<<<grid_of(C_out), 256, 0, st>>>(partb, nrc, C_out, db);
   }

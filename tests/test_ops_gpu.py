@@ -170,6 +170,8 @@ GRAD_CASES = [
     ("sc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 64, "bf16"),
     ("dc", "pen", [1, 2, 2], [1, 2, 2], 32, 16, "f32"),
     ("dc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 64, 32, "bf16"),
+    ("vsc", "surf", [1, 3, 3, 3], None, 32, 96, "bf16"),
+    ("sc", "pen", [1, 2, 2], [1, 2, 2], 3, 5, "f32"),
 ]
 
 
