@@ -435,14 +435,22 @@ def run_ops(a, torch, dev, spc, inputs):
     yd = torch.empty((n_in, co), dtype=torch.bfloat16, device=dev)
     ms = timed(lambda: spc.dc_forward(rb, xd, wd, out=yd))
     fl = 2.0 * sum_k * ci * co
-    emit("dc_2x2x2_s2_c64_c32", "surf256x4 level 0", ms, "mfma", fl / (ms * 1e-3) / 1e12,
-         "TFLOP/s", PEAKS["bf16"], {"n_in": n_out, "n_out": n_in, "sum_k": sum_k})
+    # f = s: every output row takes one input row through one W^i (37 FLOP per
+    # byte at 64 -> 32 planes, far below the matrix-core ridge): HBM-bound.
+    # Algorithmic bytes: inputs once, outputs once, the two pair columns, W.
+    dc_bytes = n_out * ci * 2 + n_in * co * 2 + 8 * sum_k + K * ci * co * 2
+    emit("dc_2x2x2_s2_c64_c32", "surf256x4 level 0", ms, "hbm", dc_bytes / (ms * 1e-3) / 1e9,
+         "GB/s", PEAKS["hbm"], {"n_in": n_out, "n_out": n_in, "sum_k": sum_k,
+                                "algorithmic_bytes": dc_bytes,
+                                "effective_tflops": fl / (ms * 1e-3) / 1e12})
     wsc = weights(K, co, ci, 24)                 # SC(32 -> 64) weights
     dysc = feats(n_out, ci, 25)
     dxsc = torch.empty((n_in, co), dtype=torch.bfloat16, device=dev)
     ms = timed(lambda: spc.backward_data(rb, spc.OP_SC, dysc, wsc, out=dxsc))
-    emit("sc_input_grad_2x2x2_s2_c32_c64", "surf256x4 level 0", ms, "mfma",
-         fl / (ms * 1e-3) / 1e12, "TFLOP/s", PEAKS["bf16"], {"sum_k": sum_k})
+    emit("sc_input_grad_2x2x2_s2_c32_c64", "surf256x4 level 0", ms, "hbm",
+         dc_bytes / (ms * 1e-3) / 1e9, "GB/s", PEAKS["hbm"],
+         {"sum_k": sum_k, "algorithmic_bytes": dc_bytes,
+          "effective_tflops": fl / (ms * 1e-3) / 1e12})
     xsc = feats(n_in, co, 26)
     ms = timed(lambda: spc.backward_weight(rb, spc.OP_SC, xsc, dysc, co, ci))
     emit("sc_weight_grad_2x2x2_s2_c32_c64", "surf256x4 level 0", ms, "mfma",

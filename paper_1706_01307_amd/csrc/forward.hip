@@ -16,6 +16,7 @@ FwdView view_of(spconv_rulebook rb) {
   v.n_cap = rb->n_cap;
   v.K = rb->K;
   v.n_src = rb->n_in;
+  v.seg = nullptr;
   return v;
 }
 
@@ -24,12 +25,14 @@ int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const vo
                  hipStream_t stream) {
   if (v.n_cap == 0) return SPCONV_OK;
   FwdCall c{v, x, 0u, w, bias, y, C_out, stream};
+  bool done = false;
   switch (wmode) {
-    case 0: forward_run_w0(c, in_dt, out_dt, C_in); break;
-    case 1: forward_run_w1(c, in_dt, out_dt, C_in); break;
-    case 2: forward_run_w2(c, in_dt, out_dt, C_in); break;
+    case 0: done = forward_run_w0(c, in_dt, out_dt, C_in); break;
+    case 1: done = forward_run_w1(c, in_dt, out_dt, C_in); break;
+    case 2: done = forward_run_w2(c, in_dt, out_dt, C_in); break;
     default: return SPCONV_EINVAL;
   }
+  if (!done) return kNotSingle;           // a segmented view with no matrix-core kernel
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 

@@ -210,9 +210,12 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K_arg,
     const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
-    const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles) {
+    const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles,
+    const int32_t* __restrict__ seg) {
   // KT > 0: the offset count is a compile-time constant and the offset loop
   // is unrolled completely (no loop-carried register hazards).
+  // seg != NULL: a segmented single-offset view; this tile's weights are
+  // W^seg[chunk] (tiles never straddle a chunk of kSegRows positions).
   const int K = KT > 0 ? KT : K_arg;
   constexpr int KC = MT<TIn>::KC;
   constexpr int CIN = NCH * KC;
@@ -238,6 +241,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   const int64_t n_rows = hdr->n_out;
   // tiles past the device-side row count (the grid is sized for a bound)
   if (tile >= ntiles || tile * TILE_ROWS >= n_rows) return;
+  static_assert(kSegRows % TILE_ROWS == 0, "tiles inside one segment chunk");
+  const int wseg = seg ? seg[tile * TILE_ROWS / kSegRows] : -1;
 
   const int col0 = blockIdx.y * COLS;
   const int wave = threadIdx.x / kWave;
@@ -270,13 +275,14 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
         const int t0 = threadIdx.x + q * 256;
         const int t = (NTASK % 256 == 0 || t0 < NTASK) ? t0 : 0;
         const int kt = t / NGRP, nt = t % NGRP;
-        const TIn* src = w + (static_cast<int64_t>(i) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
+        const int iv = wseg >= 0 ? wseg : i;
+        const TIn* src = w + (static_cast<int64_t>(iv) * CIN + kt * KPT) * C_out + col0 + nt * NPT;
 #pragma unroll
         for (int r = 0; r < KPT; ++r)
           wr[q * KPT + r] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r) * C_out);
       }
     } else {
-      const int iw = WT == 1 ? K - 1 - i : i;
+      const int iw = wseg >= 0 ? wseg : (WT == 1 ? K - 1 - i : i);
 #pragma unroll
       for (int q = 0; q < TPT_T; ++q) {
         const int t0 = threadIdx.x + q * 256;
@@ -452,8 +458,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
-      if (pos < n_rows) {
-        const int64_t row = perm[pos];
+      const int64_t row = pos < n_rows ? perm[pos] : -1;
+      if (row >= 0) {                                   // -1: padding of a segmented view
         float o[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
@@ -484,12 +490,15 @@ void launch_mfma(const Call& c) {
   // filters run the unrolled kernel; other filters (strided SC, DC and the
   // SC input gradient, whose rows come ordered by offset class so that most
   // blocks take one offset only) also skip the blocks' gathers.
-  auto kern = c.v.K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
-                          : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
+  // Single-offset views (f = s transposed runs, 1^d filters) unroll to one
+  // step with a third of the registers, so more workgroups share a CU.
+  auto kern = c.v.K == 27  ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
+              : c.v.K == 1 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 1, true, WT>
+                           : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
   kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), c.x_bytes, static_cast<const TIn*>(c.w), c.bias,
-      static_cast<TOut*>(c.y), c.C_out, ntiles);
+      static_cast<TOut*>(c.y), c.C_out, ntiles, c.v.seg);
 }
 
 template <typename TIn, int NCH, typename TOut, int WT>
@@ -544,13 +553,14 @@ void launch_vec(const Call& c, int C_in) {
 }
 
 template <int WT>
-void run(const Call& c, int in_dt, int out_dt, int C_in) {
+bool run(const Call& c, int in_dt, int out_dt, int C_in) {
   bool done = false;
   if (!force_vector_path()) {
     done = out_dt == SPCONV_F32 ? try_mfma<float, WT>(c, in_dt, C_in)
                                 : try_mfma<uint16_t, WT>(c, in_dt, C_in);
   }
-  if (done) return;
+  if (done) return true;
+  if (c.v.seg) return false;               // segmented views run on the matrix cores only
   if (in_dt == SPCONV_F32 && out_dt == SPCONV_F32)
     launch_vec<float, float, WT>(c, C_in);
   else if (in_dt == SPCONV_F32)
@@ -559,6 +569,7 @@ void run(const Call& c, int in_dt, int out_dt, int C_in) {
     launch_vec<uint16_t, float, WT>(c, C_in);
   else
     launch_vec<uint16_t, uint16_t, WT>(c, C_in);
+  return true;
 }
 
 }  // namespace

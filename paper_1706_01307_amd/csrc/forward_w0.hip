@@ -4,8 +4,8 @@
 
 namespace spc {
 
-void forward_run_w0(const FwdCall& c, int in_dt, int out_dt, int C_in) {
-  run<0>(c, in_dt, out_dt, C_in);
+bool forward_run_w0(const FwdCall& c, int in_dt, int out_dt, int C_in) {
+  return run<0>(c, in_dt, out_dt, C_in);
 }
 
 }  // namespace spc

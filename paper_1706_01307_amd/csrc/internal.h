@@ -176,10 +176,15 @@ struct spconv_rulebook_s {
   int32_t* t_perm;             // [n_in]
   int32_t* t_gmap;             // [K][t_gstride]
   int64_t t_gstride;
-  bool t_single;               // f = s: R_i also split into t_src / t_dst
-  int32_t* t_src;              // [sum k] 1 + SC output row, R_0 first
-  int32_t* t_dst;              // [sum k] SC input row
-  spc::DeviceHeader* t_hdrs;   // [K] n_out = k_i
+  // f = s: R_i also split into its two columns, each offset's run padded to
+  // whole chunks of kSegRows positions (padding: source 0, destination -1)
+  bool t_single;
+  int64_t t_npad_cap;          // bound on the padded length (sum k + K kSegRows)
+  int32_t* t_src;              // [t_npad_cap] 1 + SC output row
+  int32_t* t_dst;              // [t_npad_cap] SC input row, -1 = padding
+  int32_t* t_seg;              // [t_npad_cap / kSegRows] offset of every chunk
+  int32_t* t_chunk_off;        // [K + 1] first chunk of every offset
+  spc::DeviceHeader* t_hdrs;   // [K] n_out = k_i; [K] (one more) n_out = padded length
   std::vector<int64_t> h_pair_off;   // host copy of pair_off, filled on first use
   // host state after synchronisation
   bool synced;
@@ -211,7 +216,12 @@ struct FwdView {
   int64_t n_cap;
   int64_t K;
   int64_t n_src;
+  // Segmented single-offset views (K = 1): position chunks of kSegRows rows
+  // belong to one offset each, seg[chunk] naming which W^i they take; a
+  // position whose perm entry is negative is padding.  NULL otherwise.
+  const int32_t* seg = nullptr;
 };
+constexpr int kSegRows = 256;
 FwdView view_of(spconv_rulebook rb);
 struct FwdCall {
   FwdView v;
@@ -223,9 +233,11 @@ struct FwdCall {
   int C_out;
   hipStream_t stream;
 };
-void forward_run_w0(const FwdCall& c, int in_dt, int out_dt, int C_in);
-void forward_run_w1(const FwdCall& c, int in_dt, int out_dt, int C_in);
-void forward_run_w2(const FwdCall& c, int in_dt, int out_dt, int C_in);
+// Each returns false when the view is segmented and no matrix-core kernel
+// fits the shape (nothing is launched then).
+bool forward_run_w0(const FwdCall& c, int in_dt, int out_dt, int C_in);
+bool forward_run_w1(const FwdCall& c, int in_dt, int out_dt, int C_in);
+bool forward_run_w2(const FwdCall& c, int in_dt, int out_dt, int C_in);
 // wmode 0: W^i = w[i] ([K][C_in][C_out]); 1: w[K-1-i]^T; 2: w[i]^T (w given
 // as [K][C_out][C_in] of the layer whose gradient this is).
 int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const void* w,

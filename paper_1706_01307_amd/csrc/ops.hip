@@ -21,11 +21,11 @@
 // The output-stationary forward kernels then run DC and the input gradients
 // over this map.  When f = s every SC input row has exactly one pair, and
 // the rule book also keeps R_i split into its two columns (source rows + 1,
-// destination rows) with a per-offset row count:
-//   k_split_pairs, k_offset_counts
-// so DC and the SC input gradient run one gather-multiply-store launch per
-// offset (the forward kernels with a single offset), with no empty offsets to
-// walk.
+// destination rows), each offset's run padded to whole chunks of kSegRows:
+//   k_chunk_layout, k_seg_fill, k_seg_scatter
+// so DC and the SC input gradient run as one gather-multiply-store launch
+// (the forward kernels with one offset, W^i chosen per chunk), with no empty
+// offsets to walk.
 //
 // Weight gradient dW^i = sum over the pairs of R_i of (input row)^T x (output
 // gradient row): R_i is cut into chunks of kChunk pairs; one workgroup forms
@@ -190,26 +190,60 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t* __restrict__ a, int32
     a[r] = v;
 }
 
-// pairs (a, b) of the whole book -> src[e] = b + 1, dst[e] = a
-__global__ __launch_bounds__(256) void k_split_pairs(const int32_t* __restrict__ pairs,
+// f = s layout: chunk_off[i] = first chunk of offset i's run (runs padded to
+// whole chunks of kSegRows), hdrs[i].n_out = k_i, hdrs[K].n_out = padded length
+__global__ void k_chunk_layout(const int64_t* __restrict__ pair_off, int K,
+                               int32_t* __restrict__ chunk_off, DeviceHeader* __restrict__ hdrs) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  int64_t c = 0;
+  for (int i = 0; i < K; ++i) {
+    const int64_t k_i = pair_off[i + 1] - pair_off[i];
+    chunk_off[i] = static_cast<int32_t>(c);
+    hdrs[i].status = 0;
+    hdrs[i].n_out = k_i;
+    c += (k_i + kSegRows - 1) / kSegRows;
+  }
+  chunk_off[K] = static_cast<int32_t>(c);
+  hdrs[K].status = 0;
+  hdrs[K].n_out = c * kSegRows;
+}
+
+// seg[c] = the offset whose run holds chunk c (0 past the last run)
+__global__ __launch_bounds__(256) void k_seg_fill(const int32_t* __restrict__ chunk_off, int K,
+                                                  int64_t nchunks, int32_t* __restrict__ seg) {
+  const int64_t c = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+  if (c >= nchunks) return;
+  int lo = 0, hi = K;                 // chunk_off[lo] <= c < chunk_off[hi], else 0
+  if (c >= chunk_off[K]) {
+    seg[c] = 0;
+    return;
+  }
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) / 2;
+    if (chunk_off[mid] <= c) lo = mid; else hi = mid;
+  }
+  seg[c] = lo;
+}
+
+// pair e of R_i -> position chunk_off[i] kSegRows + (e - pair_off[i]):
+// src = 1 + SC output row, dst = SC input row
+__global__ __launch_bounds__(256) void k_seg_scatter(const int32_t* __restrict__ pairs,
                                                      const int64_t* __restrict__ pair_off, int K,
+                                                     const int32_t* __restrict__ chunk_off,
                                                      int32_t* __restrict__ src,
                                                      int32_t* __restrict__ dst) {
   const int64_t total = pair_off[K];
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
        e += stride) {
-    src[e] = pairs[2 * e + 1] + 1;
-    dst[e] = pairs[2 * e];
-  }
-}
-
-__global__ void k_offset_counts(const int64_t* __restrict__ pair_off, int K,
-                                DeviceHeader* __restrict__ h) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < K) {
-    h[i].status = 0;
-    h[i].n_out = pair_off[i + 1] - pair_off[i];
+    int lo = 0, hi = K;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) / 2;
+      if (pair_off[mid] <= e) lo = mid; else hi = mid;
+    }
+    const int64_t pos = static_cast<int64_t>(chunk_off[lo]) * kSegRows + (e - pair_off[lo]);
+    src[pos] = pairs[2 * e + 1] + 1;
+    dst[pos] = pairs[2 * e];
   }
 }
 
@@ -584,11 +618,15 @@ int pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, void* y, i
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
+static int64_t seg_cap(int64_t n_in, int64_t K) { return n_in + K * kSegRows; }
+
 size_t transpose_bytes(int64_t n_in, int64_t K) {
   const int64_t tgstride = ((n_in + kBlock - 1) / kBlock) * kBlock;
+  const int64_t npad = seg_cap(n_in, K);
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   return al(256) + al(static_cast<size_t>(n_in) * 4) + al(static_cast<size_t>(K * tgstride) * 4) +
-         2 * al(static_cast<size_t>(n_in) * 4) + al(static_cast<size_t>(K) * sizeof(DeviceHeader));
+         2 * al(static_cast<size_t>(npad) * 4) + al(static_cast<size_t>(npad / kSegRows + 1) * 4) +
+         al(static_cast<size_t>(K + 1) * 4) + al(static_cast<size_t>(K + 1) * sizeof(DeviceHeader));
 }
 
 int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
@@ -601,9 +639,15 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
   {
     char* q = mem + al(256) + al(static_cast<size_t>(n) * 4) +
               al(static_cast<size_t>(rb->K * rb->t_gstride) * 4);
+    rb->t_npad_cap = seg_cap(n, rb->K);
+    const size_t pb = al(static_cast<size_t>(rb->t_npad_cap) * 4);
     rb->t_src = reinterpret_cast<int32_t*>(q);
-    rb->t_dst = reinterpret_cast<int32_t*>(q + al(static_cast<size_t>(n) * 4));
-    rb->t_hdrs = reinterpret_cast<DeviceHeader*>(q + 2 * al(static_cast<size_t>(n) * 4));
+    rb->t_dst = reinterpret_cast<int32_t*>(q + pb);
+    rb->t_seg = reinterpret_cast<int32_t*>(q + 2 * pb);
+    const size_t sb = al(static_cast<size_t>(rb->t_npad_cap / kSegRows + 1) * 4);
+    rb->t_chunk_off = reinterpret_cast<int32_t*>(q + 2 * pb + sb);
+    rb->t_hdrs = reinterpret_cast<DeviceHeader*>(q + 2 * pb + sb +
+                                                 al(static_cast<size_t>(rb->K + 1) * 4));
   }
   rb->t_single = true;               // f = s: one pair per SC input row
   for (int j = 1; j < rb->D; ++j) rb->t_single = rb->t_single && rb->f[j] == rb->s[j];
@@ -654,10 +698,16 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
                                                           static_cast<int>(rb->K), iperm,
                                                           rb->t_gmap, rb->t_gstride);
   if (rb->t_single) {
-    k_split_pairs<<<grid_of(n), 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<int>(rb->K),
-                                              rb->t_src, rb->t_dst);
-    k_offset_counts<<<grid_of(rb->K), 256, 0, st>>>(rb->pair_off, static_cast<int>(rb->K),
-                                                    rb->t_hdrs);
+    const int64_t nchunks = rb->t_npad_cap / kSegRows + 1;
+    k_fill_i32<<<grid_of(rb->t_npad_cap), 256, 0, st>>>(rb->t_src, 0, rb->t_npad_cap);
+    k_fill_i32<<<grid_of(rb->t_npad_cap), 256, 0, st>>>(rb->t_dst, -1, rb->t_npad_cap);
+    k_chunk_layout<<<1, 64, 0, st>>>(rb->pair_off, static_cast<int>(rb->K), rb->t_chunk_off,
+                                     rb->t_hdrs);
+    k_seg_fill<<<grid_of(nchunks, 1ll << 30), 256, 0, st>>>(rb->t_chunk_off,
+                                                            static_cast<int>(rb->K), nchunks,
+                                                            rb->t_seg);
+    k_seg_scatter<<<grid_of(n), 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<int>(rb->K),
+                                              rb->t_chunk_off, rb->t_src, rb->t_dst);
   }
   if (hipFreeAsync(tmem, st) != hipSuccess) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -684,9 +734,24 @@ int transpose_single(spconv_rulebook rb, int wmode, int in_dt, const void* x, co
   // rows near the far border may lack a pair (their output site falls off
   // the SC grid); then not every destination row is written here
   if (rb->h_pair_off[rb->K] != rb->n_in) return kNotSingle;
+  // one launch over all offsets when a matrix-core kernel fits the shape
+  FwdView sv;
+  sv.gmap = rb->t_src;
+  sv.perm = rb->t_dst;
+  sv.gstride = rb->t_npad_cap;
+  sv.hdr = rb->t_hdrs + rb->K;
+  sv.n_cap = rb->t_npad_cap;
+  sv.K = 1;
+  sv.n_src = rb->n_cap;
+  sv.seg = rb->t_seg;
+  const int r0 = forward_view(sv, wmode, in_dt, x, w, bias, out_dt, y, C_in, C_out, st);
+  if (r0 != kNotSingle) return r0;
+  // otherwise one launch per offset
   const size_t esz = in_dt == SPCONV_BF16 ? 2 : 4;
+  int64_t chunk = 0;
   for (int64_t i = 0; i < rb->K; ++i) {
-    const int64_t off = rb->h_pair_off[i], k_i = rb->h_pair_off[i + 1] - off;
+    const int64_t off = chunk * kSegRows, k_i = rb->h_pair_off[i + 1] - rb->h_pair_off[i];
+    chunk += (k_i + kSegRows - 1) / kSegRows;
     if (k_i == 0) continue;
     FwdView v;
     v.gmap = rb->t_src + off;
@@ -696,6 +761,7 @@ int transpose_single(spconv_rulebook rb, int wmode, int in_dt, const void* x, co
     v.n_cap = k_i;
     v.K = 1;
     v.n_src = rb->n_cap;
+    v.seg = nullptr;
     const void* wi = static_cast<const char*>(w) + static_cast<size_t>(i) * C_in * C_out * esz;
     const int r = forward_view(v, wmode, in_dt, x, wi, bias, out_dt, y, C_in, C_out, st);
     if (r != SPCONV_OK) return r;
@@ -712,6 +778,7 @@ FwdView transpose_view(spconv_rulebook rb) {
   v.n_cap = rb->n_in;
   v.K = rb->K;
   v.n_src = rb->n_cap;
+  v.seg = nullptr;
   return v;
 }
 
