@@ -278,7 +278,7 @@ __global__ __launch_bounds__(256) void k_scatter_transpose(
 // ---------------------------------------------------------------------------
 constexpr int64_t kChunk = 4096;   // pairs per partial product
 constexpr int kSub = 64;           // pairs staged in LDS at a time
-constexpr int64_t kRowChunk = 4096;
+constexpr int64_t kRowChunk = 512;    // rows per bias-gradient partial
 
 // grid: (chunk, offset, tile); tile = (c-block of 64) x (n-block of 64).
 template <typename T, bool DC>
@@ -525,15 +525,14 @@ __global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ par
   dw[idx] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
 }
 
-// Bias gradient, stage 1: a chunk of `rows_per` rows per workgroup and up to
+// Bias gradient, stage 1: a chunk of kRowChunk rows per workgroup and up to
 // 32 groups of 16 bytes of columns (grid.y covers wider rows); lane (row
-// phase ph, column group cg) sums rows ph, ph + P, ... of the chunk, with P
-// the largest power of two that fits, then the phases are added in a fixed
-// tree through LDS.
+// phase ph, column group cg) sums rows ph, ph + P, ... of the chunk (P the
+// largest power of two that fits, loads issued 8 rows at a time), then the
+// phases are added in a fixed tree through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, int64_t rows,
-                                                    int C_out, int64_t rows_per,
-                                                    float* __restrict__ partb) {
+                                                    int C_out, float* __restrict__ partb) {
   constexpr int V = IO<T>::kVec;
   __shared__ float s[256][V + 1];
   const int ngrp_all = (C_out + V - 1) / V;       // 16-byte column groups of a row
@@ -542,22 +541,35 @@ __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, in
   int nph = 1;
   while (nph * 2 * ngrp <= 256) nph *= 2;         // row phases: a power of two
   const int ph = threadIdx.x / ngrp, cgp = g0 + threadIdx.x % ngrp;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
-  const int64_t r1 = r0 + rows_per < rows ? r0 + rows_per : rows;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kRowChunk;
+  const int64_t r1 = r0 + kRowChunk < rows ? r0 + kRowChunk : rows;
   float acc[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) acc[e] = 0.0f;
   const bool vec = C_out % V == 0;
-  if (ph < nph) {
-    for (int64_t r = r0 + ph; r < r1; r += nph) {
-      float v[V];
-      if (vec) {
-        IO<T>::ld16(dy, r * C_out + cgp * V, v);
-      } else {
+  auto row_vals = [&](int64_t r, float* v) {
+    if (vec) {
+      IO<T>::ld16(dy, r * C_out + cgp * V, v);
+    } else {
 #pragma unroll
-        for (int e = 0; e < V; ++e)
-          v[e] = cgp * V + e < C_out ? IO<T>::ld(dy, r * C_out + cgp * V + e) : 0.0f;
-      }
+      for (int e = 0; e < V; ++e)
+        v[e] = cgp * V + e < C_out ? IO<T>::ld(dy, r * C_out + cgp * V + e) : 0.0f;
+    }
+  };
+  if (ph < nph) {
+    int64_t r = r0 + ph;
+    for (; r + 7 * nph < r1; r += 8 * nph) {      // 8 rows in flight, added in row order
+      float v[8][V];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) row_vals(r + u * nph, v[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] += v[u][e];
+    }
+    for (; r < r1; r += nph) {
+      float v[V];
+      row_vals(r, v);
 #pragma unroll
       for (int e = 0; e < V; ++e) acc[e] += v[e];
     }
@@ -581,21 +593,27 @@ __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, in
   }
 }
 
-// Bias gradient, stage 2: per column, chunk partials into 8 accumulators by
-// chunk mod 8, added in order.
+// Bias gradient, stage 2: 16 columns per workgroup; lane (phase q, column)
+// adds chunk partials q, q + 16, ... (into 4 accumulators by round), then the
+// 16 phases are added in a fixed tree.
 __global__ __launch_bounds__(256) void k_db_reduce(const float* __restrict__ partb, int nchunks,
                                                    int C_out, float* __restrict__ db) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= C_out) return;
-  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int ch = 0; ch < nchunks; ++ch) a[ch & 7] += partb[static_cast<int64_t>(ch) * C_out + n];
-  db[n] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
-}
-
-// rows per bias-gradient chunk: at least kRowChunk, at most 256 chunks
-int64_t db_rows_per(int64_t rows) {
-  const int64_t by_cap = (rows + 255) / 256;
-  return by_cap > kRowChunk ? by_cap : kRowChunk;
+  __shared__ float s[16][17];
+  const int q = threadIdx.x / 16, cn = threadIdx.x % 16;
+  const int n = blockIdx.x * 16 + cn;
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  if (n < C_out) {
+    int k = 0;
+    for (int ch = q; ch < nchunks; ch += 16, ++k)
+      a[k & 3] += partb[static_cast<int64_t>(ch) * C_out + n];
+  }
+  s[q][cn] = (a[0] + a[1]) + (a[2] + a[3]);
+  __syncthreads();
+  for (int h = 8; h >= 1; h >>= 1) {
+    if (q < h) s[q][cn] += s[q + h][cn];
+    __syncthreads();
+  }
+  if (q == 0 && n < C_out) db[n] = s[0][cn];
 }
 
 int64_t dw_maxchunks(spconv_rulebook rb) { return (rb->n_cap + kChunk - 1) / kChunk; }
@@ -820,21 +838,19 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
                                                                C_out, maxchunks, dw);
   if (db) {
     const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_out;
-    const int64_t rows_per = db_rows_per(rows);
-    const int nrc = static_cast<int>((rows + rows_per - 1) / rows_per);
+    const int nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
     float* partb = part + static_cast<int64_t>(rb->K) * maxchunks * per;
     if (nrc > 0) {
       const int vec = dt == SPCONV_F32 ? 4 : 8;
       const int groups = (C_out + vec - 1) / vec;
       dim3 g(static_cast<unsigned>(nrc), static_cast<unsigned>((groups + 31) / 32));
       if (dt == SPCONV_F32)
-        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out,
-                                               rows_per, partb);
+        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out, partb);
       else
         k_db_partial<uint16_t><<<g, 256, 0, st>>>(static_cast<const uint16_t*>(dy), rows, C_out,
-                                                  rows_per, partb);
+                                                  partb);
     }
-    k_db_reduce<<<grid_of(C_out), 256, 0, st>>>(partb, nrc, C_out, db);
+    k_db_reduce<<<(C_out + 15) / 16, 256, 0, st>>>(partb, nrc, C_out, db);
   }
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
