@@ -4,12 +4,14 @@ A ctypes wrapper around ``oracle.cpp``, the plain std::map CPU statement of
 the paper's sparse convolutions (Section 3 for the layer definitions,
 including sparse max / average pooling and the deconvolution DC, Section 4
 for the rule book and the forward multiply-add), plus the derivatives of
-those sums that training needs (input, weight and bias gradients).  Only the test
+those sums that training needs (input, weight and bias gradients), and the
+per-channel affine / residual / ReLU epilogue of Section 5's blocks.  Only the test
 suite, the smoke check and the benchmark's CPU-baseline leg import this
 package; the product path never does.  It shares no code with the HIP
 library.
 
-Parity pins for every function here live in ``tests/test_oracle_pins.py``.
+Parity pins for every function here live in ``tests/test_oracle_pins.py``
+and ``tests/test_oracle_pins_ext.py``.
 """
 from __future__ import annotations
 
@@ -215,6 +217,47 @@ class Rulebook:
         if h is not None and _lib is not None:
             _lib.ref_free(h)
             self._h = None
+
+
+def fused_epilogue(y, absb, scale=None, shift=None, residual=None, relu=False, res_dt=F32):
+    """Per-channel affine map, residual add and ReLU on an exact layer output.
+
+    The networks of Section 5 follow their sparse convolutions with batch
+    normalisation and a ReLU, both acting on the active sites only, and their
+    residual blocks add the block input back before the last ReLU.  At
+    inference a batch normalisation is an affine map per channel, so for an
+    output row r and channel n (y and absb from ``forward``):
+
+        z = y[r, n] * scale[n] + shift[n] + residual[r, n]
+        out = 0 if relu and z < 0 else z     (NaN stays NaN)
+
+    scale None = 1, shift None = 0, residual None = 0.  residual holds float32
+    (res_dt F32) or bf16 bits (BF16), [n_out, C_out].  Returns (out, bound)
+    in float64, unrounded; bound = |scale| absb + |shift| + |residual| scales
+    the rounding error of the fused result (ReLU is 1-Lipschitz).
+    """
+    y = np.asarray(y, dtype=np.float64)
+    absb = np.asarray(absb, dtype=np.float64)
+    z = y.copy()
+    bound = absb.copy()
+    if scale is not None:
+        sc = np.asarray(scale, dtype=np.float32).astype(np.float64)
+        z = z * sc
+        bound = bound * np.abs(sc)
+    if shift is not None:
+        sh = np.asarray(shift, dtype=np.float32).astype(np.float64)
+        z = z + sh
+        bound = bound + np.abs(sh)
+    if residual is not None:
+        r = np.asarray(residual)
+        if res_dt == BF16:
+            r = (r.astype(np.uint32) << 16).view(np.float32)
+        r = r.astype(np.float64)
+        z = z + r
+        bound = bound + np.abs(r)
+    if relu:
+        z = np.where(z < 0, 0.0, z)
+    return z, bound
 
 
 def round_to(v, out_dt):

@@ -255,3 +255,74 @@ def test_gradient_ops_reject_mismatched_books():
             vsc.backward_data(op, np.ones((2, 2), np.float32), w)
     with pytest.raises(oracle.OracleError):
         vsc.dc_forward(np.ones((2, 2), np.float32), w)
+
+
+# ---------------------------------------------------------------------------
+# Per-channel affine + residual + ReLU epilogue (the blocks of Section 5)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kind,d,fs,ss", [(oracle.VSC, 2, 3, 1), (oracle.VSC, 3, 3, 1),
+                                          (oracle.SC, 2, 2, 2), (oracle.SC, 3, 3, 2)])
+@pytest.mark.parametrize("relu", [False, True])
+def test_fused_epilogue_matches_torch_batchnorm_residual_relu(kind, d, fs, ss, relu):
+    """Conv with bias, eval-mode batch norm, + residual, then ReLU in torch
+    (float64, dense zero-filled grid) = the oracle's forward followed by the
+    epilogue with the conv bias and the batch norm folded into scale/shift."""
+    rng = np.random.default_rng(900 + 10 * d + fs + ss + relu)
+    size, coords = _sites(rng, d, {2: 9, 3: 6}[d], 2, 0.3)
+    f = [1] + [fs] * d
+    s = [1] + [ss] * d
+    rb = oracle.Rulebook(kind, coords, size, f, s)
+    C_in, C_out, K = 3, 5, fs ** d
+    x = rng.standard_normal((len(coords), C_in)).astype(np.float32)
+    w = rng.standard_normal((K, C_in, C_out)).astype(np.float32)
+    bias = rng.standard_normal(C_out).astype(np.float32)
+    mean = rng.standard_normal(C_out)
+    var = rng.random(C_out) + 0.5
+    gamma = rng.standard_normal(C_out)
+    beta = rng.standard_normal(C_out)
+    eps = 1e-5
+    res = rng.standard_normal((rb.n_out, C_out)).astype(np.float32)
+
+    pad = (fs - 1) // 2 if kind == oracle.VSC else 0
+    conv = CONV[d](_dense(coords, size, x), _w_conv(w, [fs] * d),
+                   bias=torch.from_numpy(bias.astype(np.float64)), stride=ss, padding=pad)
+    bn = F.batch_norm(conv, torch.from_numpy(mean), torch.from_numpy(var),
+                      torch.from_numpy(gamma), torch.from_numpy(beta), training=False, eps=eps)
+    ref = _at(bn, rb.out_coords) + res.astype(np.float64)
+    if relu:
+        ref = np.maximum(ref, 0.0)
+
+    inv = gamma / np.sqrt(var + eps)
+    scale = inv.astype(np.float32)
+    shift = (beta + (bias - mean) * inv).astype(np.float32)
+    y, absb = rb.forward(x, w)
+    out, bound = oracle.fused_epilogue(y, absb, scale, shift, res, relu)
+    # scale and shift are float32 roundings of the float64 fold
+    assert np.all(np.abs(out - ref) <= 1e-6 * (bound + 1.0))
+
+
+def test_fused_epilogue_identity_and_relu():
+    rng = np.random.default_rng(950)
+    y = rng.standard_normal((40, 7))
+    absb = np.abs(y) + 1.0
+    out, bound = oracle.fused_epilogue(y, absb)
+    np.testing.assert_array_equal(out, y)
+    np.testing.assert_array_equal(bound, absb)
+    y[3, 2] = np.nan
+    out, _ = oracle.fused_epilogue(y, absb, relu=True)
+    assert np.isnan(out[3, 2])
+    ok = ~np.isnan(y)
+    np.testing.assert_array_equal(out[ok], np.where(y[ok] < 0, 0.0, y[ok]))
+
+
+def test_fused_epilogue_bf16_residual():
+    """A bf16 residual is read as the float32 value of its bits."""
+    rng = np.random.default_rng(951)
+    y = rng.standard_normal((16, 8))
+    r32 = rng.standard_normal((16, 8)).astype(np.float32)
+    bits = (r32.view(np.uint32) >> 16).astype(np.uint16)   # truncated: exact in bf16
+    exact = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    out, bound = oracle.fused_epilogue(y, np.abs(y), residual=bits, res_dt=oracle.BF16)
+    np.testing.assert_array_equal(out, y + exact)
+    np.testing.assert_array_equal(bound, np.abs(y) + np.abs(exact))
