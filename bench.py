@@ -377,10 +377,11 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
 
 
 def run_ops(a, torch, dev, spc, inputs):
-    """Pooling, DC and gradients on the workloads they belong to, one JSON
-    line each: the level-0 sites of the 4 x 256^3 encoder (2^3 stride-2 SC:
-    pooling, DC, the SC gradients) and the 8 x 128^3 headline VSC layer (its
-    input and weight gradients).  Each line gives the mean time per call from
+    """Pooling, DC, gradients and the fused block epilogue on the workloads
+    they belong to, one JSON line each: the level-0 sites of the 4 x 256^3
+    encoder (2^3 stride-2 SC: pooling, DC, the SC gradients) and the
+    8 x 128^3 headline VSC layer (its input and weight gradients, and its
+    forward with batch-norm affine + residual + ReLU fused).  Each line gives the mean time per call from
     HIP events on the stream the library runs on, and achieved / peak for the
     bound that applies (algorithmic bytes or FLOPs per call)."""
     stream = torch.cuda.current_stream()
@@ -476,6 +477,25 @@ def run_ops(a, torch, dev, spc, inputs):
     ms = timed(lambda: spc.backward_weight(rb, spc.OP_VSC, xv, dy, C, C))
     emit("vsc_weight_grad_3x3x3_c64", "surf128x8", ms, "mfma", fl / (ms * 1e-3) / 1e12,
          "TFLOP/s", PEAKS["bf16"], {"active_sites": N, "sum_k": sum_k})
+
+    # forward with the block epilogue (batch-norm affine, residual, ReLU) fused,
+    # against the plain forward and against the forward followed by the same
+    # epilogue as separate torch passes
+    scale = torch.from_numpy(inputs.normal_f32((C,), seed=34)).to(dev)
+    shift = torch.from_numpy(inputs.normal_f32((C,), std=0.5, seed=35)).to(dev)
+    res = feats(N, C, 36)
+    y = torch.empty((N, C), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: spc.forward_fused(rb, xv, w, scale, shift, res, True, out=y))
+    ms_plain = timed(lambda: spc.vsc_forward(rb, xv, w, shift, out=y))
+
+    def separate():
+        spc.vsc_forward(rb, xv, w, None, out=y)
+        y.copy_(torch.relu(torch.addcmul(shift, y.float(), scale) + res.float()))
+    ms_sep = timed(separate)
+    emit("vsc_fused_bn_res_relu_3x3x3_c64", "surf128x8", ms, "mfma", fl / (ms * 1e-3) / 1e12,
+         "TFLOP/s", PEAKS["bf16"],
+         {"active_sites": N, "sum_k": sum_k, "plain_forward_ms": ms_plain,
+          "forward_then_torch_epilogue_ms": ms_sep})
     rb.close()
 
 

@@ -160,6 +160,29 @@ int spconv_sc_forward(spconv_rulebook rb, int in_dt, const void* x,
                       const void* w, const float* bias, int out_dt, void* y,
                       int C_in, int C_out, void* stream);
 
+/* Forward pass of a VSC or SC layer with its block epilogue fused into the
+ * single store of the output.  The networks of Section 5 follow each
+ * convolution with batch normalisation and a ReLU acting on the active
+ * sites only, and their residual blocks add the block input back before the
+ * last ReLU; at inference the batch normalisation is an affine map per
+ * channel.  For every output row r and channel n:
+ *   z = acc[r][n] * scale[n] + shift[n] + residual[r][n]
+ *   y[r][n] = relu ? (z < 0 ? 0 : z) : z          (NaN stays NaN)
+ * computed in fp32 and rounded once to out_dt.
+ *   rb        rule book of kind SPCONV_VSC or SPCONV_SC
+ *   scale     device fp32 [C_out] or NULL (= 1)
+ *   shift     device fp32 [C_out] or NULL (= 0); with scale NULL this is the
+ *             bias of spconv_vsc_forward
+ *   residual  device [n_out][C_out] of dtype out_dt, or NULL (= 0); it may
+ *             be y itself (in place), but must not overlap y otherwise
+ *   relu      0 or 1
+ * Other arguments, ordering, determinism and ownership as
+ * spconv_vsc_forward.  Errors: EINVAL (kind, dtype, C < 1, NULL, relu not
+ * 0/1, alignment: x, w, y, residual 16 bytes, scale and shift 4 bytes). */
+int spconv_forward_fused(spconv_rulebook rb, int in_dt, const void* x, const void* w,
+                         const float* scale, const float* shift, const void* residual,
+                         int relu, int out_dt, void* y, int C_in, int C_out, void* stream);
+
 /* Sparse max- or average-pooling (Section 3: MP(f,s) takes the maximum of
  * the zero vector and the input vectors of the receptive field, AP(f,s)
  * f^-d times the sum of the active input vectors; both are variants of

@@ -22,7 +22,7 @@ from ._lib import (BF16, BUILD_ASYNC, BUILD_TRANSPOSE, EDUP, EINVAL, ENOMEM, ERA
 
 __all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "BUILD_TRANSPOSE", "OP_VSC", "OP_SC",
            "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "vsc_forward",
-           "sc_forward", "dc_forward", "pool_forward", "backward_data", "backward_weight",
+           "sc_forward", "forward_fused", "dc_forward", "pool_forward", "backward_data", "backward_weight",
            "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE", "ENOMEM", "ECAP", "EHIP"]
 
 
@@ -194,6 +194,43 @@ def vsc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
 def sc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):
     """SC forward on an SC rule book (output rows = rb.n_out)."""
     return _forward(_lib.load().spconv_sc_forward, SC, rb, x, w, bias, out_dtype, out, stream)
+
+
+def forward_fused(rb, x, w, scale=None, shift=None, residual=None, relu=False, out_dtype=None,
+                  out=None, stream=None):
+    """VSC or SC forward (the book's kind) with the block epilogue fused:
+    y = act(acc * scale + shift + residual), scale/shift float32 [C_out] or
+    None, residual [n_out, C_out] of the output dtype or None (may be `out`
+    itself), act = ReLU if relu."""
+    torch = _torch()
+    C_in, C_out = int(w.shape[1]), int(w.shape[2])
+    if w.dtype != x.dtype:
+        raise TypeError("x and w must share a dtype")
+    out_dtype = x.dtype if out_dtype is None else out_dtype
+    x, w = x.contiguous(), w.contiguous()
+    vecs = []
+    for v in (scale, shift):
+        if v is not None:
+            v = v.contiguous()
+            if v.dtype != torch.float32:
+                raise TypeError("scale and shift must be float32")
+        vecs.append(v)
+    if out is None:
+        out = torch.empty((rb.n_out, C_out), dtype=out_dtype, device=x.device)
+    if residual is not None:
+        if residual.dtype != out.dtype or tuple(residual.shape) != tuple(out.shape):
+            raise TypeError("residual must match the output's dtype and shape")
+        if not residual.is_contiguous():
+            residual = residual.contiguous()
+    if out.numel() == 0:
+        return out
+    ptr = (lambda t: t.data_ptr() if t is not None else None)
+    st = _lib.load().spconv_forward_fused(
+        rb.handle, _dtype_code(x.dtype), x.data_ptr() if x.numel() else None, w.data_ptr(),
+        ptr(vecs[0]), ptr(vecs[1]), ptr(residual), 1 if relu else 0, _dtype_code(out.dtype),
+        out.data_ptr(), C_in, C_out, _stream_ptr(stream))
+    _lib.check(st, "spconv_forward_fused")
+    return out
 
 
 def dc_forward(rb, x, w, bias=None, out_dtype=None, out=None, stream=None):

@@ -30,6 +30,7 @@ SIGNATURES = {
     "spconv_rulebook_out_coords": (_I, [_P, ctypes.POINTER(_P)]),
     "spconv_vsc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
     "spconv_sc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
+    "spconv_forward_fused": (_I, [_P, _I, _P, _P, _P, _P, _P, _I, _I, _P, _I, _I, _P]),
     "spconv_pool_forward": (_I, [_P, _I, _I, _P, _P, _I, _P]),
     "spconv_dc_forward": (_I, [_P, _I, _P, _P, _P, _I, _P, _I, _I, _P]),
     "spconv_backward_data": (_I, [_P, _I, _I, _P, _P, _I, _P, _I, _I, _P]),

@@ -276,9 +276,11 @@ int spconv_rulebook_out_coords(spconv_rulebook rb, const int32_t** coords) {
   return SPCONV_OK;
 }
 
+// Argument checks shared by the forward entry points; with check_only nothing
+// is launched.
 static int forward_common(spconv_rulebook rb, int kind, int in_dt, const void* x, const void* w,
                           const float* bias, int out_dt, void* y, int C_in, int C_out,
-                          void* stream) {
+                          void* stream, bool check_only = false) {
   if (!rb || rb->kind != kind) return SPCONV_EINVAL;
   if ((in_dt != SPCONV_F32 && in_dt != SPCONV_BF16) ||
       (out_dt != SPCONV_F32 && out_dt != SPCONV_BF16))
@@ -288,6 +290,7 @@ static int forward_common(spconv_rulebook rb, int kind, int in_dt, const void* x
   const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w) |
                        reinterpret_cast<uintptr_t>(y);
   if ((al & 15) || (reinterpret_cast<uintptr_t>(bias) & 3)) return SPCONV_EINVAL;
+  if (check_only) return SPCONV_OK;
   return forward(rb, in_dt, x, w, bias, out_dt, y, C_in, C_out, static_cast<hipStream_t>(stream));
 }
 
@@ -301,6 +304,31 @@ int spconv_sc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
                       const float* bias, int out_dt, void* y, int C_in, int C_out,
                       void* stream) {
   return forward_common(rb, SPCONV_SC, in_dt, x, w, bias, out_dt, y, C_in, C_out, stream);
+}
+
+int spconv_forward_fused(spconv_rulebook rb, int in_dt, const void* x, const void* w,
+                         const float* scale, const float* shift, const void* residual,
+                         int relu, int out_dt, void* y, int C_in, int C_out, void* stream) {
+  if (!rb || (rb->kind != SPCONV_VSC && rb->kind != SPCONV_SC)) return SPCONV_EINVAL;
+  if (relu != 0 && relu != 1) return SPCONV_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(scale) & 3) || (reinterpret_cast<uintptr_t>(residual) & 15))
+    return SPCONV_EINVAL;
+  // the residual may be y itself, but no other overlap (checked once the
+  // output row count is known on the host)
+  if (residual && residual != y && y && rb->synced && rb->n_out > 0 && C_out > 0) {
+    const size_t bytes = static_cast<size_t>(rb->n_out) * C_out * (out_dt == SPCONV_BF16 ? 2 : 4);
+    const uintptr_t r0 = reinterpret_cast<uintptr_t>(residual), y0 = reinterpret_cast<uintptr_t>(y);
+    if (r0 < y0 + bytes && y0 < r0 + bytes) return SPCONV_EINVAL;
+  }
+  const int st = forward_common(rb, rb->kind, in_dt, x, w, shift, out_dt, y, C_in, C_out,
+                                nullptr, /*check_only=*/true);
+  if (st != SPCONV_OK) return st;
+  Epilogue e;
+  e.scale = scale;
+  e.res = residual;
+  e.relu = relu;
+  return forward_view(view_of(rb), 0, in_dt, x, w, shift, out_dt, y, C_in, C_out,
+                      static_cast<hipStream_t>(stream), e);
 }
 
 static bool dtype_ok(int dt) { return dt == SPCONV_F32 || dt == SPCONV_BF16; }

@@ -22,9 +22,9 @@ FwdView view_of(spconv_rulebook rb) {
 
 int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const void* w,
                  const float* bias, int out_dt, void* y, int C_in, int C_out,
-                 hipStream_t stream) {
+                 hipStream_t stream, const Epilogue& epi) {
   if (v.n_cap == 0) return SPCONV_OK;
-  FwdCall c{v, x, 0u, w, bias, y, C_out, stream};
+  FwdCall c{v, x, 0u, w, bias, y, C_out, stream, epi};
   bool done = false;
   switch (wmode) {
     case 0: done = forward_run_w0(c, in_dt, out_dt, C_in); break;

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void k_fwd_vec(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
     const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
-    int C_out) {
+    int C_out, Epilogue epi) {
   const int64_t n_rows = hdr->n_out;
   const int64_t total = n_rows * C_out;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
@@ -107,8 +107,14 @@ __global__ __launch_bounds__(256) void k_fwd_vec(
         acc = fmaf(ElemIO<TIn>::load(x, xb + c),
                    ElemIO<TIn>::load(w, w_index<WT>(i, K, c, col, C_in, C_out)), acc);
     }
-    if (bias) acc += bias[col];
-    ElemIO<TOut>::store(y, static_cast<int64_t>(perm[p]) * C_out + col, acc);
+    const int64_t o = static_cast<int64_t>(perm[p]) * C_out + col;
+    if (epi.scale)
+      acc = fmaf(acc, epi.scale[col], bias ? bias[col] : 0.0f);
+    else if (bias)
+      acc += bias[col];
+    if (epi.res) acc += ElemIO<TOut>::load(static_cast<const TOut*>(epi.res), o);
+    if (epi.relu) acc = acc < 0.0f ? 0.0f : acc;
+    ElemIO<TOut>::store(y, o, acc);
   }
 }
 
@@ -169,6 +175,36 @@ template <int NCB> struct OutStore<uint16_t, NCB> {
   }
 };
 
+// NCB adjacent output elements as fp32 (the residual of the epilogue).
+template <typename TOut, int NCB> struct OutLoad;
+template <int NCB> struct OutLoad<float, NCB> {
+  __device__ static void load(const float* p, float* v) {
+    if constexpr (NCB == 4) {
+      const float4 u = *reinterpret_cast<const float4*>(p);
+      v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+    } else if constexpr (NCB == 2) {
+      const float2 u = *reinterpret_cast<const float2*>(p);
+      v[0] = u.x; v[1] = u.y;
+    } else {
+      v[0] = p[0];
+    }
+  }
+};
+template <int NCB> struct OutLoad<uint16_t, NCB> {
+  __device__ static void load(const uint16_t* p, float* v) {
+    if constexpr (NCB == 4) {
+      const uint2 u = *reinterpret_cast<const uint2*>(p);
+      v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
+      v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else if constexpr (NCB == 2) {
+      const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+      v[0] = __uint_as_float(u << 16); v[1] = __uint_as_float(u & 0xffff0000u);
+    } else {
+      v[0] = bf16_to_f32(p[0]);
+    }
+  }
+};
+
 __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
@@ -211,7 +247,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     const DeviceHeader* __restrict__ hdr, int K_arg,
     const TIn* __restrict__ x, uint32_t x_bytes, const TIn* __restrict__ w,
     const float* __restrict__ bias, TOut* __restrict__ y, int C_out, int64_t ntiles,
-    const int32_t* __restrict__ seg) {
+    const int32_t* __restrict__ seg, Epilogue epi) {
   // KT > 0: the offset count is a compile-time constant and the offset loop
   // is unrolled completely (no loop-carried register hazards).
   // seg != NULL: a segmented single-offset view; this tile's weights are
@@ -449,20 +485,54 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     }
   }
 
-  // ---- epilogue: bias, round once, store NCB adjacent columns per lane-row
-  float bv[NCB];
+  // ---- epilogue: (scale,) bias, (residual, ReLU), round once, store NCB
+  // adjacent columns per lane-row
+  float bv[NCB], sv[NCB];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
+  for (int cb = 0; cb < NCB; ++cb) {
+    bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
+    sv[cb] = epi.scale ? epi.scale[col0 + lr * NCB + cb] : 1.0f;
+  }
+  // All output rows first, then all residual loads (row -1, the padding of a
+  // segmented view, reads row 0, which exists whenever this tile runs), so
+  // that their latencies overlap instead of one per store.
+  int64_t rows[RB][4];
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
+      rows[b][v] = pos < n_rows ? perm[pos] : -1;
+    }
+  const TOut* res = static_cast<const TOut*>(epi.res);
+  float r[RB][4][NCB];
+  if (res) {
+#pragma unroll
+    for (int b = 0; b < RB; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = rows[b][v] >= 0 ? rows[b][v] : 0;
+        OutLoad<TOut, NCB>::load(res + row * C_out + col0 + lr * NCB, r[b][v]);
+      }
+  }
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
-      const int64_t row = pos < n_rows ? perm[pos] : -1;
+      const int64_t row = rows[b][v];
       if (row >= 0) {                                   // -1: padding of a segmented view
         float o[NCB];
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
+        for (int cb = 0; cb < NCB; ++cb)
+          o[cb] = epi.scale ? fmaf(acc[b][cb][v], sv[cb], bv[cb]) : acc[b][cb][v] + bv[cb];
+        if (res) {
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) o[cb] += r[b][v][cb];
+        }
+        if (epi.relu) {
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) o[cb] = o[cb] < 0.0f ? 0.0f : o[cb];
+        }
         OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
       }
     }
@@ -498,7 +568,7 @@ void launch_mfma(const Call& c) {
   kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), c.x_bytes, static_cast<const TIn*>(c.w), c.bias,
-      static_cast<TOut*>(c.y), c.C_out, ntiles, c.v.seg);
+      static_cast<TOut*>(c.y), c.C_out, ntiles, c.v.seg, c.epi);
 }
 
 template <typename TIn, int NCH, typename TOut, int WT>
@@ -549,7 +619,7 @@ void launch_vec(const Call& c, int C_in) {
   k_fwd_vec<TIn, TOut, WT><<<static_cast<unsigned>(blocks), 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), static_cast<const TIn*>(c.w), c.bias, static_cast<TOut*>(c.y),
-      C_in, c.C_out);
+      C_in, c.C_out, c.epi);
 }
 
 template <int WT>

@@ -223,6 +223,18 @@ struct FwdView {
 };
 constexpr int kSegRows = 256;
 FwdView view_of(spconv_rulebook rb);
+// Optional epilogue of a forward.  The networks of Section 5 follow each
+// convolution with batch normalisation (at inference a per-channel affine
+// map), add the block input back in residual blocks, and apply a ReLU, all at
+// the active output sites; fused here into the single store of the output:
+//   out[r][n] = act(acc[r][n] * scale[n] + bias[n] + res[r][n])
+// scale NULL = 1, res NULL = 0 (res has the output's dtype and layout),
+// relu 0 = identity, 1 = max(., 0) with NaN kept.
+struct Epilogue {
+  const float* scale = nullptr;
+  const void* res = nullptr;
+  int relu = 0;
+};
 struct FwdCall {
   FwdView v;
   const void* x;
@@ -232,6 +244,7 @@ struct FwdCall {
   void* y;
   int C_out;
   hipStream_t stream;
+  Epilogue epi;
 };
 // Each returns false when the view is segmented and no matrix-core kernel
 // fits the shape (nothing is launched then).
@@ -242,7 +255,7 @@ bool forward_run_w2(const FwdCall& c, int in_dt, int out_dt, int C_in);
 // as [K][C_out][C_in] of the layer whose gradient this is).
 int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const void* w,
                  const float* bias, int out_dt, void* y, int C_in, int C_out,
-                 hipStream_t stream);
+                 hipStream_t stream, const Epilogue& epi = Epilogue{});
 int forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
             const float* bias, int out_dt, void* y, int C_in, int C_out,
             hipStream_t stream);

@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -88,6 +88,8 @@ def test_new_entry_points_reject_bad_arguments_on_the_host():
     E = _lib.EINVAL
     assert lib.spconv_pool_forward(None, 0, 0, None, None, 4, None) == E
     assert lib.spconv_dc_forward(None, 0, None, None, None, 0, None, 1, 1, None) == E
+    assert lib.spconv_forward_fused(None, 0, None, None, None, None, None, 0, 0, None, 1, 1,
+                                    None) == E
     assert lib.spconv_backward_data(None, 0, 0, None, None, 0, None, 1, 1, None) == E
     nbytes = ctypes.c_size_t()
     assert lib.spconv_backward_weight_workspace(None, 0, 1, 1, ctypes.byref(nbytes)) == E

@@ -224,3 +224,99 @@ def test_gradient_op_must_match_the_book():
             spc.backward_data(vsc, op, dy, w)
         with pytest.raises(spc.SpconvError):
             spc.backward_weight(vsc, op, dy, dy, 8, 8)
+
+
+# ---------------------------------------------------------------------------
+# Forward with the block epilogue fused (affine per channel, residual, ReLU)
+# ---------------------------------------------------------------------------
+
+FUSED_CASES = [
+    # kind, case, f, s, C_in, C_out, dtype, out dtype
+    ("vsc", "surf", [1, 3, 3, 3], [1, 1, 1, 1], 64, 64, "bf16", "bf16"),
+    ("vsc", "surf", [1, 3, 3, 3], [1, 1, 1, 1], 32, 32, "f32", "f32"),
+    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 1, 16, "f32", "f32"),        # vector path
+    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 16, 24, "bf16", "f32"),      # vector path
+    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 32, 32, "bf16", "bf16"),     # 2 column blocks
+    ("sc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 64, "bf16", "bf16"),
+    ("sc", "pen", [1, 3, 3], [1, 2, 2], 32, 16, "f32", "bf16"),       # 1 column block
+]
+PARTS = {"all": (1, 1, 1, 1), "affine": (1, 1, 0, 0), "res_relu": (0, 0, 1, 1),
+         "scale_relu": (1, 0, 0, 1)}
+
+
+def _fused_setup(kind, case, f, s, C_in, C_out, dtype, out_dtype):
+    coords, size = _sites(case)
+    K = int(np.prod(f))
+    sk, ok = (spc.VSC, oracle.VSC) if kind == "vsc" else (spc.SC, oracle.SC)
+    rb = spc.build_rulebook(sk, _t(coords), size, f, s)
+    ref = oracle.Rulebook(ok, coords, size, f, s)
+    x = _feats(len(coords), C_in, dtype, 61)
+    wf = inputs.normal_f32((K, C_in, C_out), std=1.0 / np.sqrt(K * C_in), seed=62)
+    w = inputs.to_bf16_bits(wf) if dtype == "bf16" else wf
+    scale = inputs.normal_f32((C_out,), std=1.0, seed=63)
+    shift = inputs.normal_f32((C_out,), std=0.5, seed=64)
+    res = _feats(ref.n_out, C_out, out_dtype, 65)
+    return coords, rb, ref, x, w, scale, shift, res
+
+
+@pytest.mark.parametrize("parts", list(PARTS))
+@pytest.mark.parametrize("kind,case,f,s,C_in,C_out,dtype,out_dtype", FUSED_CASES)
+def test_fused_forward_matches_oracle(kind, case, f, s, C_in, C_out, dtype, out_dtype, parts):
+    coords, rb, ref, x, w, scale, shift, res = _fused_setup(kind, case, f, s, C_in, C_out, dtype,
+                                                            out_dtype)
+    use_s, use_b, use_r, relu = PARTS[parts]
+    _say(f"[fused] {kind} {case} N={len(coords)} f={f} s={s} C={C_in}->{C_out} {dtype}->"
+         f"{out_dtype} {parts}")
+    odt = torch.bfloat16 if out_dtype == "bf16" else torch.float32
+    y = spc.forward_fused(rb, _dev(x, dtype), _dev(w, dtype),
+                          scale=_t(scale) if use_s else None, shift=_t(shift) if use_b else None,
+                          residual=_dev(res, out_dtype) if use_r else None, relu=bool(relu),
+                          out_dtype=odt)
+    y64, absb = ref.forward(x, w, None, in_dt=_odt(dtype))
+    zo, bound = oracle.fused_epilogue(y64, absb, scale if use_s else None,
+                                      shift if use_b else None, res if use_r else None,
+                                      bool(relu), _odt(out_dtype))
+    rtol = RTOL_F32 if dtype == "f32" and out_dtype == "f32" else RTOL_BF16
+    g = _to_np(y)
+    check_features(g, zo, bound, rtol, "fused")
+    if relu:
+        assert (g >= 0).all()
+
+
+def test_fused_forward_reduces_to_the_plain_forward():
+    """scale = residual = NULL, no ReLU: bit for bit the forward with bias."""
+    for args in (FUSED_CASES[0], FUSED_CASES[2], FUSED_CASES[5]):
+        kind, case, f, s, C_in, C_out, dtype, out_dtype = args
+        _, rb, _, x, w, _, shift, _ = _fused_setup(*args)
+        odt = torch.bfloat16 if out_dtype == "bf16" else torch.float32
+        fwd = spc.vsc_forward if kind == "vsc" else spc.sc_forward
+        y0 = fwd(rb, _dev(x, dtype), _dev(w, dtype), _t(shift), out_dtype=odt)
+        y1 = spc.forward_fused(rb, _dev(x, dtype), _dev(w, dtype), shift=_t(shift), out_dtype=odt)
+        assert torch.equal(y0, y1), args
+
+
+def test_fused_forward_in_place_residual_and_overlap_errors():
+    args = FUSED_CASES[0]
+    kind, case, f, s, C_in, C_out, dtype, out_dtype = args
+    _, rb, ref, x, w, scale, shift, res = _fused_setup(*args)
+    xd, wd = _dev(x, dtype), _dev(w, dtype)
+    r = _dev(res, out_dtype)
+    y = spc.forward_fused(rb, xd, wd, _t(scale), _t(shift), r, True)
+    buf = r.clone()
+    y2 = spc.forward_fused(rb, xd, wd, _t(scale), _t(shift), buf, True, out=buf)
+    assert y2.data_ptr() == buf.data_ptr()
+    assert torch.equal(y, y2)
+    n = ref.n_out * C_out
+    big = torch.zeros(2 * n + 64, dtype=torch.bfloat16, device="cuda")
+    out = big[:n].view(ref.n_out, C_out)
+    shifted = big[64:64 + n].view(ref.n_out, C_out)     # overlaps out, not equal to it
+    with pytest.raises(spc.SpconvError):
+        spc.forward_fused(rb, xd, wd, residual=shifted, out=out)
+    lib = spc._lib.load()
+    ptr = out.data_ptr()
+    st = lib.spconv_forward_fused(rb.handle, spc.BF16, xd.data_ptr(), wd.data_ptr(), None, None,
+                                  ptr + 2 * n + 8, 0, spc.BF16, ptr, C_in, C_out, None)
+    assert st == spc._lib.EINVAL                       # residual not 16-byte aligned
+    st = lib.spconv_forward_fused(rb.handle, spc.BF16, xd.data_ptr(), wd.data_ptr(), None, None,
+                                  None, 2, spc.BF16, ptr, C_in, C_out, None)
+    assert st == spc._lib.EINVAL                       # relu not 0 / 1
