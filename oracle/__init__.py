@@ -66,7 +66,7 @@ def _load():
     lib.ref_dc_forward.restype = I32
     lib.ref_backward_data.argtypes = [P, I32, I32, P, P, I32, I32, P, P]
     lib.ref_backward_data.restype = I32
-    lib.ref_backward_weight.argtypes = [P, I32, I32, P, P, I32, I32, P, P, P, P]
+    lib.ref_backward_weight.argtypes = [P, I32, I32, P, P, I32, I32, P, P, P, P, P]
     lib.ref_backward_weight.restype = I32
     lib.ref_round.argtypes = [P, I64, I32, P]
     lib.ref_round.restype = I32
@@ -197,8 +197,11 @@ class Rulebook:
             raise OracleError(st)
         return dx, absb
 
-    def backward_weight(self, op, x, dy, C_in, C_out, dt=F32):
-        """(dw [K, C_in, C_out], db [C_out], absb_w, absb_b), all float64."""
+    def backward_weight(self, op, x, dy, C_in, C_out, dt=F32, offsets=None):
+        """(dw [K, C_in, C_out], db [C_out], absb_w, absb_b), all float64.
+
+        offsets: indices of the W^i to compute (the others stay zero), or
+        None for all of them."""
         lib = _load()
         x = np.ascontiguousarray(x)
         dy = np.ascontiguousarray(dy)
@@ -206,8 +209,12 @@ class Rulebook:
         aw = np.zeros_like(dw)
         db = np.zeros(C_out, np.float64)
         ab = np.zeros(C_out, np.float64)
+        mask = None
+        if offsets is not None:
+            mask = np.zeros(self.K, np.uint8)
+            mask[np.asarray(offsets)] = 1
         st = lib.ref_backward_weight(self._h, op, dt, _ptr(x), _ptr(dy), C_in, C_out,
-                                     _ptr(dw), _ptr(db), _ptr(aw), _ptr(ab))
+                                     _ptr(dw), _ptr(db), _ptr(aw), _ptr(ab), _ptr(mask))
         if st != OK:
             raise OracleError(st)
         return dw, db, aw, ab

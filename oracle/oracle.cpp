@@ -435,8 +435,11 @@ int ref_backward_data(void* h, int op, int dt, const void* dy, const void* w, in
 //      dw[i][c][n] = sum_{(a,b) in R_i} x[b][c] dy[a][n]
 //   db[n] = sum of dy[.][n] over all output rows (NULL: skipped)
 //   dw / db / absb_w / absb_b: host double; absb_* (sum of |terms|) or NULL
+//   omask: host [K], nonzero = compute dw for that offset (others stay 0);
+//          NULL = every offset
 int ref_backward_weight(void* h, int op, int dt, const void* x, const void* dy, int C_in,
-                        int C_out, double* dw, double* db, double* absb_w, double* absb_b) {
+                        int C_out, double* dw, double* db, double* absb_w, double* absb_b,
+                        const uint8_t* omask) {
   if (!h || C_in < 1 || C_out < 1 || (dt != F32 && dt != BF16)) return EINVAL_;
   auto* rb = static_cast<Rulebook*>(h);
   if (op == DC ? rb->kind != SC : op != rb->kind) return EINVAL_;
@@ -445,7 +448,8 @@ int ref_backward_weight(void* h, int op, int dt, const void* x, const void* dy, 
     dw[k] = 0.0;
     if (absb_w) absb_w[k] = 0.0;
   }
-  for (int64_t i = 0; i < rb->K; ++i)
+  for (int64_t i = 0; i < rb->K; ++i) {
+    if (omask && !omask[i]) continue;
     for (const auto& pr : rb->R[i]) {
       const int64_t xr = op == DC ? pr[1] : pr[0];
       const int64_t gr = op == DC ? pr[0] : pr[1];
@@ -458,6 +462,7 @@ int ref_backward_weight(void* h, int op, int dt, const void* x, const void* dy, 
         }
       }
     }
+  }
   if (db) {
     const int64_t out_rows = op == DC ? rb->n_in : rb->n_out;
     for (int n = 0; n < C_out; ++n) {

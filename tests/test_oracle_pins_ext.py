@@ -326,3 +326,21 @@ def test_fused_epilogue_bf16_residual():
     out, bound = oracle.fused_epilogue(y, np.abs(y), residual=bits, res_dt=oracle.BF16)
     np.testing.assert_array_equal(out, y + exact)
     np.testing.assert_array_equal(bound, np.abs(y) + np.abs(exact))
+
+
+def test_weight_gradient_offset_subset():
+    """Computing a subset of the W^i gives those W^i unchanged, zeros elsewhere."""
+    rng = np.random.default_rng(960)
+    size, coords = _sites(rng, 2, 9, 2, 0.4)
+    rb = oracle.Rulebook(oracle.VSC, coords, size, [1, 3, 3])
+    x = rng.standard_normal((len(coords), 3)).astype(np.float32)
+    dy = rng.standard_normal((len(coords), 4)).astype(np.float32)
+    full = rb.backward_weight(oracle.VSC, x, dy, 3, 4)
+    part = rb.backward_weight(oracle.VSC, x, dy, 3, 4, offsets=[0, 4, 7])
+    for i in range(9):
+        if i in (0, 4, 7):
+            np.testing.assert_array_equal(part[0][i], full[0][i])
+            np.testing.assert_array_equal(part[2][i], full[2][i])
+        else:
+            assert not part[0][i].any() and not part[2][i].any()
+    np.testing.assert_array_equal(part[1], full[1])
