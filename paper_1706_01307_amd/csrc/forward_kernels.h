@@ -241,7 +241,7 @@ struct WImage {
 // of W^i, and W^(i+1) (fetched one iteration earlier) is written transposed
 // into the other LDS buffer.  One barrier per offset publishes W^(i+1).
 template <typename TIn, int NCH, int NCB, int RB, typename TOut, int KT, bool SKIP = false,
-          int WT = 0, bool LSKIP = false>
+          int WT = 0, bool LSKIP = false, bool EPI = false>
 __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     const DeviceHeader* __restrict__ hdr, int K_arg,
@@ -485,55 +485,72 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
     }
   }
 
-  // ---- epilogue: (scale,) bias, (residual, ReLU), round once, store NCB
+  // ---- epilogue: bias (EPI: scale, residual, ReLU), round once, store NCB
   // adjacent columns per lane-row
-  float bv[NCB], sv[NCB];
+  float bv[NCB];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
-    sv[cb] = epi.scale ? epi.scale[col0 + lr * NCB + cb] : 1.0f;
-  }
-  // All output rows first, then all residual loads (row -1, the padding of a
-  // segmented view, reads row 0, which exists whenever this tile runs), so
-  // that their latencies overlap instead of one per store.
-  int64_t rows[RB][4];
+  for (int cb = 0; cb < NCB; ++cb) bv[cb] = bias ? bias[col0 + lr * NCB + cb] : 0.0f;
+  if constexpr (!EPI) {
 #pragma unroll
-  for (int b = 0; b < RB; ++b)
+    for (int b = 0; b < RB; ++b) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
-      rows[b][v] = pos < n_rows ? perm[pos] : -1;
+      for (int v = 0; v < 4; ++v) {
+        const int64_t pos = row0 + b * 16 + lg * 4 + v;   // schedule position
+        const int64_t row = pos < n_rows ? perm[pos] : -1;
+        if (row >= 0) {                                   // -1: padding of a segmented view
+          float o[NCB];
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) o[cb] = acc[b][cb][v] + bv[cb];
+          OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
+        }
+      }
     }
-  const TOut* res = static_cast<const TOut*>(epi.res);
-  float r[RB][4][NCB];
-  if (res) {
+  } else {
+    // the block epilogue: all output rows first, then all residual loads (a
+    // row of -1, padding, reads row 0, which exists whenever this tile runs),
+    // so that their latencies overlap instead of one per store
+    float sv[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) sv[cb] = epi.scale ? epi.scale[col0 + lr * NCB + cb] : 1.0f;
+    int64_t rows[RB][4];
 #pragma unroll
     for (int b = 0; b < RB; ++b)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t row = rows[b][v] >= 0 ? rows[b][v] : 0;
-        OutLoad<TOut, NCB>::load(res + row * C_out + col0 + lr * NCB, r[b][v]);
+        const int64_t pos = row0 + b * 16 + lg * 4 + v;
+        rows[b][v] = pos < n_rows ? perm[pos] : -1;
       }
-  }
+    const TOut* res = static_cast<const TOut*>(epi.res);
+    float r[RB][4][NCB];
+    if (res) {
 #pragma unroll
-  for (int b = 0; b < RB; ++b) {
+      for (int b = 0; b < RB; ++b)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t row = rows[b][v];
-      if (row >= 0) {                                   // -1: padding of a segmented view
-        float o[NCB];
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-          o[cb] = epi.scale ? fmaf(acc[b][cb][v], sv[cb], bv[cb]) : acc[b][cb][v] + bv[cb];
-        if (res) {
-#pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) o[cb] += r[b][v][cb];
+        for (int v = 0; v < 4; ++v) {
+          const int64_t row = rows[b][v] >= 0 ? rows[b][v] : 0;
+          OutLoad<TOut, NCB>::load(res + row * C_out + col0 + lr * NCB, r[b][v]);
         }
-        if (epi.relu) {
+    }
 #pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) o[cb] = o[cb] < 0.0f ? 0.0f : o[cb];
+    for (int b = 0; b < RB; ++b) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = rows[b][v];
+        if (row >= 0) {
+          float o[NCB];
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb)
+            o[cb] = epi.scale ? fmaf(acc[b][cb][v], sv[cb], bv[cb]) : acc[b][cb][v] + bv[cb];
+          if (res) {
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) o[cb] += r[b][v][cb];
+          }
+          if (epi.relu) {
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) o[cb] = o[cb] < 0.0f ? 0.0f : o[cb];
+          }
+          OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
         }
-        OutStore<TOut, NCB>::store(y + row * C_out + col0 + lr * NCB, o);
       }
     }
   }
@@ -565,6 +582,13 @@ void launch_mfma(const Call& c) {
   auto kern = c.v.K == 27  ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
               : c.v.K == 1 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 1, true, WT>
                            : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
+  // The block epilogue (scale / residual / ReLU) is compiled into its own
+  // kernels, so that the plain forward keeps its register count.
+  if constexpr (WT == 0) {
+    if (c.epi.scale || c.epi.res || c.epi.relu)
+      kern = c.v.K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT, false, true>
+                         : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true, true>;
+  }
   kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), c.x_bytes, static_cast<const TIn*>(c.w), c.bias,

@@ -363,6 +363,7 @@ __global__ __launch_bounds__(256) void k_dw_partial(
 typedef short dw_s4 __attribute__((ext_vector_type(4)));
 typedef __bf16 dw_bf8 __attribute__((ext_vector_type(8)));
 typedef float dw_f4 __attribute__((ext_vector_type(4)));
+typedef unsigned dw_u4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, int lane) {
   // lanes 16q + j: pairs p0 + 8q + j/4 (+4 for the upper half), channels c0 + 4(j%4)..+3
@@ -388,7 +389,7 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
   constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
   // staging tiles; the final wave reduction reuses the same bytes
   __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * STEP * 64];
-  __shared__ int32_t s_a[2][STEP], s_b[2][STEP];
+  __shared__ int2 s_pr[kChunk];                  // the chunk's pairs
   uint16_t* s_x = s_buf;
   uint16_t* s_g = s_buf + STEP * 64;
   const int i = blockIdx.y, chunk = blockIdx.x;
@@ -404,43 +405,42 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
   const int cx = C_in - c0 < 64 ? C_in - c0 : 64;     // valid columns of this tile
   const int cg = C_out - n0 < 64 ? C_out - n0 : 64;
 
-  // pair rows of step t -> s_a / s_b [t & 1] (input row, gradient row);
-  // DC reads its pairs backwards; -1 past the end of the chunk
-  auto rows_of = [&](int t) {
-    if (threadIdx.x < STEP) {
-      const int64_t e = start + static_cast<int64_t>(t) * STEP + threadIdx.x;
-      int32_t a = -1, b = -1;
-      if (t < nsteps && e < end) {
-        a = pairs[2 * (base + e)];
-        b = pairs[2 * (base + e) + 1];
-      }
-      s_a[t & 1][threadIdx.x] = DC ? b : a;
-      s_b[t & 1][threadIdx.x] = DC ? a : b;
+  // The chunk's pairs go to LDS once.  Then, over steps of STEP pairs: at
+  // step t the data rows of step t + 2 are gathered into one of two register
+  // sets, the MFMAs of step t run on the LDS tiles, and the rows of step t + 1
+  // (the other set) are written to LDS.  Every gather is unconditional (rows
+  // past the chunk and columns past C read row 0 / column 0 and are zeroed
+  // when staged), so no load sits under a branch and the in-order load
+  // counter keeps step t + 2's rows in flight while step t + 1's are waited on.
+  const int npairs = static_cast<int>(end - start);
+  for (int e = threadIdx.x; e < npairs; e += 256)
+    s_pr[e] = *reinterpret_cast<const int2*>(pairs + 2 * (base + start + e));
+  const int ch = (threadIdx.x % 8) * 8;                // this lane's 8 columns
+  const bool colx = ch < cx, colg = ch < cg;
+  typedef dw_u4 Rows[PASS];
+  auto gather = [&](int t, Rows& vx, Rows& vg, uint32_t& ok) __attribute__((always_inline)) {
+    ok = 0;
+#pragma unroll
+    for (int pass = 0; pass < PASS; ++pass) {
+      const int e = t * STEP + pass * 32 + threadIdx.x / 8;
+      const int2 pr = s_pr[e < npairs ? e : 0];
+      // (input row, gradient row); DC reads its pairs backwards
+      const int32_t ra = DC ? pr.y : pr.x, rg = DC ? pr.x : pr.y;
+      const bool okx = e < npairs && colx, okg = e < npairs && colg;
+      ok |= (okx ? 1u : 0u) << (2 * pass) | (okg ? 2u : 0u) << (2 * pass);
+      vx[pass] = *reinterpret_cast<const dw_u4*>(
+          x + (okx ? static_cast<int64_t>(ra) * C_in + c0 + ch : 0));
+      vg[pass] = *reinterpret_cast<const dw_u4*>(
+          dy + (okg ? static_cast<int64_t>(rg) * C_out + n0 + ch : 0));
     }
   };
-  uint4 vx[PASS], vg[PASS];
-  // gather the rows of step t into registers (8 lanes per 128-byte row)
-  auto gather = [&](int t) {
-    const int ch = (threadIdx.x % 8) * 8;
+  auto stage = [&](const Rows& vx, const Rows& vg, uint32_t ok) __attribute__((always_inline)) {
+    const dw_u4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int pass = 0; pass < PASS; ++pass) {
       const int pp = pass * 32 + threadIdx.x / 8;
-      const int32_t ra = s_a[t & 1][pp], rg = s_b[t & 1][pp];
-      vx[pass] = uint4{0u, 0u, 0u, 0u};
-      vg[pass] = uint4{0u, 0u, 0u, 0u};
-      if (ra >= 0 && ch < cx)
-        vx[pass] = *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(ra) * C_in + c0 + ch);
-      if (rg >= 0 && ch < cg)
-        vg[pass] = *reinterpret_cast<const uint4*>(dy + static_cast<int64_t>(rg) * C_out + n0 + ch);
-    }
-  };
-  auto stage = [&]() {
-    const int ch = (threadIdx.x % 8) * 8;
-#pragma unroll
-    for (int pass = 0; pass < PASS; ++pass) {
-      const int pp = pass * 32 + threadIdx.x / 8;
-      *reinterpret_cast<uint4*>(&s_x[pp * 64 + ch]) = vx[pass];
-      *reinterpret_cast<uint4*>(&s_g[pp * 64 + ch]) = vg[pass];
+      *reinterpret_cast<dw_u4*>(&s_x[pp * 64 + ch]) = (ok >> (2 * pass)) & 1u ? vx[pass] : z;
+      *reinterpret_cast<dw_u4*>(&s_g[pp * 64 + ch]) = (ok >> (2 * pass)) & 2u ? vg[pass] : z;
     }
   };
 
@@ -450,17 +450,20 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
 #pragma unroll
     for (int v = 0; v < 4; ++v) acc[u][v] = dw_f4{0.f, 0.f, 0.f, 0.f};
 
-  // prologue: rows of steps 0 and 1, data of step 0 into LDS
-  rows_of(0);
-  rows_of(1);
+  Rows xa, ga, xb, gb;
+  uint32_t oka = 0, okb = 0;
+  __syncthreads();                             // pairs in LDS
+  gather(0, xa, ga, oka);
+  gather(1, xb, gb, okb);
+  stage(xa, ga, oka);
   __syncthreads();
-  gather(0);
-  stage();
-  __syncthreads();
-  for (int t = 0; t < nsteps; ++t) {
-    // next step's rows in flight while this one multiplies
-    if (t + 1 < nsteps) gather(t + 1);
-    const int p0 = wave * 32;
+  const int p0 = wave * 32;
+  // step t: the set holding step t + 1 is `nx`, the free set `fr`
+  // (the gather of step t + 2 is issued even past the last step, as rows that
+  // are all zeroed, so that the number of loads in flight never depends on t)
+  auto step = [&](int t, Rows& nxx, Rows& nxg, uint32_t& nok, Rows& frx, Rows& frg,
+                  uint32_t& fok) __attribute__((always_inline)) {
+    gather(t + 2, frx, frg, fok);
     dw_bf8 fa[4], fb[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) fa[u] = tr_frag(s_x, p0, u * 16, lane);
@@ -471,13 +474,16 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[v], acc[u][v], 0, 0, 0);
-    __syncthreads();                          // tiles and s_a/s_b[t & 1] free
-    if (t + 1 < nsteps) {
-      stage();
-      rows_of(t + 2);
-    }
+    __syncthreads();                           // tiles free
+    if (t + 1 < nsteps) stage(nxx, nxg, nok);
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < nsteps; t += 2) {
+    step(t, xb, gb, okb, xa, ga, oka);
+    step(t + 1, xa, ga, oka, xb, gb, okb);
   }
+  if (t < nsteps) step(t, xb, gb, okb, xa, ga, oka);
   // wave partials -> LDS (one 16-row band of the tile at a time), summed in
   // wave order; lane (r, g) holds rows 4g + e, column r of each 16x16 block
   float (*s_red)[16][64 + 4] = reinterpret_cast<float (*)[16][64 + 4]>(s_buf);
@@ -593,23 +599,31 @@ __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, in
   }
 }
 
-// Bias gradient, stage 2: 16 columns per workgroup; lane (phase q, column)
-// adds chunk partials q, q + 16, ... (into 4 accumulators by round), then the
-// 16 phases are added in a fixed tree.
+// Bias gradient, stage 2: 4 columns per workgroup; lane (phase q of 64,
+// column) adds chunk partials q, q + 64, ... eight loads at a time into 8
+// accumulators (by round), then the 64 phases are added in a fixed tree.
 __global__ __launch_bounds__(256) void k_db_reduce(const float* __restrict__ partb, int nchunks,
                                                    int C_out, float* __restrict__ db) {
-  __shared__ float s[16][17];
-  const int q = threadIdx.x / 16, cn = threadIdx.x % 16;
-  const int n = blockIdx.x * 16 + cn;
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  constexpr int kPh = 64, kCols = 4;
+  __shared__ float s[kPh][kCols + 1];
+  const int q = threadIdx.x / kCols, cn = threadIdx.x % kCols;
+  const int n = blockIdx.x * kCols + cn;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (n < C_out) {
-    int k = 0;
-    for (int ch = q; ch < nchunks; ch += 16, ++k)
-      a[k & 3] += partb[static_cast<int64_t>(ch) * C_out + n];
+    int ch = q;
+    for (; ch + 7 * kPh < nchunks; ch += 8 * kPh) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = partb[static_cast<int64_t>(ch + u * kPh) * C_out + n];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a[u] += v[u];
+    }
+    for (int u = 0; ch < nchunks; ch += kPh, ++u)
+      a[u] += partb[static_cast<int64_t>(ch) * C_out + n];
   }
-  s[q][cn] = (a[0] + a[1]) + (a[2] + a[3]);
+  s[q][cn] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   __syncthreads();
-  for (int h = 8; h >= 1; h >>= 1) {
+  for (int h = kPh / 2; h >= 1; h >>= 1) {
     if (q < h) s[q][cn] += s[q + h][cn];
     __syncthreads();
   }
@@ -850,7 +864,7 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
         k_db_partial<uint16_t><<<g, 256, 0, st>>>(static_cast<const uint16_t*>(dy), rows, C_out,
                                                   partb);
     }
-    k_db_reduce<<<(C_out + 15) / 16, 256, 0, st>>>(partb, nrc, C_out, db);
+    k_db_reduce<<<(C_out + 3) / 4, 256, 0, st>>>(partb, nrc, C_out, db);
   }
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
