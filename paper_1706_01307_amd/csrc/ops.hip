@@ -28,7 +28,9 @@
 // offsets to walk.
 //
 // Weight gradient dW^i = sum over the pairs of R_i of (input row)^T x (output
-// gradient row): R_i is cut into chunks of kChunk pairs; one workgroup forms
+// gradient row): the output positions of the rule book's schedule are cut
+// into chunks of kChunk positions, and chunk c of R_i is its pairs whose
+// output lies in chunk c (at most kChunk of them); one workgroup forms
 // the fp32 partial product of a chunk for a 64x64 tile of dW^i (bf16: on the
 // matrix cores, pairs gathered row-major into LDS and read back transposed;
 // fp32 and odd widths: vector ALU, 4x4 outputs per lane), and a second kernel
@@ -276,27 +278,50 @@ __global__ __launch_bounds__(256) void k_scatter_transpose(
 // ---------------------------------------------------------------------------
 // Weight and bias gradients
 // ---------------------------------------------------------------------------
-constexpr int64_t kChunk = 4096;   // pairs per partial product
+constexpr int64_t kChunk = 4096;   // output positions (so at most as many pairs) per partial
 constexpr int kSub = 64;           // pairs staged in LDS at a time
+
+// The (offset, chunk) of this workgroup and its pair range inside R_i, from
+// the rule book's per-block bases (blk_base[i][b] = first pair of R_i whose
+// output is in block b of kBlock positions).  Workgroup L runs on XCD L mod 8;
+// the K offsets of one chunk go to one XCD, so that the rows they share
+// (every output row of the chunk, and its neighbours) meet in that L2.
+struct DwChunk {
+  int i, c;
+  int64_t start, end;      // pair range [start, end) relative to R_i
+};
+__device__ __forceinline__ bool dw_chunk(const int32_t* blk_base, const int64_t* pair_off,
+                                         int64_t nblk, int K, int nchunk, DwChunk* d) {
+  const int L = blockIdx.x, xcd = L % 8, q = L / 8;
+  d->c = xcd + 8 * (q / K);
+  d->i = q % K;
+  if (d->c >= nchunk) return false;
+  constexpr int64_t kBpc = kChunk / kBlock;     // rule-book blocks per chunk
+  const int64_t b0 = d->c * kBpc, b1 = b0 + kBpc;
+  const int64_t k_i = pair_off[d->i + 1] - pair_off[d->i];
+  d->start = blk_base[d->i * nblk + b0];
+  d->end = b1 < nblk ? blk_base[d->i * nblk + b1] : k_i;
+  return true;
+}
 constexpr int64_t kRowChunk = 512;    // rows per bias-gradient partial
 
-// grid: (chunk, offset, tile); tile = (c-block of 64) x (n-block of 64).
+// grid: (8 K ceil(nchunk / 8) (offset, chunk) pairs, see dw_chunk; tile);
+// tile = (c-block of 64) x (n-block of 64).
 template <typename T, bool DC>
 __global__ __launch_bounds__(256) void k_dw_partial(
     const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
-    const T* __restrict__ x, const T* __restrict__ dy, int C_in, int C_out, int maxchunks,
-    float* __restrict__ part) {
+    const int32_t* __restrict__ blk_base, int64_t nblk, const T* __restrict__ x,
+    const T* __restrict__ dy, int C_in, int C_out, int K, int nchunk, float* __restrict__ part) {
   __shared__ float s_x[kSub][64 + 1];
   __shared__ float s_g[kSub][64 + 1];
   __shared__ int32_t s_a[kSub], s_b[kSub];
-  const int i = blockIdx.y, chunk = blockIdx.x;
+  DwChunk dc_;
+  if (!dw_chunk(blk_base, pair_off, nblk, K, nchunk, &dc_)) return;
+  const int i = dc_.i, chunk = dc_.c;
   const int ntn = (C_out + 63) / 64;
-  const int c0 = (blockIdx.z / ntn) * 64, n0 = (blockIdx.z % ntn) * 64;
+  const int c0 = (blockIdx.y / ntn) * 64, n0 = (blockIdx.y % ntn) * 64;
   const int64_t base = pair_off[i];
-  const int64_t k_i = pair_off[i + 1] - base;
-  const int64_t start = static_cast<int64_t>(chunk) * kChunk;
-  if (start >= k_i) return;
-  const int64_t end = start + kChunk < k_i ? start + kChunk : k_i;
+  const int64_t start = dc_.start, end = dc_.end;
   const int tc = threadIdx.x / 16, tn = threadIdx.x % 16;
   float acc[4][4];
 #pragma unroll
@@ -337,7 +362,7 @@ __global__ __launch_bounds__(256) void k_dw_partial(
     }
     __syncthreads();
   }
-  float* out = part + (static_cast<int64_t>(i) * maxchunks + chunk) * C_in * C_out;
+  float* out = part + (static_cast<int64_t>(i) * nchunk + chunk) * C_in * C_out;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int c = c0 + tc * 4 + u;
@@ -365,14 +390,22 @@ typedef __bf16 dw_bf8 __attribute__((ext_vector_type(8)));
 typedef float dw_f4 __attribute__((ext_vector_type(4)));
 typedef unsigned dw_u4 __attribute__((ext_vector_type(4)));
 
+// Tiles of 64-channel rows (128 bytes) in LDS store the 16-byte chunk k of
+// row r at chunk k ^ (r & 7): the rows read together by one transposing read
+// then fall on different banks (unswizzled 128-byte rows all start on the
+// same bank).
+__device__ __forceinline__ int dw_swz(int row, int col) {
+  return row * 64 + ((((col >> 3) ^ (row & 7)) << 3) | (col & 7));
+}
+
 __device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, int lane) {
   // lanes 16q + j: pairs p0 + 8q + j/4 (+4 for the upper half), channels c0 + 4(j%4)..+3
   const int j = lane & 15, q = lane >> 4;
   const int row = p0 + 8 * q + (j >> 2), col = c0 + 4 * (j & 3);
   typedef __attribute__((address_space(3))) dw_s4 lds_s4;
   // generic -> LDS address-space conversion (the tile is a __shared__ array)
-  lds_s4* lo = (lds_s4*)(const_cast<uint16_t*>(tile) + row * 64 + col);
-  lds_s4* hi = (lds_s4*)(const_cast<uint16_t*>(tile) + (row + 4) * 64 + col);
+  lds_s4* lo = (lds_s4*)(const_cast<uint16_t*>(tile) + dw_swz(row, col));
+  lds_s4* hi = (lds_s4*)(const_cast<uint16_t*>(tile) + dw_swz(row + 4, col));
   const dw_s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(lo);
   const dw_s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(hi);
   typedef short s8 __attribute__((ext_vector_type(8)));
@@ -383,8 +416,9 @@ __device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, 
 template <bool DC>
 __global__ __launch_bounds__(256, 2) void k_dw_mfma(
     const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ dy, int C_in, int C_out,
-    int maxchunks, float* __restrict__ part) {
+    const int32_t* __restrict__ blk_base, int64_t nblk, const uint16_t* __restrict__ x,
+    const uint16_t* __restrict__ dy, int C_in, int C_out, int K, int nchunk,
+    float* __restrict__ part) {
   constexpr int STEP = 128;
   constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
   // staging tiles; the final wave reduction reuses the same bytes
@@ -392,18 +426,25 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
   __shared__ int2 s_pr[kChunk];                  // the chunk's pairs
   uint16_t* s_x = s_buf;
   uint16_t* s_g = s_buf + STEP * 64;
-  const int i = blockIdx.y, chunk = blockIdx.x;
+  DwChunk dc_;
+  if (!dw_chunk(blk_base, pair_off, nblk, K, nchunk, &dc_)) return;
+  const int i = dc_.i, chunk = dc_.c;
   const int ntn = (C_out + 63) / 64;
-  const int c0 = (blockIdx.z / ntn) * 64, n0 = (blockIdx.z % ntn) * 64;
+  const int c0 = (blockIdx.y / ntn) * 64, n0 = (blockIdx.y % ntn) * 64;
   const int64_t base = pair_off[i];
-  const int64_t k_i = pair_off[i + 1] - base;
-  const int64_t start = static_cast<int64_t>(chunk) * kChunk;
-  if (start >= k_i) return;
-  const int64_t end = start + kChunk < k_i ? start + kChunk : k_i;
+  const int64_t start = dc_.start, end = dc_.end;
   const int nsteps = static_cast<int>((end - start + STEP - 1) / STEP);
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int cx = C_in - c0 < 64 ? C_in - c0 : 64;     // valid columns of this tile
   const int cg = C_out - n0 < 64 ? C_out - n0 : 64;
+  float* out = part + (static_cast<int64_t>(i) * nchunk + chunk) * C_in * C_out;
+  if (nsteps == 0) {                                   // no pair of R_i in this chunk
+    for (int t = threadIdx.x; t < 64 * 64; t += 256) {
+      const int c = c0 + t / 64, n = n0 + t % 64;
+      if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = 0.0f;
+    }
+    return;
+  }
 
   // The chunk's pairs go to LDS once.  Then, over steps of STEP pairs: at
   // step t the data rows of step t + 2 are gathered into one of two register
@@ -439,8 +480,8 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
 #pragma unroll
     for (int pass = 0; pass < PASS; ++pass) {
       const int pp = pass * 32 + threadIdx.x / 8;
-      *reinterpret_cast<dw_u4*>(&s_x[pp * 64 + ch]) = (ok >> (2 * pass)) & 1u ? vx[pass] : z;
-      *reinterpret_cast<dw_u4*>(&s_g[pp * 64 + ch]) = (ok >> (2 * pass)) & 2u ? vg[pass] : z;
+      *reinterpret_cast<dw_u4*>(&s_x[dw_swz(pp, ch)]) = (ok >> (2 * pass)) & 1u ? vx[pass] : z;
+      *reinterpret_cast<dw_u4*>(&s_g[dw_swz(pp, ch)]) = (ok >> (2 * pass)) & 2u ? vg[pass] : z;
     }
   };
 
@@ -487,7 +528,6 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
   // wave partials -> LDS (one 16-row band of the tile at a time), summed in
   // wave order; lane (r, g) holds rows 4g + e, column r of each 16x16 block
   float (*s_red)[16][64 + 4] = reinterpret_cast<float (*)[16][64 + 4]>(s_buf);
-  float* out = part + (static_cast<int64_t>(i) * maxchunks + chunk) * C_in * C_out;
   const int r = lane % 16, g = lane / 16;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
@@ -509,18 +549,15 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
 // dw[i][c][n] = sum over the chunks of R_i: chunk ch goes to accumulator
 // ch mod 8, the 8 accumulators are added in order (a fixed order, so the
 // result is reproducible, with 8 loads in flight per lane).
-__global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ part,
-                                                   const int64_t* __restrict__ pair_off, int K,
-                                                   int C_in, int C_out, int maxchunks,
+__global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ part, int K,
+                                                   int C_in, int C_out, int nch,
                                                    float* __restrict__ dw) {
   const int64_t per = static_cast<int64_t>(C_in) * C_out;
   const int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
   if (idx >= K * per) return;
   const int i = static_cast<int>(idx / per);
   const int64_t rem = idx - i * per;
-  const int64_t k_i = pair_off[i + 1] - pair_off[i];
-  const int nch = static_cast<int>((k_i + kChunk - 1) / kChunk);
-  const float* p = part + static_cast<int64_t>(i) * maxchunks * per + rem;
+  const float* p = part + static_cast<int64_t>(i) * nch * per + rem;
   float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   int ch = 0;
   for (; ch + 8 <= nch; ch += 8) {
@@ -630,7 +667,10 @@ __global__ __launch_bounds__(256) void k_db_reduce(const float* __restrict__ par
   if (q == 0 && n < C_out) db[n] = s[0][cn];
 }
 
-int64_t dw_maxchunks(spconv_rulebook rb) { return (rb->n_cap + kChunk - 1) / kChunk; }
+int64_t dw_nchunk(spconv_rulebook rb) {
+  constexpr int64_t kBpc = kChunk / kBlock;
+  return (rb->nblk + kBpc - 1) / kBpc;
+}
 
 }  // namespace
 
@@ -817,43 +857,45 @@ FwdView transpose_view(spconv_rulebook rb) {
 size_t backward_weight_workspace(spconv_rulebook rb, int C_in, int C_out, int op) {
   const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_cap;
   const int64_t nrc = (rows + kRowChunk - 1) / kRowChunk;
-  return static_cast<size_t>(rb->K * dw_maxchunks(rb)) * C_in * C_out * 4 +
+  return static_cast<size_t>(rb->K * dw_nchunk(rb)) * C_in * C_out * 4 +
          static_cast<size_t>(nrc > 0 ? nrc : 1) * C_out * 4 + 256;  // nrc >= the chunk count
 }
 
 int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy, float* dw,
                     float* db, int C_in, int C_out, void* ws, hipStream_t st) {
-  const int maxchunks = static_cast<int>(dw_maxchunks(rb));
+  const int nchunk = static_cast<int>(dw_nchunk(rb));
+  const int K = static_cast<int>(rb->K);
   float* part = static_cast<float*>(ws);
   const int64_t per = static_cast<int64_t>(C_in) * C_out;
-  if (maxchunks > 0) {
+  if (nchunk > 0) {
     const int tiles = ((C_in + 63) / 64) * ((C_out + 63) / 64);
-    dim3 grid(static_cast<unsigned>(maxchunks), static_cast<unsigned>(rb->K),
-              static_cast<unsigned>(tiles));
+    // (offset, chunk) pairs: 8 XCDs x K offsets x ceil(nchunk / 8) chunks each
+    dim3 grid(static_cast<unsigned>(8 * K * ((nchunk + 7) / 8)), static_cast<unsigned>(tiles));
     const bool dc = op == SPCONV_OP_DC;
     // matrix cores for bf16 rows of whole 16-byte chunks (C % 8 == 0 keeps
     // every gathered 16-byte load inside its row)
     if (dt == SPCONV_BF16 && C_in % 8 == 0 && C_out % 8 == 0) {
       auto kern = dc ? k_dw_mfma<true> : k_dw_mfma<false>;
-      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<const uint16_t*>(x),
-                                 static_cast<const uint16_t*>(dy), C_in, C_out, maxchunks, part);
+      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, rb->blk_cnt, rb->nblk,
+                                 static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(dy),
+                                 C_in, C_out, K, nchunk, part);
     } else if (dt == SPCONV_F32) {
       auto kern = dc ? k_dw_partial<float, true> : k_dw_partial<float, false>;
-      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<const float*>(x),
-                                 static_cast<const float*>(dy), C_in, C_out, maxchunks, part);
+      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, rb->blk_cnt, rb->nblk,
+                                 static_cast<const float*>(x), static_cast<const float*>(dy), C_in,
+                                 C_out, K, nchunk, part);
     } else {
       auto kern = dc ? k_dw_partial<uint16_t, true> : k_dw_partial<uint16_t, false>;
-      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<const uint16_t*>(x),
-                                 static_cast<const uint16_t*>(dy), C_in, C_out, maxchunks, part);
+      kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, rb->blk_cnt, rb->nblk,
+                                 static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(dy),
+                                 C_in, C_out, K, nchunk, part);
     }
   }
-  k_dw_reduce<<<grid_of(rb->K * per, 1ll << 30), 256, 0, st>>>(part, rb->pair_off,
-                                                               static_cast<int>(rb->K), C_in,
-                                                               C_out, maxchunks, dw);
+  k_dw_reduce<<<grid_of(rb->K * per, 1ll << 30), 256, 0, st>>>(part, K, C_in, C_out, nchunk, dw);
   if (db) {
     const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_out;
     const int nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
-    float* partb = part + static_cast<int64_t>(rb->K) * maxchunks * per;
+    float* partb = part + static_cast<int64_t>(rb->K) * nchunk * per;
     if (nrc > 0) {
       const int vec = dt == SPCONV_F32 ? 4 : 8;
       const int groups = (C_out + vec - 1) / vec;

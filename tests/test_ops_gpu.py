@@ -5,7 +5,7 @@
   bound of the forward tests: per element |g - o| <= rtol * S and normwise
   ||g - o|| <= rtol ||o||, with rtol 1e-5 (fp32) / 2e-2 (bf16 in or out).
 * Weight and bias gradients sum up to k_i products per entry in fp32, in
-  chunks of 4096 pairs whose partial sums are then added in order; their
+  chunks of at most 4096 pairs whose partial sums are then added in order; their
   tolerance is RTOL_GRAD = 1e-4, ~25x the typical sqrt(n) * 2^-24 error of a
   4096-term fp32 sum (the worst case n * 2^-24 is 2.4e-4).
 """
