@@ -320,3 +320,30 @@ def test_fused_forward_in_place_residual_and_overlap_errors():
     st = lib.spconv_forward_fused(rb.handle, spc.BF16, xd.data_ptr(), wd.data_ptr(), None, None,
                                   None, 2, spc.BF16, ptr, C_in, C_out, None)
     assert st == spc._lib.EINVAL                       # relu not 0 / 1
+
+
+def test_empty_and_single_site_books():
+    """No sites: every op returns empty (or zero) results without launching
+    anything out of range.  One site: only the centre offset has a pair, so
+    the weight gradient is x^T dy at the centre and zero elsewhere."""
+    size = [1, 16, 16]
+    none = np.zeros((0, 3), np.int32)
+    vsc = spc.build_rulebook(spc.VSC, _t(none), size, [1, 3, 3])
+    sc = spc.build_rulebook(spc.SC, _t(none), size, [1, 2, 2], [1, 2, 2], transpose=True)
+    w = torch.zeros((9, 16, 32), device="cuda")
+    x0 = torch.zeros((0, 16), device="cuda")
+    assert spc.forward_fused(vsc, x0, w, relu=True).shape == (0, 32)
+    assert spc.backward_data(vsc, spc.OP_VSC, torch.zeros((0, 32), device="cuda"), w).shape == (0, 16)
+    dw, db = spc.backward_weight(vsc, spc.OP_VSC, x0, torch.zeros((0, 32), device="cuda"), 16, 32)
+    assert dw.shape == (9, 16, 32) and not dw.any() and not db.any()
+    assert spc.dc_forward(sc, x0, torch.zeros((4, 16, 32), device="cuda")).shape == (0, 32)
+
+    one = np.array([[0, 7, 9]], np.int32)
+    rb = spc.build_rulebook(spc.VSC, _t(one), size, [1, 3, 3])
+    x = inputs.normal_f32((1, 16), seed=71)
+    dy = inputs.normal_f32((1, 32), seed=72)
+    dw, db = spc.backward_weight(rb, spc.OP_VSC, _t(x), _t(dy), 16, 32)
+    dw = dw.cpu().numpy()
+    np.testing.assert_allclose(dw[4], np.outer(x[0], dy[0]), rtol=1e-6, atol=0)
+    assert not np.delete(dw, 4, axis=0).any()
+    np.testing.assert_array_equal(db.cpu().numpy(), dy[0])
