@@ -271,12 +271,18 @@ __global__ __launch_bounds__(256, 2) void k_fwd_mfma(
   __shared__ __attribute__((aligned(16))) unsigned char s_w[2][COLS * LDWB];
 
   // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
-  // contiguous range of tiles so neighbouring tiles share that XCD's L2.
-  const int64_t per = gridDim.x / 8;
-  const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
+  // contiguous range of tiles so neighbouring tiles share that XCD's L2.  The
+  // grid is sized for a bound on the rows (an SC output count is known only
+  // on the device), so the ranges split the device-side tile count, not the
+  // grid: otherwise a loose bound would leave whole XCDs without work.
   const int64_t n_rows = hdr->n_out;
-  // tiles past the device-side row count (the grid is sized for a bound)
-  if (tile >= ntiles || tile * TILE_ROWS >= n_rows) return;
+  const int64_t nt_real = (n_rows + TILE_ROWS - 1) / TILE_ROWS;
+  const int64_t nt = nt_real < ntiles ? nt_real : ntiles;
+  const int64_t per = (nt + 7) / 8;
+  const int64_t q = blockIdx.x / 8;
+  if (q >= per) return;
+  const int64_t tile = static_cast<int64_t>(blockIdx.x % 8) * per + q;
+  if (tile >= nt) return;
   static_assert(kSegRows % TILE_ROWS == 0, "tiles inside one segment chunk");
   const int wseg = seg ? seg[tile * TILE_ROWS / kSegRows] : -1;
 

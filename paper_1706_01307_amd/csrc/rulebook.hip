@@ -122,13 +122,30 @@ __device__ void publish_counts(const uint8_t (*s_cnt)[kBlock / kWave], int K,
   }
 }
 
-// XCD-aware block order for kernels whose neighbouring blocks share data:
-// workgroup b runs on XCD b % 8, so XCD x gets the contiguous block range
-// [x * per, (x + 1) * per) and its L2 holds that stretch of the schedule's
-// neighbourhood.  The grid must be launched with 8 * per workgroups.
-__device__ __forceinline__ int64_t xcd_block() {
-  const int64_t per = gridDim.x / 8;
-  return static_cast<int64_t>(blockIdx.x % 8) * per + blockIdx.x / 8;
+// XCD-aware block order for the probes, whose neighbouring blocks share
+// data: workgroup b runs on XCD b % 8, so the blocks that hold output
+// positions (the first ceil(n_out / kBlock); an SC output count is known only
+// on the device, the launch is sized for a bound) are dealt to the XCDs in
+// contiguous ranges, x getting [x * per, (x + 1) * per), and its L2 holds
+// that stretch of the schedule's neighbourhood.  The remaining blocks of the
+// bound, which only write zeros, follow in order.  The grid must have
+// probe_grid_size(nblk) workgroups; returns -1 for a workgroup without a block.
+__device__ __forceinline__ int64_t probe_block(int64_t n_rows, int64_t nblk) {
+  int64_t nreal = (n_rows + kBlock - 1) / kBlock;
+  if (nreal > nblk) nreal = nblk;
+  const int64_t per = (nreal + 7) / 8;
+  const int64_t L = blockIdx.x;
+  if (L < 8 * per) {
+    const int64_t b = (L % 8) * per + L / 8;
+    return b < nreal ? b : -1;
+  }
+  const int64_t b = nreal + (L - 8 * per);
+  return b < nblk ? b : -1;
+}
+// 8 ceil(nblk / 8) + 8 >= nblk + 8: the tail covers the blocks past the real
+// ones even when the first 8 per slots round up by 7.
+inline unsigned probe_grid_size(int64_t nblk) {
+  return static_cast<unsigned>(8 * ((nblk + 7) / 8) + 8);
 }
 
 __device__ __forceinline__ uint32_t wave_prefix(uint32_t packed, int wave) {
@@ -234,8 +251,8 @@ __global__ __launch_bounds__(kBlock) void k_probe(
     const DeviceHeader* __restrict__ hdr, int64_t gstride, Codec crow, Codec cin, Table t,
     OffsetTable ot, int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt,
     uint32_t* __restrict__ wpre, int64_t nblk) {
-  const int64_t blk = xcd_block();
-  if (blk >= nblk) return;
+  const int64_t blk = probe_block(hdr->n_out, nblk);
+  if (blk < 0) return;
   __shared__ int16_t s_off[kMaxK][kMaxD];
   __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
   fill_offsets(ot, s_off);
@@ -659,8 +676,8 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
     const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g, OffsetTable ot,
     const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
     int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
-  const int64_t blk = xcd_block();
-  if (blk >= nblk) return;
+  const int64_t blk = probe_block(hdr->n_out, nblk);
+  if (blk < 0) return;
   __shared__ int16_t s_off[kMaxK][kMaxD];
   __shared__ uint32_t s_dil[kMaxK][kMaxD];
   __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
@@ -892,7 +909,7 @@ void launch_scan_compact(spconv_rulebook rb) {
 void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
                                const Codec& cin, const Transient& tr) {
   const OffsetTable ot = make_offsets(rb);
-  const unsigned g = static_cast<unsigned>(8 * ((rb->nblk + 7) / 8));
+  const unsigned g = probe_grid_size(rb->nblk);
   auto launch = [&](auto kern) {
     kern<<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->perm, rb->hdr, rb->gstride, crow, cin,
                                        tr.table, ot, rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
@@ -1011,7 +1028,7 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
                        const GridBufs& b, uint64_t cells) {
   const OffsetTable ot = make_offsets(rb);
   auto launch = [&](auto kern) {
-    kern<<<static_cast<unsigned>(8 * ((rb->nblk + 7) / 8)), kBlock, 0, rb->stream>>>(
+    kern<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
         rows_sites, rb->perm, rb->hdr, rb->gstride, g, ot, b.grid, static_cast<uint32_t>(cells),
         rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
