@@ -10,6 +10,8 @@ Prints one JSON line:
   value      active sites per second over whole steps (build + forward)
   roofline   the forward kernel (the dominant one) against the bf16 dense
              matrix-core peak, from HIP events around each forward launch
+  phases     rule book and forward per step: means, 10/50/90th percentiles,
+             and medians of a few extra steps run after evicting the caches
   cpu_baseline  the oracle on one sample of the same workload, host cores
 
 Other modes (not the benchmark line): --workload with a multi-layer stack
@@ -53,6 +55,8 @@ def _args():
                    help="run one plain device copy of this many MiB (counter calibration)")
     p.add_argument("--peaks", action="store_true",
                    help="measure a device copy and a bf16 library GEMM instead")
+    p.add_argument("--cold-steps", type=int, default=10,
+                   help="extra steps after a cache-evicting write each (reported apart)")
     p.add_argument("--ops", action="store_true",
                    help="time pooling, DC and the gradients instead")
     return p.parse_args()
@@ -192,9 +196,25 @@ def main():
         step(evs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    rb_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    fwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    rb_t = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    fwd_t = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    rb_ms, fwd_ms = float(rb_t.mean()), float(fwd_t.mean())
     ms_per_step = (t1 - t0) * 1e3 / a.steps
+
+    def pct(v):
+        return [float(x) for x in np.percentile(v, [10, 50, 90])]
+
+    # cold caches (outside the timed region): before each of a few steps a
+    # 1 GiB write evicts L2 and the 256 MB Infinity Cache
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    cold = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.cold_steps)]
+    for i in range(a.cold_steps):
+        flush.fill_(float(i))
+        step(cold[i])
+    torch.cuda.synchronize()
+    del flush
+    cold_rb = np.array([e[0].elapsed_time(e[1]) for e in cold])
+    cold_fwd = np.array([e[1].elapsed_time(e[2]) for e in cold])
 
     # a last asynchronous build, checked for device-side errors
     _lib.check(lib.spconv_build_rulebook(*args_build), "build")
@@ -232,6 +252,12 @@ def main():
         "effective_tflops": tflops,
         "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
         "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
+        "phases_ms_p10_p50_p90": {"rulebook": pct(rb_t), "forward": pct(fwd_t),
+                                  "build_and_forward": pct(rb_t + fwd_t)},
+        "cold_caches_ms_median": ({"steps": a.cold_steps,
+                                   "rulebook": float(np.median(cold_rb)),
+                                   "forward": float(np.median(cold_fwd))}
+                                  if a.cold_steps > 0 else None),
         "roofline": {"bound": "mfma", "kernel": kernel, "achieved": tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": tflops / peak, "traffic": traffic,
                      "algorithmic_bytes": fwd_bytes},
