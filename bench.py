@@ -231,6 +231,11 @@ def main():
     esz = 2 if bf16 else 4
     fwd_bytes = N * Cin * esz + N * Cout * esz + 4 * K * N + K * Cin * Cout * esz + 4 * Cout
 
+    # rule-book outputs the build must write: gather map (4 K N), pairs
+    # (8 per pair), schedule (4 N), per-offset offsets; plus the coordinates
+    # it reads (4 D N)
+    rb_bytes = 4 * K * N + 8 * sum_k + 4 * N + 8 * (K + 1) + 4 * D * N
+
     headline = a.workload == "surf128x8_vsc3_c64_bf16"
     out = {
         "metric": ("VSC layer active sites/sec + effective TFLOP/s (3^3, C=64, 128^3 surfaces)"
@@ -252,6 +257,8 @@ def main():
         "effective_tflops": tflops,
         "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
         "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
+        "rulebook_io": {"algorithmic_bytes": rb_bytes,
+                        "GBps": rb_bytes / (rb_ms * 1e-3) / 1e9, "peak_GBps": PEAKS["hbm"]},
         "phases_ms_p10_p50_p90": {"rulebook": pct(rb_t), "forward": pct(fwd_t),
                                   "build_and_forward": pct(rb_t + fwd_t)},
         "cold_caches_ms_median": ({"steps": a.cold_steps,

@@ -245,6 +245,21 @@ int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, co
                            float* dw, float* db, int C_in, int C_out, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* Device memory of the rule books.  Every allocation the library makes (a
+ * rule book's persistent block and the transient buffers of a build) comes
+ * from alloc(bytes, stream, ctx) and goes back through
+ * release(ptr, stream, ctx), both on the build stream and stream-ordered
+ * there (a caching allocator may hand the memory to later work on that
+ * stream).  A rule book keeps the pair it was built with, so a change applies
+ * to later builds only.  Both NULL (the default): hipMallocAsync /
+ * hipFreeAsync.  An alloc that returns NULL makes the build return ENOMEM
+ * after releasing everything it had taken.  Ownership: the library calls
+ * release exactly once for every non-NULL pointer alloc returned.  Errors:
+ * EINVAL when only one of the two functions is given.  Set it while no build
+ * is running on another thread. */
+int spconv_set_allocator(void* (*alloc)(size_t bytes, void* stream, void* ctx),
+                         void (*release)(void* ptr, void* stream, void* ctx), void* ctx);
+
 /* Release a rule book (stream-ordered on its build stream).  NULL is a
  * no-op. */
 void spconv_rulebook_destroy(spconv_rulebook rb);

@@ -22,7 +22,8 @@ from ._lib import (BF16, BUILD_ASYNC, BUILD_TRANSPOSE, EDUP, EINVAL, ENOMEM, ERA
 
 __all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "BUILD_TRANSPOSE", "OP_VSC", "OP_SC",
            "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "vsc_forward",
-           "sc_forward", "forward_fused", "dc_forward", "pool_forward", "backward_data", "backward_weight",
+           "sc_forward", "forward_fused", "dc_forward", "pool_forward", "backward_data",
+           "backward_weight", "set_allocator", "use_torch_allocator",
            "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE", "ENOMEM", "ECAP", "EHIP"]
 
 
@@ -125,6 +126,51 @@ class Rulebook:
             self.close()
         except Exception:
             pass
+
+
+# ctypes callbacks of every allocator ever registered: a rule book built with
+# one calls its release when destroyed, possibly after a later change.
+_ALLOCATORS = []
+
+
+def set_allocator(alloc=None, release=None):
+    """Device memory of later rule-book builds from Python callables:
+    alloc(nbytes, stream_handle) -> device address (0 = out of memory) and
+    release(address, stream_handle).  Both None: back to hipMallocAsync."""
+    if (alloc is None) != (release is None):
+        raise ValueError("give both alloc and release, or neither")
+    lib = _lib.load()
+    if alloc is None:
+        _lib.check(lib.spconv_set_allocator(_lib.ALLOC_FN(), _lib.RELEASE_FN(), None),
+                   "spconv_set_allocator")
+        return
+
+    def _alloc(nbytes, stream, ctx):
+        return int(alloc(int(nbytes), int(stream or 0)) or 0)
+
+    def _release(ptr, stream, ctx):
+        release(int(ptr), int(stream or 0))
+
+    pair = (_lib.ALLOC_FN(_alloc), _lib.RELEASE_FN(_release))
+    _ALLOCATORS.append(pair)
+    _lib.check(lib.spconv_set_allocator(pair[0], pair[1], None), "spconv_set_allocator")
+
+
+def use_torch_allocator():
+    """Rule-book memory from torch's caching allocator (stream-ordered on the
+    build stream, like the default)."""
+    torch = _torch()
+
+    def alloc(nbytes, stream):
+        try:
+            return torch.cuda.caching_allocator_alloc(nbytes, torch.cuda.current_device(), stream)
+        except RuntimeError:
+            return 0
+
+    def release(ptr, stream):
+        torch.cuda.caching_allocator_delete(ptr)
+
+    set_allocator(alloc, release)
 
 
 def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, transpose=False,

@@ -22,7 +22,11 @@ BUILD_ASYNC, BUILD_TRANSPOSE = 1, 2
 
 # Every symbol the header declares, with its ctypes signature.
 _P, _I, _I64, _U = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
+RELEASE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
+
 SIGNATURES = {
+    "spconv_set_allocator": (_I, [ALLOC_FN, RELEASE_FN, _P]),
     "spconv_build_rulebook": (_I, [_I, _I, _P, _I64, _P, _P, _P, _U, _P, ctypes.POINTER(_P)]),
     "spconv_rulebook_status": (_I, [_P]),
     "spconv_rulebook_query": (_I, [_P, _P, _P, _P, _P, _P]),

@@ -70,16 +70,52 @@ int sync_rulebook(spconv_rulebook rb) {
   return rb->status;
 }
 
+std::mutex g_alloc_mu;
+Allocator g_alloc;                 // the allocator new builds take
+
 void release(spconv_rulebook rb) {
   if (!rb) return;
-  if (rb->mem) (void)hipFreeAsync(rb->mem, rb->stream);
+  if (rb->mem) (void)dev_free(rb, rb->mem, rb->stream);
   (void)hipGetLastError();
   delete rb;
 }
 
 }  // namespace
 
+int spc::dev_alloc(spconv_rulebook rb, size_t bytes, hipStream_t st, void** p) {
+  *p = nullptr;
+  if (rb->al.alloc) {
+    *p = rb->al.alloc(bytes, st, rb->al.ctx);
+    return *p ? SPCONV_OK : SPCONV_ENOMEM;
+  }
+  if (hipMallocAsync(p, bytes, st) != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return SPCONV_ENOMEM;
+  }
+  return SPCONV_OK;
+}
+
+int spc::dev_free(spconv_rulebook rb, void* p, hipStream_t st) {
+  if (!p) return SPCONV_OK;
+  if (rb->al.release) {
+    rb->al.release(p, st, rb->al.ctx);
+    return SPCONV_OK;
+  }
+  return hipFreeAsync(p, st) == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
 extern "C" {
+
+int spconv_set_allocator(void* (*alloc)(size_t, void*, void*),
+                         void (*release_fn)(void*, void*, void*), void* ctx) {
+  if ((alloc == nullptr) != (release_fn == nullptr)) return SPCONV_EINVAL;
+  std::lock_guard<std::mutex> lk(g_alloc_mu);
+  g_alloc.alloc = alloc;
+  g_alloc.release = release_fn;
+  g_alloc.ctx = alloc ? ctx : nullptr;
+  return SPCONV_OK;
+}
 
 const char* spconv_status_string(int s) {
   switch (s) {
@@ -124,6 +160,10 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   rb->n_in = N;
   rb->K = K;
   rb->stream = static_cast<hipStream_t>(stream);
+  {
+    std::lock_guard<std::mutex> lk(g_alloc_mu);
+    rb->al = g_alloc;
+  }
   (void)hipGetDevice(&rb->device);
   keep_pool_memory(rb->device);
   uint64_t cells = 1, fan = 1;
@@ -172,8 +212,7 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   bytes += align_up(n_cap * 4, 256);
   const size_t tbytes = transpose ? transpose_bytes(N, K) : 0;
   bytes += tbytes;
-  if (hipMallocAsync(&rb->mem, bytes, rb->stream) != hipSuccess) {
-    (void)hipGetLastError();
+  if (dev_alloc(rb, bytes, rb->stream, &rb->mem) != SPCONV_OK) {
     delete rb;
     return SPCONV_ENOMEM;
   }

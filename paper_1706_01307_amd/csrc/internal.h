@@ -146,6 +146,17 @@ struct DeviceHeader {          // first bytes of the rule book's allocation
 
 }  // namespace spc
 
+namespace spc {
+// Where a rule book's device memory comes from: a registered allocator
+// (spconv_set_allocator) or, with both functions NULL, hipMallocAsync /
+// hipFreeAsync.  Each rule book keeps the one it was built with.
+struct Allocator {
+  void* (*alloc)(size_t, void*, void*) = nullptr;
+  void (*release)(void*, void*, void*) = nullptr;
+  void* ctx = nullptr;
+};
+}  // namespace spc
+
 struct spconv_rulebook_s {
   int kind;
   int D;
@@ -155,6 +166,7 @@ struct spconv_rulebook_s {
   int64_t K;
   int32_t size[spc::kMaxD], f[spc::kMaxD], s[spc::kMaxD], out_size[spc::kMaxD];
   hipStream_t stream;          // build stream (owns the allocation)
+  spc::Allocator al;           // the allocator of this build (and its release)
   void* mem;                   // one stream-ordered allocation
   size_t mem_bytes;
   // carved device pointers
@@ -193,6 +205,11 @@ struct spconv_rulebook_s {
 };
 
 namespace spc {
+
+// Stream-ordered device memory through the rule book's allocator.
+// dev_alloc: SPCONV_OK or SPCONV_ENOMEM; dev_free: SPCONV_OK or SPCONV_EHIP.
+int dev_alloc(spconv_rulebook rb, size_t bytes, hipStream_t st, void** p);
+int dev_free(spconv_rulebook rb, void* p, hipStream_t st);
 
 // Launchers (rulebook.hip).  All asynchronous on rb->stream.
 int build_vsc(spconv_rulebook rb, const int32_t* coords);

@@ -740,10 +740,7 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
   const size_t tbytes = 2 * al(static_cast<size_t>(n) * 8) + 3 * al(static_cast<size_t>(n) * 4) +
                         al(scratch);
   void* tmem = nullptr;
-  if (hipMallocAsync(&tmem, tbytes, st) != hipSuccess) {
-    (void)hipGetLastError();
-    return SPCONV_ENOMEM;
-  }
+  if (dev_alloc(rb, tbytes, st, &tmem) != SPCONV_OK) return SPCONV_ENOMEM;
   char* p = static_cast<char*>(tmem);
   uint64_t* keys = reinterpret_cast<uint64_t*>(p);
   uint64_t* keys_tmp = reinterpret_cast<uint64_t*>(p + al(n * 8));
@@ -759,7 +756,7 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
     if (hipMemcpyAsync(rb->t_perm, flipped ? vals_tmp : vals, static_cast<size_t>(n) * 4,
                        hipMemcpyDeviceToDevice, st) != hipSuccess) {
       (void)hipGetLastError();
-      (void)hipFreeAsync(tmem, st);
+      (void)dev_free(rb, tmem, st);
       return SPCONV_EHIP;
     }
   } else {
@@ -781,7 +778,7 @@ int build_transpose(spconv_rulebook rb, const int32_t* coords, char* mem) {
     k_seg_scatter<<<grid_of(n), 256, 0, st>>>(rb->pairs, rb->pair_off, static_cast<int>(rb->K),
                                               rb->t_chunk_off, rb->t_src, rb->t_dst);
   }
-  if (hipFreeAsync(tmem, st) != hipSuccess) return SPCONV_EHIP;
+  if (dev_free(rb, tmem, st) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 

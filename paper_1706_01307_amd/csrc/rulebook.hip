@@ -814,10 +814,7 @@ int alloc_transient(spconv_rulebook rb, int64_t N, const Codec& cin, size_t extr
   tr->wide = cin.kbits + rbits > 64;
   size_t bytes = align_up(N * sizeof(uint64_t), 256) + align_up(slots * 8, 256) +
                  (tr->wide ? align_up(slots * 4, 256) : 0) + extra_bytes + 256;
-  if (hipMallocAsync(&tr->mem, bytes, rb->stream) != hipSuccess) {
-    (void)hipGetLastError();
-    return SPCONV_ENOMEM;
-  }
+  if (dev_alloc(rb, bytes, rb->stream, &tr->mem) != SPCONV_OK) return SPCONV_ENOMEM;
   cv->base = static_cast<char*>(tr->mem);
   tr->keys = cv->take<uint64_t>(N);
   tr->table.slots = cv->take<uint64_t>(slots);
@@ -931,7 +928,7 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
 }
 
 int finish(spconv_rulebook rb, Transient& tr) {
-  if (hipFreeAsync(tr.mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  if (dev_free(rb, tr.mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
@@ -1048,17 +1045,14 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
                    uint64_t cells) {
   const int64_t N = rb->n_in;
   void* mem = nullptr;
-  if (hipMallocAsync(&mem, grid_bytes(cells) + 256, rb->stream) != hipSuccess) {
-    (void)hipGetLastError();
-    return SPCONV_ENOMEM;
-  }
+  if (dev_alloc(rb, grid_bytes(cells) + 256, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
   const GridBufs b = take_grid(&cv, cells);
   launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr,
                       false, N);
   launch_grid_schedule(rb, b, cells, N);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
-  if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
@@ -1079,10 +1073,7 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
                        align_up(static_cast<size_t>(lnbw) * 4, 256) +
                        align_up(static_cast<size_t>(N) * 8, 256) + 256;
   void* mem = nullptr;
-  if (hipMallocAsync(&mem, bytes, rb->stream) != hipSuccess) {
-    (void)hipGetLastError();
-    return SPCONV_ENOMEM;
-  }
+  if (dev_alloc(rb, bytes, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
   const GridBufs bi = take_grid(&cv, cells_in);
   const GridBufs bo = take_grid(&cv, cells_out);
@@ -1103,7 +1094,7 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
                       cout, nullptr, false);
   launch_grid_schedule(rb, bo, cells_out, -1);
   launch_probe_grid(rb, rb->out_coords, gi, bi, cells_in);
-  if (hipFreeAsync(mem, rb->stream) != hipSuccess) return SPCONV_EHIP;
+  if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 }  // namespace

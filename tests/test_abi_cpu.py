@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -105,3 +105,12 @@ def test_new_entry_points_reject_bad_arguments_on_the_host():
                                        f.ctypes.data, s.ctypes.data, flags, None,
                                        ctypes.byref(h))
         assert st == E and h.value is None
+
+
+def test_set_allocator_needs_both_functions():
+    lib = _lib.load()
+    alloc = _lib.ALLOC_FN(lambda n, s, c: 0)
+    release = _lib.RELEASE_FN(lambda p, s, c: None)
+    assert lib.spconv_set_allocator(alloc, _lib.RELEASE_FN(), None) == _lib.EINVAL
+    assert lib.spconv_set_allocator(_lib.ALLOC_FN(), release, None) == _lib.EINVAL
+    assert lib.spconv_set_allocator(_lib.ALLOC_FN(), _lib.RELEASE_FN(), None) == _lib.OK

@@ -347,3 +347,70 @@ def test_empty_and_single_site_books():
     np.testing.assert_allclose(dw[4], np.outer(x[0], dy[0]), rtol=1e-6, atol=0)
     assert not np.delete(dw, 4, axis=0).any()
     np.testing.assert_array_equal(db.cpu().numpy(), dy[0])
+
+
+# ---------------------------------------------------------------------------
+# Allocator hook
+# ---------------------------------------------------------------------------
+
+class _CountingTorchAllocator:
+    """torch's caching allocator behind spconv_set_allocator, counting calls;
+    fail_at = k makes the k-th allocation return NULL."""
+
+    def __init__(self, fail_at=None):
+        self.fail_at, self.calls, self.live = fail_at, 0, {}
+
+    def alloc(self, nbytes, stream):
+        self.calls += 1
+        if self.fail_at == self.calls:
+            return 0
+        p = torch.cuda.caching_allocator_alloc(nbytes, torch.cuda.current_device(), stream)
+        self.live[p] = nbytes
+        return p
+
+    def release(self, ptr, stream):
+        assert ptr in self.live, "release of a pointer alloc never returned"
+        del self.live[ptr]
+        torch.cuda.caching_allocator_delete(ptr)
+
+
+def test_allocator_hook_results_and_balance():
+    coords, size = _sites("surf")
+    x = _feats(len(coords), 32, "bf16", 81)
+    w = inputs.to_bf16_bits(inputs.normal_f32((8, 32, 64), std=0.1, seed=82))
+    ref_sc = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2, 2], [1, 2, 2, 2],
+                                transpose=True)
+    y_ref = spc.sc_forward(ref_sc, _dev(x, "bf16"), _dev(w, "bf16"))
+    dx_ref = spc.backward_data(ref_sc, spc.OP_SC, y_ref, _dev(w, "bf16"))
+    ref_sc.close()
+    al = _CountingTorchAllocator()
+    spc.set_allocator(al.alloc, al.release)
+    try:
+        rb = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2, 2], [1, 2, 2, 2],
+                                transpose=True)
+        assert al.calls == 3 and len(al.live) == 1     # rule book; grids and sort buffers freed
+        y = spc.sc_forward(rb, _dev(x, "bf16"), _dev(w, "bf16"))
+        dx = spc.backward_data(rb, spc.OP_SC, y, _dev(w, "bf16"))
+        assert torch.equal(y, y_ref) and torch.equal(dx, dx_ref)
+        rb.close()
+        torch.cuda.synchronize()
+        assert not al.live
+    finally:
+        spc.set_allocator(None, None)
+
+
+@pytest.mark.parametrize("fail_at", [1, 2, 3])
+def test_allocator_failure_is_enomem_without_leaks(fail_at):
+    coords, size = _sites("pen")
+    al = _CountingTorchAllocator(fail_at)
+    spc.set_allocator(al.alloc, al.release)
+    try:
+        with pytest.raises(spc.SpconvError) as e:
+            spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2], [1, 2, 2], transpose=True)
+        assert e.value.status == spc.ENOMEM
+        torch.cuda.synchronize()
+        assert not al.live
+    finally:
+        spc.set_allocator(None, None)
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2], [1, 2, 2], transpose=True)
+    assert rb.n_out > 0                                   # the default is back
