@@ -62,6 +62,12 @@ def _args():
     return p.parse_args()
 
 
+def knobs():
+    """The library's environment switches as set for this run (None = default)."""
+    return {k: os.environ.get(k) for k in ("SPCONV_RULEBOOK", "SPCONV_FORCE_PATH",
+                                           "SPCONV_HASH_LAYOUT", "SPCONV_TEST_HASH_SLOTS")}
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("forward.hip", "forward_kernels.h", "forward_w0.hip", "internal.h"):
@@ -254,6 +260,7 @@ def main():
         "config": {"workload": a.workload, "variant": a.variant, "batch": wl.batch,
                    "grid": wl.size, "active_sites": N, "sum_k": sum_k, "K": K,
                    "c_in": Cin, "c_out": Cout, "out_dtype": dt},
+        "knobs": knobs(),
         "effective_tflops": tflops,
         "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
         "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
@@ -404,6 +411,7 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "variant": a.variant, "batch": wl.batch,
                    "grid": wl.size, "active_sites": N0, "layers": info},
+        "knobs": knobs(),
         "effective_tflops": flops / (ms * 1e-3) / 1e12,
         "bytes_features": int(sum(r["n_in"] * r["c_in"] * esz + r["n_out"] * r["c_out"] * esz
                                   for r in info))}), flush=True)
