@@ -110,6 +110,28 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
                           const int32_t* s, unsigned flags, void* stream,
                           spconv_rulebook* out);
 
+/* Build the rule book of the next layer on the output sites of an SC rule
+ * book (Section 5's networks stack VSC and SC layers level by level): the
+ * sites are parent's output coordinates in parent's row order, the grid is
+ * parent's output grid, and the site count stays on the device, so with
+ * SPCONV_BUILD_ASYNC a whole chain of levels is built without the host
+ * waiting once.  kind, f, s, flags and stream as spconv_build_rulebook
+ * (SPCONV_BUILD_TRANSPOSE not accepted here).  Until the book is
+ * synchronised its input row count is a bound (spconv_rulebook_bounds); the
+ * forward reads the real counts on the device.  parent must outlive the
+ * enqueued build (destroying it later on the same stream is enough).  Grids
+ * too large for the dense-grid path make this call wait for parent's count
+ * and build as spconv_build_rulebook does.  Errors: EINVAL (parent not SC,
+ * TRANSPOSE, as spconv_build_rulebook), and the build's own. */
+int spconv_build_rulebook_on(spconv_rulebook parent, int kind, const int32_t* f,
+                             const int32_t* s, unsigned flags, void* stream,
+                             spconv_rulebook* out);
+
+/* Host-side bounds, known without waiting for the device: input rows and
+ * output rows the book's buffers are sized for (for allocating layer outputs
+ * ahead of an asynchronous build).  Errors: EINVAL (NULL). */
+int spconv_rulebook_bounds(spconv_rulebook rb, int64_t* n_in_bound, int64_t* n_out_bound);
+
 /* Wait for the build and return its device-detected status (OK, EDUP,
  * ERANGE or ECAP).  Needed only after an SPCONV_BUILD_ASYNC build. */
 int spconv_rulebook_status(spconv_rulebook rb);

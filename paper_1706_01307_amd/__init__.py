@@ -21,7 +21,8 @@ from ._lib import (BF16, BUILD_ASYNC, BUILD_TRANSPOSE, EDUP, EINVAL, ENOMEM, ERA
                    SpconvError)
 
 __all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "BUILD_TRANSPOSE", "OP_VSC", "OP_SC",
-           "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "vsc_forward",
+           "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "build_rulebook_on",
+           "vsc_forward",
            "sc_forward", "forward_fused", "dc_forward", "pool_forward", "backward_data",
            "backward_weight", "set_allocator", "use_torch_allocator",
            "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE", "ENOMEM", "ECAP", "EHIP"]
@@ -84,6 +85,13 @@ class Rulebook:
 
     def status(self):
         return _lib.load().spconv_rulebook_status(self._h)
+
+    def bounds(self):
+        """(input rows, output rows) the buffers are sized for, without waiting."""
+        a, b = ctypes.c_int64(), ctypes.c_int64()
+        _lib.check(_lib.load().spconv_rulebook_bounds(self._h, ctypes.byref(a), ctypes.byref(b)),
+                   "spconv_rulebook_bounds")
+        return a.value, b.value
 
     @property
     def n_in(self):
@@ -203,6 +211,26 @@ def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, transpos
                                    ctypes.byref(h))
     _lib.check(st, "spconv_build_rulebook")
     return Rulebook(h, kind, D, st_ptr)
+
+
+def build_rulebook_on(parent, kind, f, s=None, *, sync=True, stream=None):
+    """Rule book of the next layer on the output sites of the SC rule book
+    `parent` (its coordinates, grid and device-side count); with sync=False
+    nothing waits for the device (see Rulebook.bounds for sizing outputs)."""
+    lib = _lib.load()
+    if parent.kind != SC:
+        raise ValueError("the parent must be an SC rule book")
+    D = parent.D
+    fa = _i32_array(f, D, "f")
+    sa = _i32_array(np.ones(D) if s is None else s, D, "s")
+    h = ctypes.c_void_p()
+    st_ptr = _stream_ptr(stream)
+    _lib.check(lib.spconv_build_rulebook_on(parent.handle, kind, fa.ctypes.data, sa.ctypes.data,
+                                            0 if sync else BUILD_ASYNC, st_ptr, ctypes.byref(h)),
+               "spconv_build_rulebook_on")
+    rb = Rulebook(h, kind, D, st_ptr)
+    rb._parent = parent            # its sites are read by the enqueued build
+    return rb
 
 
 def _forward(fn, kind, rb, x, w, bias, out_dtype, out, stream):

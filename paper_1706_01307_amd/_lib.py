@@ -28,6 +28,8 @@ RELEASE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_v
 SIGNATURES = {
     "spconv_set_allocator": (_I, [ALLOC_FN, RELEASE_FN, _P]),
     "spconv_build_rulebook": (_I, [_I, _I, _P, _I64, _P, _P, _P, _U, _P, ctypes.POINTER(_P)]),
+    "spconv_build_rulebook_on": (_I, [_P, _I, _P, _P, _U, _P, ctypes.POINTER(_P)]),
+    "spconv_rulebook_bounds": (_I, [_P, _P, _P]),
     "spconv_rulebook_status": (_I, [_P]),
     "spconv_rulebook_query": (_I, [_P, _P, _P, _P, _P, _P]),
     "spconv_rulebook_export": (_I, [_P, _P, _P, _P]),

@@ -64,6 +64,16 @@ int sync_rulebook(spconv_rulebook rb) {
     (void)hipGetLastError();
     return SPCONV_EHIP;
   }
+  if (rb->in_count) {
+    int64_t n_in = 0;
+    if (hipMemcpyAsync(&n_in, rb->n_in_dev, sizeof(n_in), hipMemcpyDeviceToHost, rb->stream) !=
+            hipSuccess ||
+        hipStreamSynchronize(rb->stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return SPCONV_EHIP;
+    }
+    rb->n_in = n_in;
+  }
   rb->synced = true;
   rb->status = status_from_bits(h.status);
   rb->n_out = h.n_out;
@@ -130,9 +140,17 @@ const char* spconv_status_string(int s) {
   }
 }
 
-int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
-                          const int32_t* spatial_size, const int32_t* f, const int32_t* s,
-                          unsigned flags, void* stream, spconv_rulebook* out) {
+}  // extern "C"
+
+// Internal status: a book on another book's outputs cannot take the grid
+// path; the caller reads the count on the host and builds normally.
+constexpr int kNeedHostCount = 2;
+
+// The build behind both entry points.  in_count (device) set: rows [0, N)
+// of coords are a bound and only the first *in_count exist.
+static int build_impl(int kind, int D, const int32_t* coords, int64_t N,
+                      const int64_t* in_count, const int32_t* spatial_size, const int32_t* f,
+                      const int32_t* s, unsigned flags, void* stream, spconv_rulebook* out) {
   if (!out) return SPCONV_EINVAL;
   *out = nullptr;
   if (kind != SPCONV_VSC && kind != SPCONV_SC) return SPCONV_EINVAL;
@@ -158,6 +176,8 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   rb->kind = kind;
   rb->D = D;
   rb->n_in = N;
+  rb->n_in_bound = N;
+  rb->in_count = in_count;
   rb->K = K;
   rb->stream = static_cast<hipStream_t>(stream);
   {
@@ -196,6 +216,10 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
   }
   rb->nblk = (rb->n_cap + kBlock - 1) / kBlock;
   rb->gstride = rb->nblk * kBlock;
+  if (in_count && N > 0 && !grid_build(rb)) {
+    delete rb;
+    return kNeedHostCount;
+  }
 
   // One persistent allocation: header, output sites, gather map, counts,
   // offsets and the pair lists (sized for the worst case K * n_cap so the
@@ -225,6 +249,8 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
     return q;
   };
   rb->hdr = reinterpret_cast<DeviceHeader*>(take(256));
+  rb->n_in_dev = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(rb->hdr) + 128);
+  if (in_count) copy_in_count(rb);
   rb->out_coords = reinterpret_cast<int32_t*>(take(n_cap * D * 4));
   rb->gmap = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->gstride) * 4));
   rb->blk_cnt = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->nblk) * 4 * 2));
@@ -249,6 +275,43 @@ int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
     }
   }
   *out = rb;
+  return SPCONV_OK;
+}
+
+extern "C" {
+
+int spconv_build_rulebook(int kind, int D, const int32_t* coords, int64_t N,
+                          const int32_t* spatial_size, const int32_t* f, const int32_t* s,
+                          unsigned flags, void* stream, spconv_rulebook* out) {
+  return build_impl(kind, D, coords, N, nullptr, spatial_size, f, s, flags, stream, out);
+}
+
+int spconv_build_rulebook_on(spconv_rulebook parent, int kind, const int32_t* f, const int32_t* s,
+                             unsigned flags, void* stream, spconv_rulebook* out) {
+  if (!out) return SPCONV_EINVAL;
+  *out = nullptr;
+  if (!parent || parent->kind != SPCONV_SC || (flags & SPCONV_BUILD_TRANSPOSE))
+    return SPCONV_EINVAL;
+  const int st = build_impl(kind, parent->D, parent->out_coords, parent->n_cap,
+                            &parent->hdr->n_out, parent->out_size, f, s, flags, stream, out);
+  if (st != kNeedHostCount) return st;
+  // the hash-table path needs the count on the host: read it, build normally
+  int64_t n = 0;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(&n, &parent->hdr->n_out, sizeof(n), hipMemcpyDeviceToHost, hs) !=
+          hipSuccess ||
+      hipStreamSynchronize(hs) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_EHIP;
+  }
+  return build_impl(kind, parent->D, parent->out_coords, n, nullptr, parent->out_size, f, s,
+                    flags, stream, out);
+}
+
+int spconv_rulebook_bounds(spconv_rulebook rb, int64_t* n_in_bound, int64_t* n_out_bound) {
+  if (!rb) return SPCONV_EINVAL;
+  if (n_in_bound) *n_in_bound = rb->n_in_bound;
+  if (n_out_bound) *n_out_bound = rb->n_cap;
   return SPCONV_OK;
 }
 

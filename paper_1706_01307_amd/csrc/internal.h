@@ -161,8 +161,15 @@ struct spconv_rulebook_s {
   int kind;
   int D;
   int device;
-  int64_t n_in;
+  int64_t n_in;                // input rows (a bound until synchronised, for a book
+                               // built on another book's outputs)
+  int64_t n_in_bound;          // input rows the buffers are sized for
   int64_t n_cap;               // output rows the buffers are sized for
+  // A book built on another SC book's output sites: the input row count is
+  // that book's device-side output count (read during the build only), and
+  // a copy of it lives in this book's header block (n_in_dev).
+  const int64_t* in_count = nullptr;
+  int64_t* n_in_dev = nullptr;
   int64_t K;
   int32_t size[spc::kMaxD], f[spc::kMaxD], s[spc::kMaxD], out_size[spc::kMaxD];
   hipStream_t stream;          // build stream (owns the allocation)
@@ -213,6 +220,11 @@ int dev_free(spconv_rulebook rb, void* p, hipStream_t st);
 
 // Launchers (rulebook.hip).  All asynchronous on rb->stream.
 int build_vsc(spconv_rulebook rb, const int32_t* coords);
+// Whether the build of this book takes the dense-grid path (the one that can
+// take a device-side input count).
+bool grid_build(spconv_rulebook rb);
+// Enqueue the copy of *rb->in_count into rb->n_in_dev.
+void copy_in_count(spconv_rulebook rb);
 int build_sc(spconv_rulebook rb, const int32_t* coords);
 
 // Radix sort (sort.hip).

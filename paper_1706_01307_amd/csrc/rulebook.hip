@@ -427,13 +427,13 @@ __global__ __launch_bounds__(kBlock) void k_compact(
 // y_j = (x_j - o_j) / s_j when that is a non-negative integer inside the
 // output extent E_j; bit L(y) = lexicographic linear index of y.
 __global__ __launch_bounds__(kBlock) void k_sc_mark(
-    const uint64_t* __restrict__ keys, int64_t N, Codec cin, OffsetTable ot, Extents E,
-    uint32_t* __restrict__ bitmap) {
+    const uint64_t* __restrict__ keys, int64_t N, const int64_t* __restrict__ count, Codec cin,
+    OffsetTable ot, Extents E, uint32_t* __restrict__ bitmap) {
   __shared__ int16_t s_off[kMaxK][kMaxD];
   fill_offsets(ot, s_off);
   __syncthreads();
   const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
-  if (r >= N) return;
+  if (r >= N || (count && r >= *count)) return;
   const uint64_t key = keys[r];
   if (key == kEmpty) return;
   int32_t x[kMaxD];
@@ -464,10 +464,12 @@ __global__ __launch_bounds__(kBlock) void k_bitsum(const uint32_t* __restrict__ 
 }
 
 // Single block: exclusive scan of the block sums; n_out = total.  A total
-// other than `expect` (when >= 0) flags duplicate sites.
+// other than `expect` (when >= 0), or than *expect_dev (when given), flags
+// duplicate sites.
 __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum, int64_t nb,
                                                     DeviceHeader* __restrict__ hdr,
-                                                    int64_t expect) {
+                                                    int64_t expect,
+                                                    const int64_t* __restrict__ expect_dev) {
   int64_t carry = 0;
   for (int64_t base = 0; base < nb; base += 4 * kBlock) {
     uint32_t v[4];
@@ -490,7 +492,8 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
   }
   if (threadIdx.x == 0) {
     hdr->n_out = carry;
-    if (expect >= 0 && carry != expect) atomicOr(&hdr->status, kStDup);
+    if ((expect >= 0 && carry != expect) || (expect_dev && carry != *expect_dev))
+      atomicOr(&hdr->status, kStDup);
   }
 }
 
@@ -1013,10 +1016,10 @@ void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
 // Z-order schedule from the grid; also sets n_out to the number of occupied
 // cells, flagging duplicates when that is not `expect` (>= 0).
 void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
-                          int64_t expect) {
+                          int64_t expect, const int64_t* expect_dev = nullptr) {
   k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
                                                                         b.bitmap, b.bsum);
-  k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect, expect_dev);
   k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
       b.bitmap, b.nwords, b.bsum, b.grid, rb->perm);
 }
@@ -1048,9 +1051,10 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
   if (dev_alloc(rb, grid_bytes(cells) + 256, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
   const GridBufs b = take_grid(&cv, cells);
-  launch_grid_scatter(rb, coords, N, nullptr, g, cells, b, rb->out_coords, Codec{}, nullptr,
-                      false, N);
-  launch_grid_schedule(rb, b, cells, N);
+  // rows [0, N), or [0, *in_count) for a book on another book's outputs
+  launch_grid_scatter(rb, coords, N, rb->in_count, g, cells, b, rb->out_coords, Codec{}, nullptr,
+                      false, rb->in_count ? 0 : N);
+  launch_grid_schedule(rb, b, cells, rb->in_count ? -1 : N, rb->in_count);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
   if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -1082,12 +1086,12 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
   Extents E{};
   for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
-  launch_grid_scatter(rb, coords, N, nullptr, gi, cells_in, bi, nullptr, cin, keys, true, 0);
+  launch_grid_scatter(rb, coords, N, rb->in_count, gi, cells_in, bi, nullptr, cin, keys, true, 0);
   k_fill_u32<<<grid_for(static_cast<int64_t>(lwords)), kBlock, 0, rb->stream>>>(lex, 0u, lwords);
   const OffsetTable ot = make_offsets(rb);
-  k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, cin, ot, E, lex);
+  k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, rb->in_count, cin, ot, E, lex);
   k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
-  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1, nullptr);
   k_sc_emit<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
                                                                      rb->out_coords, nullptr);
   launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
@@ -1098,6 +1102,25 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 }  // namespace
+
+__global__ void k_copy_count(int64_t* __restrict__ dst, const int64_t* __restrict__ src) {
+  if (threadIdx.x == 0) *dst = *src;
+}
+
+void copy_in_count(spconv_rulebook rb) {
+  k_copy_count<<<1, 64, 0, rb->stream>>>(rb->n_in_dev, rb->in_count);
+}
+
+bool grid_build(spconv_rulebook rb) {
+  const int64_t N = rb->n_in;
+  GridGeom g, go;
+  uint64_t ci = 0, co = 0;
+  if (N <= 0 || !make_grid_geom(rb->D, rb->size, &g, &ci) || !use_grid(ci, N)) return false;
+  if (rb->kind == SPCONV_VSC) return true;
+  for (int j = 0; j < rb->D; ++j)
+    if (rb->out_size[j] <= 0) return false;
+  return make_grid_geom(rb->D, rb->out_size, &go, &co);
+}
 
 int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   const int64_t N = rb->n_in;
@@ -1157,9 +1180,9 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_fill_u32<<<grid_for(static_cast<int64_t>(nwords)), kBlock, 0, rb->stream>>>(bitmap, 0u,
                                                                                nwords);
     const OffsetTable ot = make_offsets(rb);
-    k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(tr.keys, N, cin, ot, E, bitmap);
+    k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(tr.keys, N, nullptr, cin, ot, E, bitmap);
     k_bitsum<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(bitmap, nwords, bsum);
-    k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1);
+    k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1, nullptr);
     k_sc_emit<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
     launch_schedule(rb, out_keys, cout, &cv);

@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 16, names
+    assert len(names) == 18, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -114,3 +114,14 @@ def test_set_allocator_needs_both_functions():
     assert lib.spconv_set_allocator(alloc, _lib.RELEASE_FN(), None) == _lib.EINVAL
     assert lib.spconv_set_allocator(_lib.ALLOC_FN(), release, None) == _lib.EINVAL
     assert lib.spconv_set_allocator(_lib.ALLOC_FN(), _lib.RELEASE_FN(), None) == _lib.OK
+
+
+def test_chained_build_and_bounds_reject_null():
+    lib = _lib.load()
+    h = ctypes.c_void_p()
+    f = np.asarray([1, 3, 3], np.int32)
+    s = np.asarray([1, 1, 1], np.int32)
+    assert lib.spconv_build_rulebook_on(None, 0, f.ctypes.data, s.ctypes.data, 0, None,
+                                        ctypes.byref(h)) == _lib.EINVAL
+    assert h.value is None
+    assert lib.spconv_rulebook_bounds(None, None, None) == _lib.EINVAL

@@ -1,0 +1,115 @@
+"""Rule books built on the output sites of an SC rule book (a chain of
+levels) without the host waiting: pair for pair and bit for bit the books
+built from the exported output sites, also for the hash-table path (which
+reads the count on the host) and a three-level chain."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_1706_01307_amd as spc  # noqa: E402
+from paper_1706_01307_amd import inputs  # noqa: E402
+from tests.test_parity_gpu import _bf16_tensor, _t  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _feats(n, C, seed):
+    return _bf16_tensor(inputs.to_bf16_bits(inputs.normal_f32((n, C), seed=seed)))
+
+
+def _weights(K, ci, co, seed):
+    return _bf16_tensor(inputs.to_bf16_bits(
+        inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci), seed=seed)))
+
+
+def _same_book(rb, ref):
+    assert rb.status() == spc.OK
+    assert rb.n_in == ref.n_in and rb.n_out == ref.n_out
+    np.testing.assert_array_equal(rb.pair_off, ref.pair_off)
+    oc, pr = rb.export()
+    oc_r, pr_r = ref.export()
+    assert torch.equal(oc, oc_r) and torch.equal(pr, pr_r)
+
+
+def _forward(rb, x, w, C_out, out_rows):
+    y = torch.zeros((out_rows, C_out), dtype=torch.bfloat16, device="cuda")
+    fwd = spc.vsc_forward if rb.kind == spc.VSC else spc.sc_forward
+    return fwd(rb, x, w, None, out=y)
+
+
+@pytest.mark.parametrize("path", ["grid", "hash"])
+@pytest.mark.parametrize("kind,f,s", [(spc.VSC, [1, 3, 3, 3], None),
+                                      (spc.SC, [1, 2, 2, 2], [1, 2, 2, 2]),
+                                      (spc.SC, [1, 3, 3, 3], [1, 2, 2, 2])])
+def test_chained_book_equals_book_on_exported_sites(monkeypatch, path, kind, f, s):
+    monkeypatch.setenv("SPCONV_RULEBOOK", path)
+    c = inputs.surfaces(2, 48, 6, 20, seed=9, variant="literal")
+    size = [2, 48, 48, 48]
+    parent = spc.build_rulebook(spc.SC, _t(c), size, [1, 2, 2, 2], [1, 2, 2, 2], sync=False)
+    rb = spc.build_rulebook_on(parent, kind, f, s, sync=False)
+    nb_in, nb_out = rb.bounds()
+    K = int(np.prod(f))
+    # features of the parent's outputs, allocated by the bound (no wait yet)
+    x = _feats(nb_in, 32, 31)
+    w = _weights(K, 32, 32, 32)
+    y = _forward(rb, x, w, 32, nb_out)
+    _say(f"[chain] {path} kind={kind} f={f} parent n_out={parent.n_out} bounds={nb_in},{nb_out}")
+    oc, _ = parent.export()
+    ref = spc.build_rulebook(kind, oc, parent.out_spatial_size, f, s)
+    assert nb_in >= parent.n_out and nb_out >= ref.n_out
+    _same_book(rb, ref)
+    y_ref = _forward(ref, x[:parent.n_out].contiguous(), w, 32, ref.n_out)
+    assert torch.equal(y[:ref.n_out], y_ref)
+
+
+def test_three_level_chain_without_waiting():
+    c = inputs.surfaces(2, 64, 8, 28, seed=10, variant="literal")
+    size = [2, 64, 64, 64]
+    f2 = [1, 2, 2, 2]
+    levels = [spc.build_rulebook(spc.SC, _t(c), size, f2, f2, sync=False)]
+    vsc = []
+    for _ in range(2):
+        vsc.append(spc.build_rulebook_on(levels[-1], spc.VSC, [1, 3, 3, 3], sync=False))
+        levels.append(spc.build_rulebook_on(levels[-1], spc.SC, f2, f2, sync=False))
+    # now compare every level with books built from exported sites
+    sites, sz = _t(c), size
+    ref_sc = spc.build_rulebook(spc.SC, sites, sz, f2, f2)
+    for lvl in range(3):
+        _same_book(levels[lvl], ref_sc)
+        sites, _ = ref_sc.export()
+        sz = ref_sc.out_spatial_size
+        if lvl < 2:
+            _same_book(vsc[lvl], spc.build_rulebook(spc.VSC, sites, sz, [1, 3, 3, 3]))
+            ref_sc = spc.build_rulebook(spc.SC, sites, sz, f2, f2)
+
+
+def test_chained_build_argument_errors():
+    c = inputs.pen_strokes(2, 64, seed=3)
+    vsc = spc.build_rulebook(spc.VSC, _t(c), [2, 64, 64], [1, 3, 3])
+    with pytest.raises(ValueError):
+        spc.build_rulebook_on(vsc, spc.VSC, [1, 3, 3])
+    sc = spc.build_rulebook(spc.SC, _t(c), [2, 64, 64], [1, 2, 2], [1, 2, 2])
+    lib = spc._lib.load()
+    import ctypes
+    h = ctypes.c_void_p()
+    f = np.asarray([1, 3, 3], np.int32)
+    one = np.ones(3, np.int32)
+    assert lib.spconv_build_rulebook_on(vsc.handle, 0, f.ctypes.data, one.ctypes.data, 0, None,
+                                        ctypes.byref(h)) == spc.EINVAL
+    assert lib.spconv_build_rulebook_on(sc.handle, 1, f.ctypes.data, one.ctypes.data,
+                                        spc.BUILD_TRANSPOSE, None, ctypes.byref(h)) == spc.EINVAL
+    assert h.value is None
