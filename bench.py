@@ -59,6 +59,9 @@ def _args():
                    help="extra steps after a cache-evicting write each (reported apart)")
     p.add_argument("--ops", action="store_true",
                    help="time pooling, DC and the gradients instead")
+    p.add_argument("--stack-sync", action="store_true",
+                   help="stack mode: wait for each SC build's output count on the host "
+                        "instead of chaining the next build on the device-side count")
     return p.parse_args()
 
 
@@ -312,9 +315,12 @@ def measure_peaks(torch, dev):
 def run_stack(a, wl, torch, dev, lib, _lib, inputs):
     """A stack of layers: VSC levels joined by strided SC layers.  One VSC
     rule book per level serves all its VSC layers (Section 4: layers on the
-    same sites share it); each SC build waits once (the next level needs its
-    output count on the host) and its output sites feed the next build in
-    place.  A step = every build + every forward + releases."""
+    same sites share it).  By default every build after the first is chained
+    on the last SC book (its output sites and device-side count) and feature
+    buffers are sized by the books' row bounds, so a step enqueues all its
+    work without the host waiting; --stack-sync instead reads each SC book's
+    output count on the host before the next level.  A step = every build +
+    every forward + releases."""
     D = wl.d + 1
     bf16 = wl.dtype == "bf16"
     esz = 2 if bf16 else 4
@@ -339,55 +345,67 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
         x0 = torch.from_numpy(xf).to(dev)
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
+    chain = not a.stack_sync
     info = []
+
+    def rows_out(h):
+        if chain:
+            nb_in, nb_out = ctypes.c_int64(), ctypes.c_int64()
+            _lib.check(lib.spconv_rulebook_bounds(h, ctypes.byref(nb_in), ctypes.byref(nb_out)),
+                       "bounds")
+            return nb_out.value
+        n_out = ctypes.c_int64()
+        _lib.check(lib.spconv_rulebook_query(h, None, ctypes.byref(n_out), None, None, None),
+                   "query")
+        return n_out.value
 
     def step(record=False):
         coords, N = ctypes.c_void_p(ct.data_ptr()), N0
         size = np.array(wl.spatial_size, np.int32)
-        x, rb, handles = x0, None, []
+        x, rb, parent, handles = x0, None, None, []
         for j, L in enumerate(wl.layers):
             wt, bt = params[j]
             f = np.array([1] + [L.f] * wl.d, np.int32)
             s = np.array([1] + [L.s] * wl.d, np.int32)
-            if L.kind == "vsc":
-                if rb is None:
-                    rb = ctypes.c_void_p()
-                    _lib.check(lib.spconv_build_rulebook(_lib.VSC, D, coords, N, size.ctypes.data,
-                                                         f.ctypes.data, s.ctypes.data,
-                                                         _lib.BUILD_ASYNC, sp, ctypes.byref(rb)),
-                               "build")
-                    handles.append(rb)
-                y = torch.empty((N, L.c_out), dtype=tdt, device=dev)
-                _lib.check(lib.spconv_vsc_forward(rb, dt_code, ctypes.c_void_p(x.data_ptr()),
-                                                  ctypes.c_void_p(wt.data_ptr()),
-                                                  ctypes.c_void_p(bt.data_ptr()), dt_code,
-                                                  ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out,
-                                                  sp), "vsc forward")
-                k_pairs = None
-            else:
+            kind = _lib.VSC if L.kind == "vsc" else _lib.SC
+            h = rb if L.kind == "vsc" else None
+            if h is None:
                 h = ctypes.c_void_p()
-                _lib.check(lib.spconv_build_rulebook(_lib.SC, D, coords, N, size.ctypes.data,
-                                                     f.ctypes.data, s.ctypes.data, 0, sp,
-                                                     ctypes.byref(h)), "build")
+                flags = _lib.BUILD_ASYNC if (chain or L.kind == "vsc") else 0
+                if chain and parent is not None:
+                    _lib.check(lib.spconv_build_rulebook_on(parent, kind, f.ctypes.data,
+                                                            s.ctypes.data, flags, sp,
+                                                            ctypes.byref(h)), "build on")
+                else:
+                    _lib.check(lib.spconv_build_rulebook(kind, D, coords, N, size.ctypes.data,
+                                                         f.ctypes.data, s.ctypes.data, flags, sp,
+                                                         ctypes.byref(h)), "build")
                 handles.append(h)
-                n_out, osz = ctypes.c_int64(), np.zeros(D, np.int32)
-                _lib.check(lib.spconv_rulebook_query(h, None, ctypes.byref(n_out), None,
-                                                     osz.ctypes.data, None), "query")
-                y = torch.empty((n_out.value, L.c_out), dtype=tdt, device=dev)
-                _lib.check(lib.spconv_sc_forward(h, dt_code, ctypes.c_void_p(x.data_ptr()),
-                                                 ctypes.c_void_p(wt.data_ptr()),
-                                                 ctypes.c_void_p(bt.data_ptr()), dt_code,
-                                                 ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out,
-                                                 sp), "sc forward")
-                oc = ctypes.c_void_p()
-                _lib.check(lib.spconv_rulebook_out_coords(h, ctypes.byref(oc)), "out coords")
-                coords, N, size, rb = oc, n_out.value, osz, None
+            y = torch.empty((rows_out(h), L.c_out), dtype=tdt, device=dev)
+            fwd = lib.spconv_vsc_forward if L.kind == "vsc" else lib.spconv_sc_forward
+            _lib.check(fwd(h, dt_code, ctypes.c_void_p(x.data_ptr()),
+                           ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(bt.data_ptr()),
+                           dt_code, ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out, sp),
+                       "forward")
+            if L.kind == "vsc":
+                rb = h
+            else:
+                rb, parent = None, h
+                if not chain:
+                    osz = np.zeros(D, np.int32)
+                    _lib.check(lib.spconv_rulebook_query(h, None, None, None, osz.ctypes.data,
+                                                         None), "query")
+                    oc = ctypes.c_void_p()
+                    _lib.check(lib.spconv_rulebook_out_coords(h, ctypes.byref(oc)),
+                               "out coords")
+                    coords, N, size = oc, y.shape[0], osz
             if record:
+                n_in, n_out = ctypes.c_int64(), ctypes.c_int64()
                 off = np.zeros(L.f ** wl.d + 1, np.int64)
-                _lib.check(lib.spconv_rulebook_query(handles[-1], None, None, None, None,
-                                                     off.ctypes.data), "query")
-                info.append({"layer": j, "kind": L.kind, "n_in": int(x.shape[0]),
-                             "n_out": int(y.shape[0]), "c_in": L.c_in, "c_out": L.c_out,
+                _lib.check(lib.spconv_rulebook_query(h, ctypes.byref(n_in), ctypes.byref(n_out),
+                                                     None, None, off.ctypes.data), "query")
+                info.append({"layer": j, "kind": L.kind, "n_in": n_in.value,
+                             "n_out": n_out.value, "c_in": L.c_in, "c_out": L.c_out,
                              "sum_k": int(off[-1])})
             x = y
         for h in handles:
@@ -399,8 +417,11 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
         step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    host = 0.0
     for _ in range(a.steps):
+        h0 = time.perf_counter()
         step()
+        host += time.perf_counter() - h0
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / a.steps
     flops = sum(2.0 * r["sum_k"] * r["c_in"] * r["c_out"] for r in info)
@@ -410,9 +431,11 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
         "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "variant": a.variant, "batch": wl.batch,
-                   "grid": wl.size, "active_sites": N0, "layers": info},
+                   "grid": wl.size, "active_sites": N0, "layers": info,
+                   "builds": "chained on device counts" if chain else "host waits per SC"},
         "knobs": knobs(),
         "effective_tflops": flops / (ms * 1e-3) / 1e12,
+        "host_enqueue_ms_per_step": host * 1e3 / a.steps,
         "bytes_features": int(sum(r["n_in"] * r["c_in"] * esz + r["n_out"] * r["c_out"] * esz
                                   for r in info))}), flush=True)
 

@@ -273,14 +273,34 @@ int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, co
  * release(ptr, stream, ctx), both on the build stream and stream-ordered
  * there (a caching allocator may hand the memory to later work on that
  * stream).  A rule book keeps the pair it was built with, so a change applies
- * to later builds only.  Both NULL (the default): hipMallocAsync /
- * hipFreeAsync.  An alloc that returns NULL makes the build return ENOMEM
+ * to later builds only.  Both NULL (the default): the library's own block
+ * cache (see spconv_release_cached_memory).  An alloc that returns NULL makes
+ * the build return ENOMEM
  * after releasing everything it had taken.  Ownership: the library calls
  * release exactly once for every non-NULL pointer alloc returned.  Errors:
  * EINVAL when only one of the two functions is given.  Set it while no build
  * is running on another thread. */
 int spconv_set_allocator(void* (*alloc)(size_t bytes, void* stream, void* ctx),
                          void (*release)(void* ptr, void* stream, void* ctx), void* ctx);
+
+/* The default allocator keeps the device memory that rule books and builds
+ * give back (on their build stream) and hands it to later requests of up to
+ * the block's size on any stream: an event recorded where the block was given
+ * back is waited for on the new stream (on the device; the host never waits),
+ * so the blocks of a book rebuilt every step are reused without driver calls.
+ * When a fresh hipMalloc fails, the idle blocks of that device are freed and
+ * the allocation is tried once more.  spconv_release_cached_memory frees every
+ * idle block on every device (waiting for the work that last used each) and
+ * stores the bytes freed in *released (may be NULL); blocks of live rule books
+ * stay.  Always SPCONV_OK.  Another allocator in the same process (a caching
+ * one such as torch's) cannot take memory held idle here: call this first, or
+ * route the library through that allocator with spconv_set_allocator. */
+int spconv_release_cached_memory(int64_t* released);
+
+/* Bytes of device memory on `device` that the default allocator has handed
+ * out (live rule books and running builds) and holds idle.  Either pointer
+ * may be NULL.  Errors: EINVAL for a device index out of range, EHIP. */
+int spconv_memory_stats(int device, int64_t* in_use, int64_t* cached);
 
 /* Release a rule book (stream-ordered on its build stream).  NULL is a
  * no-op. */

@@ -24,7 +24,8 @@ __all__ = ["VSC", "SC", "F32", "BF16", "BUILD_ASYNC", "BUILD_TRANSPOSE", "OP_VSC
            "OP_DC", "POOL_MAX", "POOL_AVG", "Rulebook", "build_rulebook", "build_rulebook_on",
            "vsc_forward",
            "sc_forward", "forward_fused", "dc_forward", "pool_forward", "backward_data",
-           "backward_weight", "set_allocator", "use_torch_allocator",
+           "backward_weight", "set_allocator", "use_torch_allocator", "release_cached_memory",
+           "memory_stats",
            "SpconvError", "OK", "EINVAL", "EDUP", "ERANGE", "ENOMEM", "ECAP", "EHIP"]
 
 
@@ -144,7 +145,8 @@ _ALLOCATORS = []
 def set_allocator(alloc=None, release=None):
     """Device memory of later rule-book builds from Python callables:
     alloc(nbytes, stream_handle) -> device address (0 = out of memory) and
-    release(address, stream_handle).  Both None: back to hipMallocAsync."""
+    release(address, stream_handle).  Both None: back to the library's own
+    block cache (see release_cached_memory)."""
     if (alloc is None) != (release is None):
         raise ValueError("give both alloc and release, or neither")
     lib = _lib.load()
@@ -179,6 +181,26 @@ def use_torch_allocator():
         torch.cuda.caching_allocator_delete(ptr)
 
     set_allocator(alloc, release)
+
+
+def release_cached_memory():
+    """Free the device memory the library's block cache holds idle (on every
+    device); returns the bytes freed.  Rule books alive keep theirs."""
+    n = ctypes.c_int64()
+    _lib.check(_lib.load().spconv_release_cached_memory(ctypes.byref(n)),
+               "spconv_release_cached_memory")
+    return n.value
+
+
+def memory_stats(device=None):
+    """(bytes in use, bytes cached idle) of the library's default allocator
+    on `device` (default: torch's current device)."""
+    torch = _torch()
+    dev = torch.cuda.current_device() if device is None else int(device)
+    a, b = ctypes.c_int64(), ctypes.c_int64()
+    _lib.check(_lib.load().spconv_memory_stats(dev, ctypes.byref(a), ctypes.byref(b)),
+               "spconv_memory_stats")
+    return a.value, b.value
 
 
 def build_rulebook(kind, coords, spatial_size, f, s=None, *, sync=True, transpose=False,

@@ -30,6 +30,8 @@ SIGNATURES = {
     "spconv_build_rulebook": (_I, [_I, _I, _P, _I64, _P, _P, _P, _U, _P, ctypes.POINTER(_P)]),
     "spconv_build_rulebook_on": (_I, [_P, _I, _P, _P, _U, _P, ctypes.POINTER(_P)]),
     "spconv_rulebook_bounds": (_I, [_P, _P, _P]),
+    "spconv_release_cached_memory": (_I, [_P]),
+    "spconv_memory_stats": (_I, [_I, _P, _P]),
     "spconv_rulebook_status": (_I, [_P]),
     "spconv_rulebook_query": (_I, [_P, _P, _P, _P, _P, _P]),
     "spconv_rulebook_export": (_I, [_P, _P, _P, _P]),

@@ -30,23 +30,6 @@ namespace {
 
 using namespace spc;
 
-// Keep freed stream-ordered memory in the device's default pool, so that
-// rule books rebuilt every step reuse it instead of returning it to the
-// driver.
-void keep_pool_memory(int dev) {
-  static std::mutex mu;
-  static bool done[64] = {};
-  std::lock_guard<std::mutex> lk(mu);
-  if (dev < 0 || dev >= 64 || done[dev]) return;
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-    uint64_t thr = ~0ull;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
-  }
-  (void)hipGetLastError();
-  done[dev] = true;
-}
-
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 int status_from_bits(uint32_t bits) {
@@ -98,12 +81,8 @@ int spc::dev_alloc(spconv_rulebook rb, size_t bytes, hipStream_t st, void** p) {
     *p = rb->al.alloc(bytes, st, rb->al.ctx);
     return *p ? SPCONV_OK : SPCONV_ENOMEM;
   }
-  if (hipMallocAsync(p, bytes, st) != hipSuccess) {
-    (void)hipGetLastError();
-    *p = nullptr;
-    return SPCONV_ENOMEM;
-  }
-  return SPCONV_OK;
+  *p = cache_alloc(rb->device, bytes, st);
+  return *p ? SPCONV_OK : SPCONV_ENOMEM;
 }
 
 int spc::dev_free(spconv_rulebook rb, void* p, hipStream_t st) {
@@ -112,7 +91,7 @@ int spc::dev_free(spconv_rulebook rb, void* p, hipStream_t st) {
     rb->al.release(p, st, rb->al.ctx);
     return SPCONV_OK;
   }
-  return hipFreeAsync(p, st) == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+  return cache_free(rb->device, p, st) == SPCONV_OK ? SPCONV_OK : SPCONV_EHIP;
 }
 
 extern "C" {
@@ -124,6 +103,26 @@ int spconv_set_allocator(void* (*alloc)(size_t, void*, void*),
   g_alloc.alloc = alloc;
   g_alloc.release = release_fn;
   g_alloc.ctx = alloc ? ctx : nullptr;
+  return SPCONV_OK;
+}
+
+int spconv_release_cached_memory(int64_t* released) {
+  const size_t n = cache_release_all();
+  if (released) *released = static_cast<int64_t>(n);
+  return SPCONV_OK;
+}
+
+int spconv_memory_stats(int device, int64_t* in_use, int64_t* cached) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_EHIP;
+  }
+  if (device < 0 || device >= n) return SPCONV_EINVAL;
+  size_t live = 0, idle = 0;
+  cache_stats(device, &live, &idle);
+  if (in_use) *in_use = static_cast<int64_t>(live);
+  if (cached) *cached = static_cast<int64_t>(idle);
   return SPCONV_OK;
 }
 
@@ -185,7 +184,6 @@ static int build_impl(int kind, int D, const int32_t* coords, int64_t N,
     rb->al = g_alloc;
   }
   (void)hipGetDevice(&rb->device);
-  keep_pool_memory(rb->device);
   uint64_t cells = 1, fan = 1;
   for (int j = 0; j < D; ++j) {
     rb->size[j] = spatial_size[j];

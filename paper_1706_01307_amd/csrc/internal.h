@@ -213,6 +213,15 @@ struct spconv_rulebook_s {
 
 namespace spc {
 
+// The library's default allocator (blockcache.hip): blocks of device `dev`
+// handed out on, and given back on, a stream; reuse is ordered by events.
+// cache_alloc returns nullptr when the device has no memory left;
+// cache_free: SPCONV_OK, SPCONV_EINVAL (not a cache block) or SPCONV_EHIP.
+void* cache_alloc(int dev, size_t bytes, hipStream_t st);
+int cache_free(int dev, void* p, hipStream_t st);
+size_t cache_release_all();      // frees the idle blocks of every device
+void cache_stats(int dev, size_t* live_bytes, size_t* idle_bytes);
+
 // Stream-ordered device memory through the rule book's allocator.
 // dev_alloc: SPCONV_OK or SPCONV_ENOMEM; dev_free: SPCONV_OK or SPCONV_EHIP.
 int dev_alloc(spconv_rulebook rb, size_t bytes, hipStream_t st, void** p);

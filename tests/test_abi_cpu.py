@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 18, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -125,3 +125,12 @@ def test_chained_build_and_bounds_reject_null():
                                         ctypes.byref(h)) == _lib.EINVAL
     assert h.value is None
     assert lib.spconv_rulebook_bounds(None, None, None) == _lib.EINVAL
+
+
+def test_block_cache_entry_points_without_a_device():
+    lib = _lib.load()
+    n = ctypes.c_int64(-1)
+    assert lib.spconv_release_cached_memory(ctypes.byref(n)) == _lib.OK
+    assert n.value == 0
+    assert lib.spconv_release_cached_memory(None) == _lib.OK
+    assert lib.spconv_memory_stats(-1, None, None) in (_lib.EINVAL, _lib.EHIP)

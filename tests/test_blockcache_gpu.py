@@ -1,0 +1,89 @@
+"""The library's default allocator (a block cache): blocks come back when
+rule books are destroyed, are reused by later builds on the same or another
+stream (ordered by events, the host never waiting), and are freed on
+request."""
+import gc
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_1706_01307_amd as spc  # noqa: E402
+from paper_1706_01307_amd import inputs  # noqa: E402
+from tests.test_parity_gpu import _t  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _book_arrays(rb):
+    oc, pr = rb.export()
+    return rb.pair_off, oc.cpu().numpy(), pr.cpu().numpy()
+
+
+def test_blocks_return_to_the_cache_and_are_released():
+    gc.collect()
+    torch.cuda.synchronize()
+    used0, _ = spc.memory_stats()
+    c = inputs.surfaces(2, 64, 8, 28, seed=4, variant="literal")
+    rbs = [spc.build_rulebook(spc.VSC, _t(c), [2, 64, 64, 64], [1, 3, 3, 3]),
+           spc.build_rulebook(spc.SC, _t(c), [2, 64, 64, 64], [1, 2, 2, 2], [1, 2, 2, 2],
+                              transpose=True)]
+    used1, cached1 = spc.memory_stats()
+    _say(f"[cache] in use {used0} -> {used1}, cached {cached1}")
+    assert used1 > used0
+    for rb in rbs:
+        rb.close()
+    used2, cached2 = spc.memory_stats()
+    assert used2 == used0
+    assert cached2 >= used1 - used0
+    # the same builds again take the cached blocks: nothing new is allocated
+    rb = spc.build_rulebook(spc.VSC, _t(c), [2, 64, 64, 64], [1, 3, 3, 3])
+    used3, cached3 = spc.memory_stats()
+    assert used3 > used0 and used3 + cached3 == used2 + cached2
+    rb.close()
+    torch.cuda.synchronize()
+    freed = spc.release_cached_memory()
+    used4, cached4 = spc.memory_stats()
+    assert cached4 == 0 and used4 == used0 and freed >= cached2
+
+
+@pytest.mark.parametrize("kind", [spc.VSC, spc.SC])
+def test_block_reused_on_another_stream_while_the_first_is_busy(kind):
+    spc.release_cached_memory()
+    c = inputs.surfaces(2, 64, 8, 28, seed=5, variant="literal")
+    size = [2, 64, 64, 64]
+    f = [1, 3, 3, 3] if kind == spc.VSC else [1, 2, 2, 2]
+    s = None if kind == spc.VSC else [1, 2, 2, 2]
+    ref = _book_arrays(spc.build_rulebook(kind, _t(c), size, f, s))
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    big = torch.randn(4096, 4096, device="cuda")
+    ct = _t(c)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        with torch.cuda.stream(sa):
+            for _ in range(6):
+                big = (big @ big).clamp_(-1, 1)      # keeps stream A busy
+            rb_a = spc.build_rulebook(kind, ct, size, f, s, sync=False, stream=sa)
+            rb_a.close()                               # its blocks go idle with A still busy
+        with torch.cuda.stream(sb):
+            rb_b = spc.build_rulebook(kind, ct, size, f, s, sync=False, stream=sb)
+            got = _book_arrays(rb_b)
+            rb_b.close()
+        _say(f"[cache] kind={kind} rep={rep} pairs={int(got[0][-1])}")
+        np.testing.assert_array_equal(got[0], ref[0])
+        np.testing.assert_array_equal(got[1], ref[1])
+        np.testing.assert_array_equal(got[2], ref[2])
+    torch.cuda.synchronize()
