@@ -73,7 +73,7 @@ def knobs():
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("forward.hip", "forward_kernels.h", "forward_w0.hip", "internal.h"):
+    for f in ("forward.hip", "forward_kernels.h", "forward_w0.hip", "forward_types.h"):
         with open(os.path.join(ROOT, "paper_1706_01307_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
