@@ -2,7 +2,7 @@
 // sites to rows, then list the (input row, output row) pairs of every filter
 // offset).  Two interchangeable site maps, chosen per build:
 //
-// Dense grid (grids of up to 2^29 cells and at most ~64 cells per site):
+// Dense grid (grids of up to 2^29 cells and at most ~400 cells per site):
 //   every cell of the grid holds 1 + row (0 = empty), cells laid out along
 //   the Z-order curve of the sites.
 //   k_zero_u32 + k_grid_scatter   clear, then store 1 + r into r's cell
@@ -963,17 +963,19 @@ bool make_grid_geom(int D, const int32_t* size, GridGeom* g, uint64_t* cells) {
   return *cells < kGridMaxCells;
 }
 
-// Dense grid or hash table for the input sites.  The grid costs about 8
-// bytes of memory traffic per cell (clearing it, deriving its bitmap), the
-// hash table a few hundred nanoseconds of latency-bound work per thousand
-// sites; the grid is taken while it has at most 64 cells per site (plus 4M
-// cells for small inputs).  SPCONV_RULEBOOK=hash / =grid forces a choice.
+// Dense grid or hash table for the input sites.  The grid costs memory
+// traffic per cell of its power-of-two padded extent (clearing it, deriving
+// its bitmap), the hash table latency-bound work per site plus a fixed
+// ~170 us of sorting and compaction.  Measured on surfaces (VSC 3^3 and SC
+// 2^3/2 builds), the two cross between 400 and 600 padded cells per site, so
+// the grid is taken while it has at most 400 cells per site (plus 4M cells
+// for small inputs).  SPCONV_RULEBOOK=hash / =grid forces a choice.
 bool use_grid(uint64_t cells, int64_t N) {
   if (const char* e = std::getenv("SPCONV_RULEBOOK")) {
     if (std::strcmp(e, "hash") == 0) return false;
     if (std::strcmp(e, "grid") == 0) return true;
   }
-  return cells <= 64ull * static_cast<uint64_t>(N) + (1ull << 22);
+  return cells <= 400ull * static_cast<uint64_t>(N) + (1ull << 22);
 }
 
 struct GridBufs {
