@@ -662,6 +662,7 @@ __global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict
   }
 }
 
+typedef uint32_t dw4 __attribute__((ext_vector_type(4)));
 constexpr uint32_t kBufDword3 = 0x00020000u;   // gfx9 raw buffer descriptor word 3
 constexpr uint32_t kOOB = 0x80000000u;         // byte offset past every buffer: loads 0
 
@@ -741,6 +742,136 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
     }
   }
   publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk, blk);
+}
+
+// The same probe for VSC 3x3x3 on a 4-D grid (sample + 3 coordinates) whose
+// two lowest Z bits are the lowest bits of coordinates 3 and 2: the four
+// cells that differ only there are 16 contiguous bytes, so the 3 x 3 window
+// of a cell in those coordinates lies in 2 x 2 such groups, and 12 16-byte
+// loads cover the 26 neighbours where the generic probe makes 26 4-byte
+// loads (each of which costs the L1 a tag lookup per lane).  Group addresses
+// stay inside the grid even for neighbours off its edge (the dilated
+// addition wraps within the coordinate's bits); those are masked by the
+// coordinate range checks.  Offset i = 9 (dx + 1) + 3 (dy + 1) + (dz + 1).
+__global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
+    const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
+    const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g,
+    const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
+    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
+  const int64_t blk = probe_block(hdr->n_out, nblk);
+  if (blk < 0) return;
+  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
+  const int64_t n_rows = hdr->n_out;
+  const int64_t p = blk * kBlock + threadIdx.x;
+  const bool valid = p < n_rows;
+  const int wave = threadIdx.x / kWave;
+  const int32_t y = valid ? perm[p] : 0;
+  int4 c = make_int4(0, 0, 0, 0);
+  if (valid) c = reinterpret_cast<const int4*>(rows_sites)[y];
+  // dilated +1 / -1 in every coordinate (uniform)
+  // (-1 in a coordinate's bits is all of them; +1 is the lowest)
+  uint32_t dp[4], dm[4];
+#pragma unroll
+  for (int j = 1; j < 4; ++j) {
+    dm[j] = g.M[j];
+    dp[j] = g.M[j] & (0u - g.M[j]);
+  }
+  const uint32_t z1 = deposit(static_cast<uint32_t>(c.y), g.M[1]) | ~g.M[1];
+  const uint32_t z2 = deposit(static_cast<uint32_t>(c.z), g.M[2]) | ~g.M[2];
+  const uint32_t z3 = deposit(static_cast<uint32_t>(c.w), g.M[3]) | ~g.M[3];
+  const uint32_t base = static_cast<uint32_t>(c.x) << g.B;
+  const uint32_t xp[3] = {(z1 + dm[1]) & g.M[1], z1 & g.M[1], (z1 + dp[1]) & g.M[1]};
+  const uint32_t yp[2] = {(z2 + dm[2]) & g.M[2], (z2 + dp[2]) & g.M[2]};
+  const uint32_t zp[2] = {(z3 + dm[3]) & g.M[3], (z3 + dp[3]) & g.M[3]};
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(grid), 0, static_cast<int>(cells * 4), static_cast<int>(kBufDword3));
+  dw4 v[3][2][2];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        const uint32_t cell = (base | xp[a] | yp[b] | zp[d]) & ~3u;
+        v[a][b][d] = __builtin_bit_cast(
+            dw4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, valid ? cell * 4 : kOOB, 0, 0));
+      }
+  const int yo = c.z & 1, zo = c.w & 1;
+  bool xok[3], yok[3], zok[3];
+#pragma unroll
+  for (int o = 0; o < 3; ++o) {
+    xok[o] = valid && c.y + o - 1 >= 0 && c.y + o - 1 < g.size[1];
+    yok[o] = c.z + o - 1 >= 0 && c.z + o - 1 < g.size[2];
+    zok[o] = c.w + o - 1 >= 0 && c.w + o - 1 < g.size[3];
+  }
+#pragma unroll
+  for (int i = 0; i < 27; ++i) {
+    const int dx = i / 9, dy = (i / 3) % 3, dz = i % 3;   // 0, 1, 2 = -1, 0, +1
+    int32_t e;
+    if (i == 13) {
+      e = valid ? y + 1 : 0;
+    } else {
+      // group in y: the lower one holds y - 1 (and y when y is odd)
+      const bool bh = dy == 2 || (dy == 1 && !yo);
+      const bool dh = dz == 2 || (dz == 1 && !zo);
+      const dw4 w0 = bh ? v[dx][1][0] : v[dx][0][0];
+      const dw4 w1 = bh ? v[dx][1][1] : v[dx][0][1];
+      const dw4 w = dh ? w1 : w0;
+      const int ey = dy == 1 ? yo : yo ^ 1;       // bit 0 of y + dy - 1
+      const int ez = dz == 1 ? zo : zo ^ 1;
+      const uint32_t lo = ez ? w.y : w.x, hi = ez ? w.w : w.z;
+      const uint32_t val = ey ? hi : lo;
+      e = (xok[dx] && yok[dy] && zok[dz]) ? static_cast<int32_t>(val) : 0;
+    }
+    if (p < gstride) gmap[i * gstride + p] = e;   // 1 + input row, 0 = none
+    const uint64_t m = __ballot(e != 0);
+    if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
+  }
+  publish_counts(s_cnt, 27, blk_cnt, wpre, nblk, blk);
+}
+
+// SC 2^3 with stride 2 on a 4-D grid whose three lowest Z bits are the lowest
+// bits of coordinates 3, 2, 1: the receptive field of output site c is the
+// aligned 2 x 2 x 2 cube at 2c, 8 consecutive cells (32 bytes) in the order
+// of the offsets (i = 4 o_1 + 2 o_2 + o_3), read with two 16-byte loads
+// instead of eight 4-byte ones.
+__global__ __launch_bounds__(kBlock) void k_probe_grid_sc2(
+    const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
+    const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g,
+    const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
+    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
+  const int64_t blk = probe_block(hdr->n_out, nblk);
+  if (blk < 0) return;
+  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
+  const int64_t n_rows = hdr->n_out;
+  const int64_t p = blk * kBlock + threadIdx.x;
+  const bool valid = p < n_rows;
+  const int wave = threadIdx.x / kWave;
+  const int32_t y = valid ? perm[p] : 0;
+  int4 c = make_int4(0, 0, 0, 0);
+  if (valid) c = reinterpret_cast<const int4*>(rows_sites)[y];
+  const uint32_t cell = (static_cast<uint32_t>(c.x) << g.B) |
+                        deposit(2u * static_cast<uint32_t>(c.y), g.M[1]) |
+                        deposit(2u * static_cast<uint32_t>(c.z), g.M[2]) |
+                        deposit(2u * static_cast<uint32_t>(c.w), g.M[3]);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(grid), 0, static_cast<int>(cells * 4), static_cast<int>(kBufDword3));
+  const dw4 v0 = __builtin_bit_cast(
+      dw4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, valid ? cell * 4 : kOOB, 0, 0));
+  const dw4 v1 = __builtin_bit_cast(
+      dw4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, valid ? cell * 4 + 16 : kOOB, 0, 0));
+  const uint32_t cv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int o1 = i >> 2, o2 = (i >> 1) & 1, o3 = i & 1;
+    const bool ok = valid && 2 * c.y + o1 < g.size[1] && 2 * c.z + o2 < g.size[2] &&
+                    2 * c.w + o3 < g.size[3];
+    const int32_t e = ok ? static_cast<int32_t>(cv[i]) : 0;
+    if (p < gstride) gmap[i * gstride + p] = e;   // 1 + input row, 0 = none
+    const uint64_t m = __ballot(e != 0);
+    if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
+  }
+  publish_counts(s_cnt, 8, blk_cnt, wpre, nblk, blk);
 }
 
 // ---------------------------------------------------------------------------
@@ -1035,6 +1166,22 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
         rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
   };
   const bool sc = rb->kind == SPCONV_SC;
+  if (!sc && rb->D == 4 && rb->f[1] == 3 && rb->f[2] == 3 && rb->f[3] == 3 &&
+      (g.M[3] & 1u) && (g.M[2] & 2u)) {
+    k_probe_grid_g4<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
+        rows_sites, rb->perm, rb->hdr, rb->gstride, g, b.grid, static_cast<uint32_t>(cells),
+        rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
+    launch_scan_compact(rb);
+    return;
+  }
+  if (sc && rb->D == 4 && rb->f[1] == 2 && rb->f[2] == 2 && rb->f[3] == 2 && rb->s[1] == 2 &&
+      rb->s[2] == 2 && rb->s[3] == 2 && (g.M[3] & 1u) && (g.M[2] & 2u) && (g.M[1] & 4u)) {
+    k_probe_grid_sc2<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
+        rows_sites, rb->perm, rb->hdr, rb->gstride, g, b.grid, static_cast<uint32_t>(cells),
+        rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
+    launch_scan_compact(rb);
+    return;
+  }
 #define SPC_PROBE(S)                                         \
   switch (rb->D) {                                           \
     case 2: launch(k_probe_grid<S, 2>); break;               \
