@@ -487,3 +487,25 @@ def test_forward_on_both_rulebook_paths(monkeypatch, path):
                   dtype="bf16", what=f"forward {path}")
     compare_layer(spc.SC, coords, [3, 36, 36, 36], [1, 2, 2, 2], [1, 2, 2, 2], 64, 64,
                   dtype="bf16", what=f"forward SC {path}")
+
+
+# Grids that exercise the grouped probes (VSC 3^3 and SC 2^3 stride 2 on 4-D
+# grids read 16-byte cell groups) at their edges: odd and tiny extents, and
+# extents of 1 that send a build to the one-cell-per-load probe instead.
+GROUP_PROBE_SIZES = [[2, 3, 5, 7], [1, 2, 2, 2], [3, 9, 2, 4], [2, 6, 6, 1], [2, 1, 5, 5],
+                     [1, 17, 3, 33]]
+
+
+@pytest.mark.parametrize("density", [0.5, 0.06])
+@pytest.mark.parametrize("size", GROUP_PROBE_SIZES)
+def test_group_probe_edges(monkeypatch, size, density):
+    monkeypatch.setenv("SPCONV_RULEBOOK", "grid")
+    rng = np.random.default_rng(int(np.prod(size)) + int(density * 100))
+    c = dense_ref.random_sites(rng, size, density)
+    if len(c) == 0:
+        c = np.zeros((1, 4), np.int32)
+    compare_layer(spc.VSC, c, size, [1, 3, 3, 3], [1, 1, 1, 1], 32, 32, dtype="bf16",
+                  what="group probe VSC")
+    if all(v >= 2 for v in size[1:]):
+        compare_layer(spc.SC, c, size, [1, 2, 2, 2], [1, 2, 2, 2], 32, 32, dtype="bf16",
+                      what="group probe SC")
