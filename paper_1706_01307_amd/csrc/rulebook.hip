@@ -647,19 +647,37 @@ __global__ __launch_bounds__(kBlock) void k_grid_bits(const uint32_t* __restrict
 // Rows of the occupied cells in cell order -> perm (the Z-order schedule),
 // one bitmap word per thread; block bases from k_grid_bits + k_bitscan.
 __global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict__ bitmap,
-                                                      uint64_t nwords,
+                                                      uint64_t nwords, uint64_t cells,
                                                       const uint32_t* __restrict__ bbase,
                                                       const uint32_t* __restrict__ grid,
                                                       int32_t* __restrict__ perm) {
   const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
-  uint32_t word = w < nwords ? bitmap[w] : 0u;
+  const uint32_t word = w < nwords ? bitmap[w] : 0u;
   uint32_t tot;
   uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
-  while (word) {
-    const int b = __builtin_ctz(word);
-    word &= word - 1;
-    perm[rank++] = static_cast<int32_t>(grid[32 * w + b]) - 1;
+  if (!word) return;
+  // the word's 32 cells as eight 16-byte loads issued together (a loop of
+  // one load per occupied cell waits out each load's latency in turn); a
+  // word's cells are whole 16-byte groups except in a grid's last word,
+  // where the cells past the end are not read
+  uint32_t v[32];
+  if (32 * w + 32 <= cells) {
+    const uint4* q = reinterpret_cast<const uint4*>(grid + 32 * w);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint4 t = q[k];
+      v[4 * k] = t.x;
+      v[4 * k + 1] = t.y;
+      v[4 * k + 2] = t.z;
+      v[4 * k + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 32; ++k) v[k] = 32 * w + k < cells ? grid[32 * w + k] : 0u;
   }
+#pragma unroll
+  for (int k = 0; k < 32; ++k)
+    if ((word >> k) & 1u) perm[rank++] = static_cast<int32_t>(v[k]) - 1;
 }
 
 typedef uint32_t dw4 __attribute__((ext_vector_type(4)));
@@ -1154,7 +1172,7 @@ void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
                                                                         b.bitmap, b.bsum);
   k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect, expect_dev);
   k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
-      b.bitmap, b.nwords, b.bsum, b.grid, rb->perm);
+      b.bitmap, b.nwords, cells, b.bsum, b.grid, rb->perm);
 }
 
 void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const GridGeom& g,
