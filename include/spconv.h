@@ -33,8 +33,9 @@
  *          level (the order the forward walks its output tiles).
  * Memory.  coords, x, w, bias, y are device pointers owned by the caller:
  *          contiguous, row-major, 16-byte aligned.  Host pointers are marked
- *          "host".  A rule book owns its device memory (stream-ordered
- *          allocations on the build stream) until spconv_rulebook_destroy.
+ *          "host".  A rule book owns its device memory (taken on the build
+ *          stream from the library's allocator, see spconv_set_allocator)
+ *          until spconv_rulebook_destroy.
  * Streams. `stream` is a hipStream_t passed as void*; NULL is the null
  *          stream.  All work is enqueued on it.
  * Errors.  Every call returns a spconv_status; nothing is printed and
