@@ -87,3 +87,30 @@ def test_block_reused_on_another_stream_while_the_first_is_busy(kind):
         np.testing.assert_array_equal(got[1], ref[1])
         np.testing.assert_array_equal(got[2], ref[2])
     torch.cuda.synchronize()
+
+
+def test_chained_builds_return_every_block():
+    gc.collect()
+    torch.cuda.synchronize()
+    used0, _ = spc.memory_stats()
+    c = inputs.surfaces(2, 64, 8, 28, seed=6, variant="literal")
+    f2 = [1, 2, 2, 2]
+    books = [spc.build_rulebook(spc.SC, _t(c), [2, 64, 64, 64], f2, f2, sync=False)]
+    for _ in range(2):
+        books.append(spc.build_rulebook_on(books[-1], spc.VSC, [1, 3, 3, 3], sync=False))
+        books.append(spc.build_rulebook_on(books[-2], spc.SC, f2, f2, sync=False))
+    assert all(b.status() == spc.OK for b in books)
+    used1, _ = spc.memory_stats()
+    assert used1 > used0
+    for b in reversed(books):
+        b.close()
+    used2, _ = spc.memory_stats()
+    _say(f"[cache] chain of {len(books)} books: in use {used0} -> {used1} -> {used2}")
+    assert used2 == used0
+
+
+def test_memory_stats_rejects_bad_device():
+    lib = spc._lib.load()
+    n = torch.cuda.device_count()
+    assert lib.spconv_memory_stats(n, None, None) == spc.EINVAL
+    assert lib.spconv_memory_stats(-1, None, None) == spc.EINVAL
