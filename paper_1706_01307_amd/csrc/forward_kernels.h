@@ -587,6 +587,7 @@ void launch_mfma(const Call& c) {
   // step with a third of the registers, so more workgroups share a CU.
   auto kern = c.v.K == 27  ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
               : c.v.K == 1 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 1, true, WT>
+              : c.v.K == 8 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 8, true, WT, true>
                            : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
   // The block epilogue (scale / residual / ReLU) is compiled into its own
   // kernels, so that the plain forward keeps its register count.
