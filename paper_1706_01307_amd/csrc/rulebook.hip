@@ -438,6 +438,10 @@ __global__ __launch_bounds__(kBlock) void k_sc_mark(
   if (key == kEmpty) return;
   int32_t x[kMaxD];
   unpack_site(cin, key, x);
+  // Offsets are tried in turn even where f = s leaves one candidate: the
+  // inputs of one output site then set its bit in different rounds, and all
+  // but the first find it set and skip the atomic (computing the one output
+  // directly and setting every lane's bit at once measured ~45 % slower).
   for (int i = 0; i < ot.K; ++i) {
     uint32_t L = 0;
     bool ok = true;
@@ -507,16 +511,33 @@ __global__ __launch_bounds__(kBlock) void k_sc_emit(
   uint32_t word = w < nwords ? bitmap[w] : 0u;
   uint32_t tot;
   uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
+  if (!word) return;
+  // coordinates of the word's first cell (one division per dimension); a set
+  // bit b adds b to the last coordinate, carried into the others only when
+  // it passes the extent
+  int32_t y0[kMaxD];
+  {
+    uint32_t L = static_cast<uint32_t>(w * 32);
+    for (int j = cout.D - 1; j >= 0; --j) {
+      y0[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
+      L /= static_cast<uint32_t>(E.e[j]);
+    }
+  }
   while (word) {
     const int b = __builtin_ctz(word);
     word &= word - 1;
-    uint32_t L = static_cast<uint32_t>(w * 32 + b);
     int32_t yv[kMaxD];
-    for (int j = cout.D - 1; j >= 0; --j) {
-      yv[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
-      L /= static_cast<uint32_t>(E.e[j]);
+    for (int j = 0; j < cout.D; ++j) yv[j] = y0[j];
+    yv[cout.D - 1] += b;
+    for (int j = cout.D - 1; j > 0 && yv[j] >= E.e[j]; --j) {
+      yv[j - 1] += yv[j] / E.e[j];
+      yv[j] %= E.e[j];
     }
-    for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
+    if (cout.D == 4) {
+      reinterpret_cast<int4*>(out_coords)[rank] = make_int4(yv[0], yv[1], yv[2], yv[3]);
+    } else {
+      for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
+    }
     if (out_keys) out_keys[rank] = pack_site(cout, yv);
     ++rank;
   }
