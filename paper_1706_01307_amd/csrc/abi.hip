@@ -248,7 +248,8 @@ static int build_impl(int kind, int D, const int32_t* coords, int64_t N,
   };
   rb->hdr = reinterpret_cast<DeviceHeader*>(take(256));
   rb->n_in_dev = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(rb->hdr) + 128);
-  if (in_count) copy_in_count(rb);
+  // (with rows, the input scatter of the grid build copies the count)
+  if (in_count && N == 0) copy_in_count(rb);
   rb->out_coords = reinterpret_cast<int32_t*>(take(n_cap * D * 4));
   rb->gmap = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->gstride) * 4));
   rb->blk_cnt = reinterpret_cast<int32_t*>(take(Kz * static_cast<size_t>(rb->nblk) * 4 * 2));

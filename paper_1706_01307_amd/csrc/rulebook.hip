@@ -614,8 +614,10 @@ template <bool CAS>
 __global__ __launch_bounds__(kBlock) void k_grid_scatter(
     const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
     GridGeom g, uint32_t* __restrict__ grid, int32_t* __restrict__ copy_out, Codec ckey,
-    uint64_t* __restrict__ keys_out, uint32_t* __restrict__ status) {
+    uint64_t* __restrict__ keys_out, uint32_t* __restrict__ status,
+    int64_t* __restrict__ count_copy) {
   const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (count_copy && r == 0) *count_copy = *count;   // the book's own copy of the row count
   if (r >= N || (count && r >= *count)) return;
   int32_t x[kMaxD];
   bool ok = true;
@@ -1181,8 +1183,10 @@ void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
                          uint64_t* keys_out, bool cas, int64_t init_n = -1) {
   launch_zero(b.grid, cells, rb->stream, init_n >= 0 ? rb->hdr : nullptr, init_n);
   auto kern = cas ? k_grid_scatter<true> : k_grid_scatter<false>;
+  // a book on another book's outputs keeps its own copy of their count
+  int64_t* cc = count && count == rb->in_count ? rb->n_in_dev : nullptr;
   kern<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out, ckey,
-                                               keys_out, &rb->hdr->status);
+                                               keys_out, &rb->hdr->status, cc);
 }
 
 // Z-order schedule from the grid; also sets n_out to the number of occupied
