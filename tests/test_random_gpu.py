@@ -52,3 +52,38 @@ def test_random_layer(monkeypatch, seed):
     _say(f"[random {seed}] path={path}")
     compare_layer(kind, c, size, f, s, ci, co, dtype=dtype, out_dtype=out_dtype, seed=seed,
                   what=f"random {seed}")
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_fused_forward(seed):
+    """The forward with a random subset of the block epilogue (scale, shift,
+    residual, ReLU) fused, on random layers."""
+    import oracle
+    from paper_1706_01307_amd import inputs
+    from tests.test_ops_gpu import _dev, _feats, _odt
+    from tests.test_parity_gpu import RTOL_BF16, RTOL_F32, _t, _to_np, check_features
+    kind, c, size, f, s, ci, co, dtype, out_dtype, path = _case(seed + 500)
+    rng = np.random.default_rng(seed)
+    use_s, use_b, use_r, relu = (bool(v) for v in rng.integers(0, 2, size=4))
+    rb = spc.build_rulebook(kind, _t(c), size, f, s)
+    ref = oracle.Rulebook(kind, c, size, f, s)
+    K = ref.K
+    x = _feats(len(c), ci, dtype, 11 * seed + 1)
+    wf = inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci), seed=11 * seed + 2)
+    w = inputs.to_bf16_bits(wf) if dtype == "bf16" else wf
+    scale = inputs.normal_f32((co,), std=1.0, seed=11 * seed + 3)
+    shift = inputs.normal_f32((co,), std=0.5, seed=11 * seed + 4)
+    res = _feats(ref.n_out, co, out_dtype, 11 * seed + 5)
+    _say(f"[random fused {seed}] kind={kind} N={len(c)} f={f} s={s} C={ci}->{co} {dtype}->"
+         f"{out_dtype} parts={use_s, use_b, use_r, relu}")
+    odt = torch.bfloat16 if out_dtype == "bf16" else torch.float32
+    y = spc.forward_fused(rb, _dev(x, dtype), _dev(w, dtype),
+                          scale=_t(scale) if use_s else None, shift=_t(shift) if use_b else None,
+                          residual=_dev(res, out_dtype) if use_r else None, relu=relu,
+                          out_dtype=odt)
+    y64, absb = ref.forward(x, w, None, in_dt=_odt(dtype))
+    zo, bound = oracle.fused_epilogue(y64, absb, scale if use_s else None,
+                                      shift if use_b else None, res if use_r else None,
+                                      relu, _odt(out_dtype))
+    rtol = RTOL_F32 if dtype == "f32" and out_dtype == "f32" else RTOL_BF16
+    check_features(_to_np(y), zo, bound, rtol, "fused")
