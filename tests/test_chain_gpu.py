@@ -113,3 +113,30 @@ def test_chained_build_argument_errors():
     assert lib.spconv_build_rulebook_on(sc.handle, 1, f.ctypes.data, one.ctypes.data,
                                         spc.BUILD_TRANSPOSE, None, ctypes.byref(h)) == spc.EINVAL
     assert h.value is None
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_chains(seed):
+    """Random 4-D grids, densities and filters: a book chained on an SC
+    book equals the book built from the exported sites."""
+    from tests import dense_ref
+    rng = np.random.default_rng(700 + seed)
+    size = [int(rng.integers(1, 4))] + [int(rng.choice([2, 4, 7, 16, 33])) for _ in range(3)]
+    c = dense_ref.random_sites(rng, size, float(rng.choice([0.05, 0.3, 0.9])))
+    if len(c) == 0:
+        c = np.zeros((1, 4), np.int32)
+    fp = [1] + [int(rng.integers(1, min(3, e) + 1)) for e in size[1:]]
+    sp = [1] + [int(rng.integers(1, 3)) for _ in range(3)]
+    parent = spc.build_rulebook(spc.SC, _t(c), size, fp, sp, sync=False)
+    if rng.random() < 0.5:
+        kind, f, s = spc.VSC, [1] + [int(rng.choice([1, 3])) for _ in range(3)], None
+    else:
+        kind, f, s = spc.SC, [1, 2, 2, 2], [1, 2, 2, 2]
+    osz = parent.out_spatial_size
+    if kind == spc.SC and any(e < 2 for e in osz[1:]):
+        kind, f, s = spc.VSC, [1, 3, 3, 3], None
+    rb = spc.build_rulebook_on(parent, kind, f, s, sync=False)
+    _say(f"[random chain {seed}] size={size} fp={fp} sp={sp} -> kind={kind} f={f}")
+    oc, _ = parent.export()
+    ref = spc.build_rulebook(kind, oc, osz, f, s)
+    _same_book(rb, ref)
