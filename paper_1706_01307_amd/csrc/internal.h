@@ -168,7 +168,7 @@ struct spconv_rulebook_s {
   int64_t K;
   int32_t size[spc::kMaxD], f[spc::kMaxD], s[spc::kMaxD], out_size[spc::kMaxD];
   hipStream_t stream;          // build stream (owns the allocation)
-  spc::Allocator al;           // the allocator of this build (and its release)
+  spc::Allocator al;           // the allocator the book was built with (and releases through)
   void* mem;                   // one stream-ordered allocation
   size_t mem_bytes;
   // carved device pointers
