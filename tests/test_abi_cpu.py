@@ -134,3 +134,22 @@ def test_block_cache_entry_points_without_a_device():
     assert n.value == 0
     assert lib.spconv_release_cached_memory(None) == _lib.OK
     assert lib.spconv_memory_stats(-1, None, None) in (_lib.EINVAL, _lib.EHIP)
+
+
+def test_product_path_does_not_load_the_oracle():
+    """The package never imports the oracle (which is test infrastructure)."""
+    import subprocess
+    import sys
+    code = ("import sys; import paper_1706_01307_amd as spc; from paper_1706_01307_amd import "
+            "_lib, inputs; _lib.load(); print('oracle' in sys.modules)")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "False"
+    pkg = os.path.join(ROOT, "paper_1706_01307_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for name in files:
+            if name.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, name)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, re.M), name
+                assert "oracle.h" not in text and "oracle.cpp" not in text, name
