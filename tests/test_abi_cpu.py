@@ -153,3 +153,17 @@ def test_product_path_does_not_load_the_oracle():
                 text = open(os.path.join(dirpath, name)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle\b", text, re.M), name
                 assert "oracle.h" not in text and "oracle.cpp" not in text, name
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """Without the built library every entry point raises: no fallback."""
+    import subprocess
+    import sys
+    code = ("import paper_1706_01307_amd._lib as L; L.LIB_PATH = %r; L._lib = None\n"
+            "import paper_1706_01307_amd as spc\n"
+            "try:\n    spc.release_cached_memory()\nexcept ImportError as e:\n"
+            "    print('raised', 'missing' in str(e))\n" % str(tmp_path / "libspconv.so"))
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "raised True"
