@@ -35,7 +35,9 @@
  *          contiguous, row-major, 16-byte aligned.  Host pointers are marked
  *          "host".  A rule book owns its device memory (taken on the build
  *          stream from the library's allocator, see spconv_set_allocator)
- *          until spconv_rulebook_destroy.
+ *          until spconv_rulebook_destroy.  A feature pointer whose row count
+ *          is zero may be NULL (an SC book's output rows count as zero only
+ *          once the book is synchronised; before, their bound counts).
  * Streams. `stream` is a hipStream_t passed as void*; NULL is the null
  *          stream.  All work is enqueued on it.
  * Errors.  Every call returns a spconv_status; nothing is printed and

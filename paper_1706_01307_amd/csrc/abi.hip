@@ -379,6 +379,11 @@ int spconv_rulebook_out_coords(spconv_rulebook rb, const int32_t** coords) {
 
 // Argument checks shared by the forward entry points; with check_only nothing
 // is launched.
+// Output rows of a book as far as the host knows them: the count once the
+// book is synchronised, its bound before.  A pointer to rows that turn out to
+// be none may be NULL.
+static int64_t out_rows(spconv_rulebook rb) { return rb->synced ? rb->n_out : rb->n_cap; }
+
 static int forward_common(spconv_rulebook rb, int kind, int in_dt, const void* x, const void* w,
                           const float* bias, int out_dt, void* y, int C_in, int C_out,
                           void* stream, bool check_only = false) {
@@ -387,7 +392,7 @@ static int forward_common(spconv_rulebook rb, int kind, int in_dt, const void* x
       (out_dt != SPCONV_F32 && out_dt != SPCONV_BF16))
     return SPCONV_EINVAL;
   if (C_in < 1 || C_out < 1) return SPCONV_EINVAL;
-  if (rb->n_cap > 0 && (!y || !w || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
+  if (out_rows(rb) > 0 && (!y || !w || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
   const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w) |
                        reinterpret_cast<uintptr_t>(y);
   if ((al & 15) || (reinterpret_cast<uintptr_t>(bias) & 3)) return SPCONV_EINVAL;
@@ -439,7 +444,7 @@ int spconv_pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, voi
                         void* stream) {
   if (!rb || rb->kind != SPCONV_SC || !dtype_ok(dt) || C < 1) return SPCONV_EINVAL;
   if (mode != SPCONV_POOL_MAX && mode != SPCONV_POOL_AVG) return SPCONV_EINVAL;
-  if (rb->n_cap > 0 && (!y || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
+  if (out_rows(rb) > 0 && (!y || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
   if (misaligned(x) || misaligned(y)) return SPCONV_EINVAL;
   return pool_forward(rb, mode, dt, x, y, C, static_cast<hipStream_t>(stream));
 }
@@ -449,7 +454,7 @@ int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
                       void* stream) {
   if (!rb || rb->kind != SPCONV_SC || !rb->t_gmap) return SPCONV_EINVAL;
   if (!dtype_ok(in_dt) || !dtype_ok(out_dt) || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
-  if (rb->n_in > 0 && (!y || !w || (rb->n_cap > 0 && !x))) return SPCONV_EINVAL;
+  if (rb->n_in > 0 && (!y || !w || (out_rows(rb) > 0 && !x))) return SPCONV_EINVAL;
   if (misaligned(x) || misaligned(w) || misaligned(y) ||
       (reinterpret_cast<uintptr_t>(bias) & 3))
     return SPCONV_EINVAL;
@@ -492,7 +497,10 @@ int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, con
   const int vs = data_grad_view(rb, op, &v, &wmode);
   if (vs != SPCONV_OK) return vs;
   if (!dtype_ok(dt) || !dtype_ok(out_dt) || C_in < 1 || C_out < 1) return SPCONV_EINVAL;
-  if (v.n_cap > 0 && (!dx || !w || (v.n_src > 0 && !dy))) return SPCONV_EINVAL;
+  // rows of dx and dy: VSC both n_in; SC dx n_in, dy n_out; DC the reverse
+  const int64_t dst = op == SPCONV_OP_DC ? out_rows(rb) : rb->n_in;
+  const int64_t src = op == SPCONV_OP_SC ? out_rows(rb) : rb->n_in;
+  if (dst > 0 && (!dx || !w || (src > 0 && !dy))) return SPCONV_EINVAL;
   if (misaligned(dy) || misaligned(w) || misaligned(dx)) return SPCONV_EINVAL;
   // the kernels' input channels are the layer's output channels
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -518,12 +526,15 @@ int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, co
   if (op == SPCONV_OP_DC ? rb->kind != SPCONV_SC : op != rb->kind) return SPCONV_EINVAL;
   if (!workspace || workspace_bytes < backward_weight_workspace(rb, C_in, C_out, op))
     return SPCONV_EINVAL;
-  if (rb->n_cap > 0 && (!x || !dy)) return SPCONV_EINVAL;
   if (misaligned(x) || misaligned(dy) || misaligned(workspace) ||
       (reinterpret_cast<uintptr_t>(dw) & 3) || (reinterpret_cast<uintptr_t>(db) & 3))
     return SPCONV_EINVAL;
   const int st = sync_rulebook(rb);    // the bias gradient needs n_out on the host
   if (st != SPCONV_OK) return st;
+  // rows of x and dy: VSC both n_in; SC x n_in, dy n_out; DC the reverse
+  const int64_t xr = op == SPCONV_OP_DC ? rb->n_out : rb->n_in;
+  const int64_t gr = op == SPCONV_OP_SC ? rb->n_out : rb->n_in;
+  if ((xr > 0 && !x) || (gr > 0 && !dy)) return SPCONV_EINVAL;
   return backward_weight(rb, op, dt, x, dy, dw, db, C_in, C_out, workspace,
                          static_cast<hipStream_t>(stream));
 }

@@ -25,6 +25,7 @@ int forward_view(const FwdView& v, int wmode, int in_dt, const void* x, const vo
                  hipStream_t stream, const Epilogue& epi) {
   if (v.n_cap == 0) return SPCONV_OK;
   FwdCall c{v, x, 0u, w, bias, y, C_out, stream, epi};
+  if (!x) c.v.n_src = 0;   // no source rows (the map then names none): every gather reads 0
   bool done = false;
   switch (wmode) {
     case 0: done = forward_run_w0(c, in_dt, out_dt, C_in); break;

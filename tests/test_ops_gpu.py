@@ -414,3 +414,42 @@ def test_allocator_failure_is_enomem_without_leaks(fail_at):
         spc.set_allocator(None, None)
     rb = spc.build_rulebook(spc.SC, _t(coords), size, [1, 2, 2], [1, 2, 2], transpose=True)
     assert rb.n_out > 0                                   # the default is back
+
+
+@pytest.mark.parametrize("sites,size,f,s", [
+    ([[0, 4]], [1, 5], [1, 2], [1, 2]),              # f = s, the site past the last window
+    ([[0, 1], [0, 2], [0, 4]], [1, 7], [1, 1], [1, 3]),  # no site on a stride multiple
+])
+def test_sc_book_without_outputs(sites, size, f, s):
+    """An SC book whose inputs feed no output: every op accepts the empty
+    tensors (NULL pointers below the ABI) and matches the oracle."""
+    coords = np.asarray(sites, np.int32)
+    rb = spc.build_rulebook(spc.SC, _t(coords), size, f, s, transpose=True)
+    ref = oracle.Rulebook(oracle.SC, coords, size, f, s)
+    assert rb.n_out == 0 == ref.n_out and rb.n_in == len(coords)
+    K, ci, co = ref.K, 8, 16
+    x_in = _feats(len(coords), ci, "f32", 1)
+    w = inputs.normal_f32((K, ci, co), std=0.5, seed=2)
+    b = inputs.normal_f32((co,), std=0.1, seed=3)
+    empty_ci = torch.zeros((0, ci), device="cuda")
+    empty_co = torch.zeros((0, co), device="cuda")
+    assert spc.sc_forward(rb, _t(x_in), _t(w), _t(b)).shape == (0, co)
+    assert spc.pool_forward(rb, _t(x_in), spc.POOL_MAX).shape == (0, ci)
+    # DC from no coarse rows: the bias at every fine site
+    y = spc.dc_forward(rb, empty_ci, _t(w), _t(b))
+    yo, _ = ref.dc_forward(np.zeros((0, ci), np.float32), w, b, in_dt=oracle.F32)
+    assert y.shape == (len(coords), co)
+    np.testing.assert_array_equal(y.cpu().numpy(), yo.astype(np.float32))
+    # SC input gradient from no output rows: zeros
+    dx = spc.backward_data(rb, spc.OP_SC, empty_co, _t(w))
+    assert dx.shape == (len(coords), ci) and not dx.abs().sum().item()
+    # SC weight and bias gradients: zeros
+    dw, db = spc.backward_weight(rb, spc.OP_SC, _t(x_in), empty_co, ci, co)
+    assert not dw.abs().sum().item() and not db.abs().sum().item()
+    # DC gradients: dy at the fine sites, no coarse rows
+    dy = _feats(len(coords), co, "f32", 4)
+    dw, db = spc.backward_weight(rb, spc.OP_DC, empty_ci, _t(dy), ci, co)
+    dwo, dbo, aw, ab = ref.backward_weight(oracle.DC, np.zeros((0, ci), np.float32), dy, ci, co,
+                                           oracle.F32)
+    check_features(dw.cpu().numpy(), dwo, aw, RTOL_GRAD, "dw")
+    check_features(db.cpu().numpy(), dbo, ab, RTOL_GRAD, "db")
