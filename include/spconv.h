@@ -264,7 +264,9 @@ int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C
  *   workspace device scratch of at least spconv_backward_weight_workspace
  *             bytes, owned by the caller (its contents are overwritten)
  * Each R_i is summed in fixed chunks, and the chunks in ascending order:
- * deterministic, no atomics.  Asynchronous; allocates nothing.
+ * deterministic, no atomics.  Allocates nothing; asynchronous, except that
+ * a book built with SPCONV_BUILD_ASYNC is waited for once here (the bias
+ * gradient needs its output count on the host).
  * Errors: EINVAL (op / book mismatch, dtype, NULL, workspace too small). */
 int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy,
                            float* dw, float* db, int C_in, int C_out, void* workspace,
