@@ -230,7 +230,9 @@ int spconv_pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, voi
  *   x       device [n_out][C_in] (features on the SC output sites)
  *   w       device [K][C_in][C_out]; bias fp32 [C_out] or NULL
  *   y       device [n_in][C_out] (rows in the SC input order), overwritten
- * Accumulation, rounding and determinism as spconv_vsc_forward.
+ * Accumulation, rounding and determinism as spconv_vsc_forward.  For
+ * f = s the first such call on a book reads its pair offsets once (a wait);
+ * later calls are asynchronous.
  * Errors: EINVAL (kind, no transposed book, dtype, C < 1, NULL). */
 int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
                       const float* bias, int out_dt, void* y, int C_in, int C_out,
@@ -244,7 +246,9 @@ int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
  *                                 dy [n_out][C_out] -> dx [n_in][C_in]
  *   op SPCONV_OP_DC  (SC book):   dy [n_in][C_out]  -> dx [n_out][C_in]
  * dt is the dtype of dy and w, out_dt that of dx.  fp32 accumulation in a
- * fixed order, rounded once; deterministic; asynchronous; allocates nothing.
+ * fixed order, rounded once; deterministic; allocates nothing; asynchronous
+ * (for op SC with f = s the first such call on a book reads its pair offsets
+ * once, as spconv_dc_forward).
  * Errors: EINVAL (op / book mismatch, missing transposed book, dtype, NULL). */
 int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, const void* w,
                          int out_dt, void* dx, int C_in, int C_out, void* stream);
