@@ -32,8 +32,9 @@ F32, BF16 = 0, 1
 
 
 def build():
-    """Compile oracle.cpp into liboracle.so (plain g++, host code only)."""
-    cmd = ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-o", _LIB + ".tmp",
+    """Compile oracle.cpp into liboracle.so (plain g++, host code only; its
+    loops over output rows run on OpenMP threads)."""
+    cmd = ["g++", "-O2", "-std=c++17", "-fopenmp", "-shared", "-fPIC", "-o", _LIB + ".tmp",
            _SRC]
     subprocess.run(cmd, check=True)
     os.replace(_LIB + ".tmp", _LIB)
@@ -72,8 +73,16 @@ def _load():
     lib.ref_round.restype = I32
     lib.ref_free.argtypes = [P]
     lib.ref_free.restype = None
+    lib.ref_set_threads.argtypes = [I32]
+    lib.ref_set_threads.restype = I32
     _lib = lib
     return lib
+
+
+def set_threads(n):
+    """Threads for the oracle's parallel loops (n <= 0 keeps the current
+    setting); returns the count in effect.  Results do not depend on it."""
+    return int(_load().ref_set_threads(int(n)))
 
 
 def _ptr(a):

@@ -37,9 +37,8 @@
 //   * W^i multiplies the input at s*y + i (SC) or y + i - (f-1)/2 (VSC): a
 //     cross-correlation, offsets flattened row-major (last dimension fastest);
 //   * SC output rows are numbered in lexicographic order of the output site;
-//   * pairs inside R_i are ordered along the Z-order (Morton) curve of their
-//     output site: sample index first, then the coordinates' bits level by
-//     level from the most significant, dimension 1 first within a level;
+//   * pairs inside R_i are ordered by ascending output row (each output row
+//     has at most one input per offset, so this is a total order);
 //   * the bias (optional) is added once at every active output site;
 //   * accumulation is in double, rounded once to the output type (RNE);
 //   * MP and AP run on an SC rule book; f^-d is 1 / prod_j f_j over the
@@ -54,6 +53,10 @@
 #include <map>
 #include <set>
 #include <vector>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 namespace {
 
@@ -82,17 +85,6 @@ double bf16_to_double(uint16_t b) {
 double load(int dt, const void* p, int64_t idx) {
   if (dt == F32) return static_cast<double>(static_cast<const float*>(p)[idx]);
   return bf16_to_double(static_cast<const uint16_t*>(p)[idx]);
-}
-
-// Z-order comparison of two sites (see the readings above).
-bool zorder_less(const Site& a, const Site& b, int D) {
-  if (a[0] != b[0]) return a[0] < b[0];
-  for (int L = 15; L >= 0; --L)
-    for (int j = 1; j < D; ++j) {
-      const int ba = (a[j] >> L) & 1, bb = (b[j] >> L) & 1;
-      if (ba != bb) return ba < bb;
-    }
-  return false;
 }
 
 // Offset index i (flattened, last dimension fastest) -> per-dimension offset.
@@ -192,26 +184,28 @@ int ref_build(int kind, int D, const int32_t* coords, int64_t N,
   for (int64_t r = 0; r < rb->n_out; ++r)
     for (int j = 0; j < D; ++j) rb->out_coords[r * D + j] = out_sites[r][j];
 
-  // Rule book: for every offset i and every output row y, visited in Z-order
-  // of the output site, the input site feeding y through W^i, if active.
-  std::vector<int64_t> visit(rb->n_out);
-  for (int64_t y = 0; y < rb->n_out; ++y) visit[y] = y;
-  std::sort(visit.begin(), visit.end(), [&](int64_t a, int64_t b) {
-    return zorder_less(out_sites[a], out_sites[b], D);
-  });
+  // Rule book: for every offset i and every output row y, in ascending order,
+  // the input site feeding y through W^i, if active.  The lookups of one
+  // offset are independent read-only map queries (run in parallel over y);
+  // the list is then appended in row order, so R_i does not depend on the
+  // thread count.
   rb->R.resize(rb->K);
-  std::vector<int32_t> o(D);
+  std::vector<int64_t> found(rb->n_out);
   for (int64_t i = 0; i < rb->K; ++i) {
-    unflatten(i, D, rb->f, o.data());
-    for (int64_t y : visit) {
+    int32_t o[4] = {0, 0, 0, 0};
+    unflatten(i, D, rb->f, o);
+#pragma omp parallel for schedule(static)
+    for (int64_t y = 0; y < rb->n_out; ++y) {
       Site x{0, 0, 0, 0};
       for (int j = 0; j < D; ++j) {
         if (kind == VSC) x[j] = out_sites[y][j] + o[j] - (f[j] - 1) / 2;
         else x[j] = s[j] * out_sites[y][j] + o[j];
       }
       auto it = in_map.find(x);
-      if (it != in_map.end()) rb->R[i].push_back({it->second, y});
+      found[y] = it == in_map.end() ? -1 : it->second;
     }
+    for (int64_t y = 0; y < rb->n_out; ++y)
+      if (found[y] >= 0) rb->R[i].push_back({found[y], y});
   }
   *out = rb;
   return OK;
@@ -256,6 +250,66 @@ int ref_export(void* h, int32_t* out_coords, int32_t* pairs) {
   return OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// For every offset i and output row y, the input row R_i pairs with y, or -1
+// (each output row has at most one input per offset).
+std::vector<int64_t> source_rows(const Rulebook& rb) {
+  std::vector<int64_t> src(static_cast<size_t>(rb.K * rb.n_out), -1);
+  for (int64_t i = 0; i < rb.K; ++i)
+    for (const auto& pr : rb.R[i]) src[i * rb.n_out + pr[1]] = pr[0];
+  return src;
+}
+
+// The forward multiply-add of Section 4 for one output row yo: start from the
+// bias, then add input row times W^i for every offset i in ascending order,
+// input plane c in ascending order, all in double.
+void forward_row(int64_t yo, const int64_t* src, int64_t K, int64_t n_out, int in_dt,
+                 const void* x, const void* w, const float* bias, int C_in, int C_out,
+                 double* y, double* absb, const double* x_absb) {
+  double* yr = y + yo * C_out;
+  double* ar = absb ? absb + yo * C_out : nullptr;
+  for (int n = 0; n < C_out; ++n) {
+    const double b = bias ? static_cast<double>(bias[n]) : 0.0;
+    yr[n] = b;
+    if (ar) ar[n] = std::fabs(b);
+  }
+  for (int64_t i = 0; i < K; ++i) {
+    const int64_t xi = src[i * n_out + yo];
+    if (xi < 0) continue;
+    for (int c = 0; c < C_in; ++c) {
+      const double xv = load(in_dt, x, xi * C_in + c);
+      const double xa = x_absb ? x_absb[xi * C_in + c] : std::fabs(xv);
+      for (int n = 0; n < C_out; ++n) {
+        const double wv = load(in_dt, w, (i * C_in + c) * C_out + n);
+        yr[n] += xv * wv;
+        if (ar) ar[n] += xa * std::fabs(wv);
+      }
+    }
+  }
+}
+
+// The forward for the output rows with rows_mask[y] != 0 (every row when
+// rows_mask is NULL).  Rows are independent and each row's sum has one fixed
+// order, so the result does not depend on how many threads share the rows.
+void forward_impl(const Rulebook& rb, int in_dt, const void* x, const void* w,
+                  const float* bias, int C_in, int C_out, const uint8_t* rows_mask,
+                  double* y, double* absb, const double* x_absb) {
+  const std::vector<int64_t> src = source_rows(rb);
+  const int64_t K = rb.K, n_out = rb.n_out;
+#pragma omp parallel for schedule(dynamic, 256)
+  for (int64_t yo = 0; yo < n_out; ++yo) {
+    if (rows_mask && !rows_mask[yo]) continue;
+    forward_row(yo, src.data(), K, n_out, in_dt, x, w, bias, C_in, C_out, y, absb, x_absb);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
 // Forward pass.  x: host [n_in][C_in] of in_dt (0 = fp32, 1 = bf16 bits);
 // w: host [K][C_in][C_out] of in_dt; bias: host fp32 [C_out] or NULL.
 // y: host double [n_out][C_out], the exact-as-double result.
@@ -267,26 +321,8 @@ int ref_forward(void* h, int in_dt, const void* x, const void* w,
                 double* absb, const double* x_absb) {
   if (!h || C_in < 1 || C_out < 1 || (in_dt != F32 && in_dt != BF16))
     return EINVAL_;
-  auto* rb = static_cast<Rulebook*>(h);
-  for (int64_t r = 0; r < rb->n_out; ++r)
-    for (int n = 0; n < C_out; ++n) {
-      double b = bias ? static_cast<double>(bias[n]) : 0.0;
-      y[r * C_out + n] = b;
-      if (absb) absb[r * C_out + n] = std::fabs(b);
-    }
-  for (int64_t i = 0; i < rb->K; ++i)
-    for (const auto& pr : rb->R[i]) {
-      const int64_t xi = pr[0], yo = pr[1];
-      for (int c = 0; c < C_in; ++c) {
-        const double xv = load(in_dt, x, xi * C_in + c);
-        const double xa = x_absb ? x_absb[xi * C_in + c] : std::fabs(xv);
-        for (int n = 0; n < C_out; ++n) {
-          const double wv = load(in_dt, w, (i * C_in + c) * C_out + n);
-          y[yo * C_out + n] += xv * wv;
-          if (absb) absb[yo * C_out + n] += xa * std::fabs(wv);
-        }
-      }
-    }
+  forward_impl(*static_cast<Rulebook*>(h), in_dt, x, w, bias, C_in, C_out, nullptr, y, absb,
+               x_absb);
   return OK;
 }
 
@@ -296,32 +332,24 @@ int ref_forward(void* h, int in_dt, const void* x, const void* w,
 int ref_forward_rows(void* h, int in_dt, const void* x, const void* w,
                      const float* bias, int C_in, int C_out,
                      const uint8_t* rows_mask, double* y, double* absb) {
-  if (!h || !rows_mask || C_in < 1 || C_out < 1 ||
+  if (!h || !rows_mask || !absb || C_in < 1 || C_out < 1 ||
       (in_dt != F32 && in_dt != BF16))
     return EINVAL_;
-  auto* rb = static_cast<Rulebook*>(h);
-  for (int64_t r = 0; r < rb->n_out; ++r) {
-    if (!rows_mask[r]) continue;
-    for (int n = 0; n < C_out; ++n) {
-      double b = bias ? static_cast<double>(bias[n]) : 0.0;
-      y[r * C_out + n] = b;
-      absb[r * C_out + n] = std::fabs(b);
-    }
-  }
-  for (int64_t i = 0; i < rb->K; ++i)
-    for (const auto& pr : rb->R[i]) {
-      const int64_t xi = pr[0], yo = pr[1];
-      if (!rows_mask[yo]) continue;
-      for (int c = 0; c < C_in; ++c) {
-        const double xv = load(in_dt, x, xi * C_in + c);
-        for (int n = 0; n < C_out; ++n) {
-          const double wv = load(in_dt, w, (i * C_in + c) * C_out + n);
-          y[yo * C_out + n] += xv * wv;
-          absb[yo * C_out + n] += std::fabs(xv) * std::fabs(wv);
-        }
-      }
-    }
+  forward_impl(*static_cast<Rulebook*>(h), in_dt, x, w, bias, C_in, C_out, rows_mask, y, absb,
+               nullptr);
   return OK;
+}
+
+// Threads the parallel loops above may use (0 or less: the OpenMP default).
+// Returns the count now in effect (1 when built without OpenMP).
+int ref_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
 }
 
 // Sparse pooling on an SC rule book.
@@ -448,21 +476,27 @@ int ref_backward_weight(void* h, int op, int dt, const void* x, const void* dy, 
     dw[k] = 0.0;
     if (absb_w) absb_w[k] = 0.0;
   }
-  for (int64_t i = 0; i < rb->K; ++i) {
-    if (omask && !omask[i]) continue;
-    for (const auto& pr : rb->R[i]) {
-      const int64_t xr = op == DC ? pr[1] : pr[0];
-      const int64_t gr = op == DC ? pr[0] : pr[1];
-      for (int c = 0; c < C_in; ++c) {
+  // Every entry (i, c, n) sums over the pairs of R_i in list order; the
+  // entries of different (i, c) are independent and run in parallel, so the
+  // result does not depend on the thread count.
+  const int64_t K = rb->K;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+  for (int64_t i = 0; i < K; ++i)
+    for (int c = 0; c < C_in; ++c) {
+      if (omask && !omask[i]) continue;
+      double* dwr = dw + (i * C_in + c) * C_out;
+      double* awr = absb_w ? absb_w + (i * C_in + c) * C_out : nullptr;
+      for (const auto& pr : rb->R[i]) {
+        const int64_t xr = op == DC ? pr[1] : pr[0];
+        const int64_t gr = op == DC ? pr[0] : pr[1];
         const double xv = load(dt, x, xr * C_in + c);
         for (int n = 0; n < C_out; ++n) {
           const double g = load(dt, dy, gr * C_out + n);
-          dw[(i * C_in + c) * C_out + n] += xv * g;
-          if (absb_w) absb_w[(i * C_in + c) * C_out + n] += std::fabs(xv) * std::fabs(g);
+          dwr[n] += xv * g;
+          if (awr) awr[n] += std::fabs(xv) * std::fabs(g);
         }
       }
     }
-  }
   if (db) {
     const int64_t out_rows = op == DC ? rb->n_in : rb->n_out;
     for (int n = 0; n < C_out; ++n) {

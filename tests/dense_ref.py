@@ -99,7 +99,7 @@ def zorder(sites):
 
 def rulebook_dense(kind, coords, size, f, s, out_coords):
     """Per-offset (input row, output row) lists from a dense row grid, each
-    list ordered along the Z-order curve of the output site."""
+    list ordered by ascending output row."""
     size = list(size)
     D = len(size)
     rg = row_grid(coords, size)
@@ -112,8 +112,7 @@ def rulebook_dense(kind, coords, size, f, s, out_coords):
         inb = np.all((x >= 0) & (x < np.array(size)), axis=1)
         rows = np.full(len(out_coords), -1, np.int64)
         rows[inb] = rg[tuple(x[inb].T)]
-        y = zorder(out_coords)
-        y = y[rows[y] >= 0]
+        y = np.nonzero(rows >= 0)[0]
         R.append(np.stack([rows[y], y], axis=1).astype(np.int32))
     return R
 

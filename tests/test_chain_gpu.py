@@ -1,7 +1,10 @@
 """Rule books built on the output sites of an SC rule book (a chain of
-levels) without the host waiting: pair for pair and bit for bit the books
-built from the exported output sites, also for the hash-table path (which
-reads the count on the host) and a three-level chain."""
+levels) without the host waiting.  Each chained book is compared with the
+oracle's book built on the oracle's own SC output sites (bit for bit, pairs
+canonicalised per R_i) and its forward with the oracle's forward; it is also
+compared with the library's book built from the exported output sites, also
+for the hash-table path (which reads the count on the host) and a
+three-level chain."""
 import sys
 
 import numpy as np
@@ -9,9 +12,11 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
+import oracle  # noqa: E402
 import paper_1706_01307_amd as spc  # noqa: E402
 from paper_1706_01307_amd import inputs  # noqa: E402
-from tests.test_parity_gpu import _bf16_tensor, _t  # noqa: E402
+from tests.rb_check import check_rulebook  # noqa: E402
+from tests.test_parity_gpu import RTOL_BF16, _bf16_tensor, _t, _to_np, check_features  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -27,13 +32,33 @@ def _say(*a):
     sys.stdout.flush()
 
 
+def _feat_bits(n, C, seed):
+    return inputs.to_bf16_bits(inputs.normal_f32((n, C), seed=seed))
+
+
+def _weight_bits(K, ci, co, seed):
+    return inputs.to_bf16_bits(inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci),
+                                                 seed=seed))
+
+
 def _feats(n, C, seed):
-    return _bf16_tensor(inputs.to_bf16_bits(inputs.normal_f32((n, C), seed=seed)))
+    return _bf16_tensor(_feat_bits(n, C, seed))
 
 
 def _weights(K, ci, co, seed):
-    return _bf16_tensor(inputs.to_bf16_bits(
-        inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci), seed=seed)))
+    return _bf16_tensor(_weight_bits(K, ci, co, seed))
+
+
+def _oracle_kind(kind):
+    return oracle.VSC if kind == spc.VSC else oracle.SC
+
+
+def _same_as_oracle(rb, ref):
+    """A (chained) GPU book against an oracle.Rulebook."""
+    assert rb.status() == spc.OK
+    assert rb.n_in == ref.n_in and rb.n_out == ref.n_out
+    oc, pr = rb.export()
+    check_rulebook(oc.cpu().numpy(), pr.cpu().numpy(), rb.pair_off, ref)
 
 
 def _same_book(rb, ref):
@@ -68,6 +93,14 @@ def test_chained_book_equals_book_on_exported_sites(monkeypatch, path, kind, f, 
     w = _weights(K, 32, 32, 32)
     y = _forward(rb, x, w, 32, nb_out)
     _say(f"[chain] {path} kind={kind} f={f} parent n_out={parent.n_out} bounds={nb_in},{nb_out}")
+    # the oracle's chain: its own SC output sites feed its next book
+    o_parent = oracle.Rulebook(oracle.SC, c, size, [1, 2, 2, 2], [1, 2, 2, 2])
+    o_book = oracle.Rulebook(_oracle_kind(kind), o_parent.out_coords, o_parent.out_size, f, s)
+    _same_as_oracle(rb, o_book)
+    yo, absb = o_book.forward(_feat_bits(nb_in, 32, 31)[:o_book.n_in],
+                              _weight_bits(K, 32, 32, 32), None, in_dt=oracle.BF16)
+    check_features(_to_np(y[:o_book.n_out]), yo, absb, RTOL_BF16, "chained forward")
+    # and the library's own book built from the exported sites
     oc, _ = parent.export()
     ref = spc.build_rulebook(kind, oc, parent.out_spatial_size, f, s)
     assert nb_in >= parent.n_out and nb_out >= ref.n_out
@@ -85,7 +118,15 @@ def test_three_level_chain_without_waiting():
     for _ in range(2):
         vsc.append(spc.build_rulebook_on(levels[-1], spc.VSC, [1, 3, 3, 3], sync=False))
         levels.append(spc.build_rulebook_on(levels[-1], spc.SC, f2, f2, sync=False))
-    # now compare every level with books built from exported sites
+    # every level against the oracle's chain on its own output sites
+    o_sites, o_size = c, size
+    for lvl in range(3):
+        o_sc = oracle.Rulebook(oracle.SC, o_sites, o_size, f2, f2)
+        _same_as_oracle(levels[lvl], o_sc)
+        o_sites, o_size = o_sc.out_coords, o_sc.out_size
+        if lvl < 2:
+            _same_as_oracle(vsc[lvl], oracle.Rulebook(oracle.VSC, o_sites, o_size, [1, 3, 3, 3]))
+    # and with the library's books built from exported sites
     sites, sz = _t(c), size
     ref_sc = spc.build_rulebook(spc.SC, sites, sz, f2, f2)
     for lvl in range(3):
@@ -137,6 +178,10 @@ def test_random_chains(seed):
         kind, f, s = spc.VSC, [1, 3, 3, 3], None
     rb = spc.build_rulebook_on(parent, kind, f, s, sync=False)
     _say(f"[random chain {seed}] size={size} fp={fp} sp={sp} -> kind={kind} f={f}")
+    o_parent = oracle.Rulebook(oracle.SC, c, size, fp, sp)
+    _same_as_oracle(parent, o_parent)
+    _same_as_oracle(rb, oracle.Rulebook(_oracle_kind(kind), o_parent.out_coords,
+                                        o_parent.out_size, f, s or [1, 1, 1, 1]))
     oc, _ = parent.export()
     ref = spc.build_rulebook(kind, oc, osz, f, s)
     _same_book(rb, ref)

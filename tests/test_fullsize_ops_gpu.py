@@ -5,11 +5,11 @@ transposed form, preallocated outputs, the same kernels).
 * level 0 of the 4 x 256^3 encoder (1.70 M sites -> 0.51 M through 2^3
   stride 2): MP bit for bit and AP over every output row; DC, the SC input
   gradient and the SC weight and bias gradients over every entry.
-* the 8 x 128^3 headline VSC layer (0.90 M sites, 64 -> 64): sampled rows of
+* the 8 x 128^3 headline VSC layer (0.90 M sites, 64 -> 64): every row of
   the input gradient (a VSC forward with the flipped, transposed weights,
-  an identity pinned on small cases), three of the 27 W^i of the weight
-  gradient and the whole bias gradient, and sampled rows of the forward
-  with the block epilogue fused.
+  an identity pinned on small cases), all 27 W^i of the weight gradient and
+  the whole bias gradient, and every row of the forward with the block
+  epilogue fused.
 """
 import sys
 import time
@@ -26,7 +26,6 @@ from tests.test_parity_gpu import RTOL_BF16, _bf16_tensor, _t, _to_np, check_fea
 
 pytestmark = pytest.mark.gpu
 RTOL_GRAD = 1e-4
-N_SAMPLE_ROWS = 3000
 
 
 def _say(*a):
@@ -103,20 +102,18 @@ def test_fullsize_headline_gradients_and_fused_forward():
     ref = oracle.Rulebook(oracle.VSC, wl.coords, wl.spatial_size, f)
     K, C = 27, 64
     _say(f"[headline] N={N}, books built ({time.time() - t0:.1f}s)")
-    rng = np.random.default_rng(31)
-    rows = np.sort(rng.choice(N, N_SAMPLE_ROWS, replace=False))
 
     w, dy, xv = _wbits(K, C, C, 31), _bits(N, C, 32), _bits(N, C, 33)
     dx = spc.backward_data(rb, spc.OP_VSC, _bf16_tensor(dy), _bf16_tensor(w))
     w_flip = np.ascontiguousarray(w[::-1].transpose(0, 2, 1))
-    dxo, absb = ref.forward_rows(rows, dy, w_flip, None, in_dt=oracle.BF16)
-    check_features(_to_np(dx)[rows], dxo, absb, RTOL_BF16, "VSC dx")
+    dxo, absb = ref.forward(dy, w_flip, None, in_dt=oracle.BF16)
+    check_features(_to_np(dx), dxo, absb, RTOL_BF16, "VSC dx")
+    del dxo, absb
     _say(f"[headline] VSC input gradient ok ({time.time() - t0:.1f}s)")
 
     dw, db = spc.backward_weight(rb, spc.OP_VSC, _bf16_tensor(xv), _bf16_tensor(dy), C, C)
-    sel = [0, 13, 22]
-    dwo, dbo, aw, ab = ref.backward_weight(oracle.VSC, xv, dy, C, C, oracle.BF16, offsets=sel)
-    check_features(dw.cpu().numpy()[sel], dwo[sel], aw[sel], RTOL_GRAD, "VSC dw")
+    dwo, dbo, aw, ab = ref.backward_weight(oracle.VSC, xv, dy, C, C, oracle.BF16)
+    check_features(dw.cpu().numpy(), dwo, aw, RTOL_GRAD, "VSC dw")
     check_features(db.cpu().numpy(), dbo, ab, RTOL_GRAD, "VSC db")
     _say(f"[headline] VSC weight gradient ok ({time.time() - t0:.1f}s)")
 
@@ -125,7 +122,7 @@ def test_fullsize_headline_gradients_and_fused_forward():
     res = _bits(N, C, 36)
     y = spc.forward_fused(rb, _bf16_tensor(xv), _bf16_tensor(w), _t(scale), _t(shift),
                           _bf16_tensor(res), True)
-    yo, absb = ref.forward_rows(rows, xv, w, None, in_dt=oracle.BF16)
-    zo, bound = oracle.fused_epilogue(yo, absb, scale, shift, res[rows], True, oracle.BF16)
-    check_features(_to_np(y)[rows], zo, bound, RTOL_BF16, "fused")
+    yo, absb = ref.forward(xv, w, None, in_dt=oracle.BF16)
+    zo, bound = oracle.fused_epilogue(yo, absb, scale, shift, res, True, oracle.BF16)
+    check_features(_to_np(y), zo, bound, RTOL_BF16, "fused")
     _say(f"[headline] fused forward ok ({time.time() - t0:.1f}s)")

@@ -179,7 +179,8 @@ def test_filter_size_one_is_a_matmul():
 
 
 # ---------------------------------------------------------------------------
-# Pair order inside R_i: the Z-order (Morton) curve of the output site
+# Pair order inside R_i: ascending output row (the oracle's canonical order);
+# the Z-order curve the GPU library emits is checked against dense_ref.zorder
 # ---------------------------------------------------------------------------
 
 def test_zorder_reference_is_the_textbook_curve():
@@ -193,18 +194,30 @@ def test_zorder_reference_is_the_textbook_curve():
     assert list(dense_ref.zorder(two)) == [1, 0]
 
 
-def test_rule_book_pairs_follow_zorder_of_output_site():
+def test_zorder_reference_matches_bit_interleaving():
+    """Sorting by the interleaved key (coordinate 1's bit first inside a
+    level, sample index above all bits) is the same order."""
+    rng = np.random.default_rng(8)
+    sites = np.unique(np.stack([rng.integers(0, 3, 500), rng.integers(0, 40, 500),
+                                rng.integers(0, 40, 500), rng.integers(0, 40, 500)], 1), axis=0)
+    key = sites[:, 0].astype(object) << 48
+    for L in range(15, -1, -1):
+        for j in (1, 2, 3):
+            key = key + (((sites[:, j] >> L) & 1).astype(object) << (3 * L + (3 - j)))
+    expect = sorted(range(len(sites)), key=lambda k: key[k])
+    assert list(dense_ref.zorder(sites)) == expect
+
+
+def test_rule_book_pairs_ascend_by_output_row():
     rng = np.random.default_rng(55)
     size = [2, 16, 16, 16]
     coords = dense_ref.random_sites(rng, size, 0.1)
     for kind, f, s in ((oracle.VSC, [1, 3, 3, 3], [1, 1, 1, 1]),
-                       (oracle.SC, [1, 2, 2, 2], [1, 2, 2, 2])):
+                       (oracle.SC, [1, 2, 2, 2], [1, 2, 2, 2]),
+                       (oracle.SC, [1, 3, 3, 3], [1, 2, 2, 2])):
         rb = oracle.Rulebook(kind, coords, size, f, s)
-        rank = np.empty(rb.n_out, np.int64)
-        rank[dense_ref.zorder(rb.out_coords)] = np.arange(rb.n_out)
         for i in range(rb.K):
-            r = rank[rb.offset_pairs(i)[:, 1]]
-            assert np.all(np.diff(r) > 0)
+            assert np.all(np.diff(rb.offset_pairs(i)[:, 1]) > 0)
 
 
 # ---------------------------------------------------------------------------
@@ -363,3 +376,115 @@ def test_status_codes():
     # empty input: fine, empty output
     rb = oracle.Rulebook(oracle.SC, np.zeros((0, 3), np.int32), [1, 4, 4], [1, 2, 2], [1, 2, 2])
     assert rb.n_out == 0 and rb.pair_off[-1] == 0
+
+
+# ---------------------------------------------------------------------------
+# Sampled-row forward, the tolerance scale and the bound carried through a
+# stack of layers
+# ---------------------------------------------------------------------------
+
+def _abs_dense(kind, coords, size, f, s, xa, w, b):
+    """|b| + sum |x| |w| by the dense brute force on absolute values."""
+    if kind == oracle.VSC:
+        return dense_ref.vsc_dense(coords, size, f, xa, np.abs(w), np.abs(b))
+    return dense_ref.sc_dense(coords, size, f, s, xa, np.abs(w), np.abs(b))[1]
+
+
+@pytest.mark.parametrize("dt", [oracle.F32, oracle.BF16])
+@pytest.mark.parametrize("kind,f,s", [(oracle.VSC, [1, 3, 3], [1, 1, 1]),
+                                      (oracle.VSC, [1, 3, 5, 1], [1, 1, 1, 1]),
+                                      (oracle.SC, [1, 2, 2], [1, 2, 2]),
+                                      (oracle.SC, [1, 3, 2, 2], [1, 2, 1, 2])])
+def test_forward_rows_matches_dense_bruteforce(dt, kind, f, s):
+    """forward_rows on a random subset of rows: values and the absolute-sum
+    scale S = |b| + sum |x||w| equal the dense zero-filled convolution of x
+    and of |x| with |w| (plus |b|), and equal the full forward on those rows."""
+    from paper_1706_01307_amd import inputs
+    rng = np.random.default_rng(17 + len(f) + kind)
+    size = [2] + [7] * (len(f) - 1)
+    coords = dense_ref.random_sites(rng, size, 0.35)
+    K = int(np.prod(f))
+    xf = rng.standard_normal((len(coords), 5)).astype(np.float32)
+    wf = rng.standard_normal((K, 5, 6)).astype(np.float32)
+    b = rng.standard_normal(6).astype(np.float32)
+    if dt == oracle.BF16:
+        x, w = inputs.to_bf16_bits(xf), inputs.to_bf16_bits(wf)
+        xv, wv = inputs.bf16_bits_to_f32(x), inputs.bf16_bits_to_f32(w)
+    else:
+        x, w, xv, wv = xf, wf, xf, wf
+    rb = oracle.Rulebook(kind, coords, size, f, s)
+    rows = np.sort(rng.choice(rb.n_out, max(1, rb.n_out // 3), replace=False))
+    yr, ar = rb.forward_rows(rows, x, w, b, in_dt=dt)
+    if kind == oracle.VSC:
+        ref = dense_ref.vsc_dense(coords, size, f, xv, wv, b)
+    else:
+        oc, ref = dense_ref.sc_dense(coords, size, f, s, xv, wv, b)
+        np.testing.assert_array_equal(oc, rb.out_coords)
+    aref = _abs_dense(kind, coords, size, f, s, np.abs(xv), wv, b)
+    tol = 1e-12 * (1 + aref.max())
+    np.testing.assert_allclose(yr, ref[rows], rtol=0, atol=tol)
+    np.testing.assert_allclose(ar, aref[rows], rtol=0, atol=tol)
+    # and the same rows of the whole-layer forward, bit for bit (same sums)
+    y, a = rb.forward(x, w, b, in_dt=dt)
+    np.testing.assert_array_equal(yr, y[rows])
+    np.testing.assert_array_equal(ar, a[rows])
+    np.testing.assert_allclose(a, aref, rtol=0, atol=tol)
+
+
+@pytest.mark.parametrize("kind2,f2,s2", [(oracle.VSC, [1, 3, 3], [1, 1, 1]),
+                                         (oracle.SC, [1, 2, 2], [1, 2, 2])])
+def test_carried_bound_of_a_two_layer_chain(kind2, f2, s2):
+    """Layer 2 given x_absb = layer 1's bound S1: its bound equals
+    |b2| + sum S1 |w2|, recomputed with the dense brute force layer by layer
+    (and differs from the bound on |x| alone, so the argument is used)."""
+    rng = np.random.default_rng(91)
+    size = [2, 9, 9]
+    coords = dense_ref.random_sites(rng, size, 0.4)
+    f1 = [1, 3, 3]
+    x = rng.standard_normal((len(coords), 3)).astype(np.float32)
+    w1 = rng.standard_normal((9, 3, 4)).astype(np.float32)
+    b1 = rng.standard_normal(4).astype(np.float32)
+    rb1 = oracle.Rulebook(oracle.VSC, coords, size, f1)
+    y1, s1 = rb1.forward(x, w1, b1)
+    s1_dense = _abs_dense(oracle.VSC, coords, size, f1, None, np.abs(x), w1, b1)
+    np.testing.assert_allclose(s1, s1_dense, rtol=0, atol=1e-12 * s1_dense.max())
+    x2 = oracle.round_to(y1, oracle.F32)
+    K2 = int(np.prod(f2))
+    w2 = rng.standard_normal((K2, 4, 5)).astype(np.float32)
+    b2 = rng.standard_normal(5).astype(np.float32)
+    rb2 = oracle.Rulebook(kind2, coords, size, f2, s2)
+    y2, s2_carried = rb2.forward(x2, w2, b2, x_absb=s1)
+    expect = _abs_dense(kind2, coords, size, f2, s2, s1, w2, b2)
+    np.testing.assert_allclose(s2_carried, expect, rtol=0, atol=1e-12 * expect.max())
+    _, s2_plain = rb2.forward(x2, w2, b2)
+    assert not np.allclose(s2_plain, s2_carried)
+    # the values themselves do not depend on the carried bound
+    np.testing.assert_array_equal(y2, rb2.forward(x2, w2, b2)[0])
+
+
+def test_results_do_not_depend_on_thread_count():
+    """The rule book's lookups, the forward's rows and the weight gradient's
+    entries run in parallel; each sum has one fixed order, so 1 and several
+    threads agree bitwise."""
+    from paper_1706_01307_amd import inputs
+    coords = inputs.surfaces(2, 32, 4.0, 14.0, seed=3, target=3000)
+    size = [2, 32, 32, 32]
+    x = inputs.to_bf16_bits(inputs.normal_f32((len(coords), 16), seed=1))
+    w = inputs.to_bf16_bits(inputs.normal_f32((27, 16, 8), seed=2))
+    b = inputs.normal_f32((8,), seed=3)
+    before = oracle.set_threads(0)
+    try:
+        out = []
+        for th in (1, 3, 8):
+            oracle.set_threads(th)
+            rb = oracle.Rulebook(oracle.VSC, coords, size, [1, 3, 3, 3])
+            y, a = rb.forward(x, w, b, in_dt=oracle.BF16)
+            rbs = oracle.Rulebook(oracle.SC, coords, size, [1, 3, 3, 3], [1, 2, 2, 2])
+            dw, db, aw, ab = rb.backward_weight(oracle.VSC, x, x[:, :8].copy(), 16, 8,
+                                                oracle.BF16)
+            out.append((rb.pairs, y, a, rbs.pairs, rbs.out_coords, dw, aw, db))
+        for o in out[1:]:
+            for u, v in zip(out[0], o):
+                np.testing.assert_array_equal(u, v)
+    finally:
+        oracle.set_threads(before)

@@ -18,6 +18,7 @@ import oracle  # noqa: E402
 import paper_1706_01307_amd as spc  # noqa: E402
 from paper_1706_01307_amd import inputs  # noqa: E402
 from tests import dense_ref  # noqa: E402
+from tests.rb_check import check_rulebook  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -102,9 +103,7 @@ def compare_layer(kind, coords, size, f, s, C_in, C_out, dtype="f32", out_dtype=
          f"C={C_in}->{C_out} {dtype}->{out_dtype}")
     oc, pairs, pair_off, y, rb = run_layer(kind, coords, size, f, s, x, w, b, dtype, out_dtype)
     ref = oracle.Rulebook(kind, coords, size, f, s)
-    np.testing.assert_array_equal(oc, ref.out_coords)
-    np.testing.assert_array_equal(pair_off, ref.pair_off)
-    np.testing.assert_array_equal(pairs, ref.pairs)
+    check_rulebook(oc, pairs, pair_off, ref)
     yo, absb = ref.forward(x, w, b, in_dt=oracle.BF16 if dtype == "bf16" else oracle.F32)
     rtol = RTOL_F32 if (dtype == "f32" and out_dtype == "f32") else RTOL_BF16
     check_features(y, yo, absb, rtol, what)
@@ -146,8 +145,7 @@ def test_pen_stack_vsc_vsc_vsc_sc_f32():
     ys = spc.sc_forward(rbs, xg, _t(w), _t(b))
     ref_sc = oracle.Rulebook(oracle.SC, coords, size, [1, 2, 2], [1, 2, 2])
     oc, pairs = rbs.export()
-    np.testing.assert_array_equal(oc.cpu().numpy(), ref_sc.out_coords)
-    np.testing.assert_array_equal(pairs.cpu().numpy(), ref_sc.pairs)
+    check_rulebook(oc.cpu().numpy(), pairs.cpu().numpy(), rbs.pair_off, ref_sc)
     yo, absb = ref_sc.forward(oracle.round_to(xo, oracle.F32), w, b, x_absb=xa)
     check_features(_to_np(ys), yo, absb, RTOL_F32, "stack SC")
 
@@ -362,10 +360,10 @@ def test_async_build_and_reuse():
     size = [1, 32, 32, 32]
     x = inputs.normal_f32((len(coords), 32), seed=2)
     w, b = make_layer(8, 27, 32, 32, "f32")
-    _, pairs, _, y, rb = run_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1], x, w, b,
-                                   "f32", "f32", sync=False)
+    oc, pairs, pair_off, y, rb = run_layer(spc.VSC, coords, size, [1, 3, 3, 3], [1, 1, 1, 1],
+                                           x, w, b, "f32", "f32", sync=False)
     ref = oracle.Rulebook(oracle.VSC, coords, size, [1, 3, 3, 3])
-    np.testing.assert_array_equal(pairs, ref.pairs)
+    check_rulebook(oc, pairs, pair_off, ref)
     # the same rule book serves a second layer
     w2, b2 = make_layer(9, 27, 32, 32, "f32")
     y2 = spc.vsc_forward(rb, _t(x), _t(w2), _t(b2))
@@ -446,8 +444,8 @@ def test_non_contiguous_coords_through_python_api():
     assert not cf.is_contiguous()
     rb = spc.build_rulebook(spc.VSC, cf, [2, 32, 32], [1, 3, 3])
     ref = oracle.Rulebook(oracle.VSC, coords, [2, 32, 32], [1, 3, 3])
-    _, pairs = rb.export()
-    np.testing.assert_array_equal(pairs.cpu().numpy(), ref.pairs)
+    oc, pairs = rb.export()
+    check_rulebook(oc.cpu().numpy(), pairs.cpu().numpy(), rb.pair_off, ref)
 
 
 @pytest.mark.parametrize("path", ["mfma", "vec"])
