@@ -311,8 +311,11 @@ int spconv_release_cached_memory(int64_t* released);
  * may be NULL.  Errors: EINVAL for a device index out of range, EHIP. */
 int spconv_memory_stats(int device, int64_t* in_use, int64_t* cached);
 
-/* Release a rule book (stream-ordered on its build stream).  NULL is a
- * no-op. */
+/* Release a rule book.  Stream-ordered: the memory is given back on the
+ * build stream after the build stream's own work and after the latest work
+ * that any other stream enqueued on this book (every call that takes the
+ * book records, on a stream other than the build stream, an event there
+ * that the release waits on).  The host does not wait.  NULL is a no-op. */
 void spconv_rulebook_destroy(spconv_rulebook rb);
 
 /* Static string naming a status code. */

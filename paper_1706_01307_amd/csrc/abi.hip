@@ -66,8 +66,47 @@ int sync_rulebook(spconv_rulebook rb) {
 std::mutex g_alloc_mu;
 Allocator g_alloc;                 // the allocator new builds take
 
+// Record that work reading rb was enqueued on `stream` (after it was
+// enqueued).  On the build stream nothing is needed: the release is ordered
+// there.  On another stream an event is (re)recorded after the work, for the
+// release to wait on; if no event can be made, the stream is drained now.
+int note_use(spconv_rulebook rb, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (st == rb->stream) return SPCONV_OK;
+  std::lock_guard<std::mutex> lk(rb->uses_mu);
+  spconv_rulebook_s::Use* u = nullptr;
+  for (auto& e : rb->uses)
+    if (e.stream == st) u = &e;
+  if (!u) {
+    hipEvent_t ev;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess) {
+      rb->uses.push_back({st, ev});
+      u = &rb->uses.back();
+    }
+  }
+  if (u && hipEventRecord(u->done, st) == hipSuccess) return SPCONV_OK;
+  (void)hipGetLastError();
+  if (hipStreamSynchronize(st) != hipSuccess) {
+    (void)hipGetLastError();
+    return SPCONV_EHIP;
+  }
+  return SPCONV_OK;
+}
+
+int used_on(spconv_rulebook rb, void* stream, int st) {
+  if (st != SPCONV_OK) return st;
+  return note_use(rb, stream);
+}
+
 void release(spconv_rulebook rb) {
   if (!rb) return;
+  // the memory is freed on the build stream, after every other stream's
+  // latest work on this book
+  for (auto& u : rb->uses) {
+    (void)hipStreamWaitEvent(rb->stream, u.done, 0);
+    (void)hipEventDestroy(u.done);
+  }
+  rb->uses.clear();
   if (rb->mem) (void)dev_free(rb, rb->mem, rb->stream);
   (void)hipGetLastError();
   delete rb;
@@ -293,7 +332,7 @@ int spconv_build_rulebook_on(spconv_rulebook parent, int kind, const int32_t* f,
     return SPCONV_EINVAL;
   const int st = build_impl(kind, parent->D, parent->out_coords, parent->n_cap,
                             &parent->hdr->n_out, parent->out_size, f, s, flags, stream, out);
-  if (st != kNeedHostCount) return st;
+  if (st != kNeedHostCount) return used_on(parent, stream, st);
   // the hash-table path needs the count on the host: read it, build normally
   int64_t n = 0;
   hipStream_t hs = static_cast<hipStream_t>(stream);
@@ -303,8 +342,9 @@ int spconv_build_rulebook_on(spconv_rulebook parent, int kind, const int32_t* f,
     (void)hipGetLastError();
     return SPCONV_EHIP;
   }
-  return build_impl(kind, parent->D, parent->out_coords, n, nullptr, parent->out_size, f, s,
-                    flags, stream, out);
+  return used_on(parent, stream,
+                 build_impl(kind, parent->D, parent->out_coords, n, nullptr, parent->out_size,
+                            f, s, flags, stream, out));
 }
 
 int spconv_rulebook_bounds(spconv_rulebook rb, int64_t* n_in_bound, int64_t* n_out_bound) {
@@ -368,7 +408,7 @@ int spconv_rulebook_export(spconv_rulebook rb, int32_t* out_coords, int32_t* pai
       return SPCONV_EHIP;
     }
   }
-  return SPCONV_OK;
+  return note_use(rb, stream);
 }
 
 int spconv_rulebook_out_coords(spconv_rulebook rb, const int32_t** coords) {
@@ -397,7 +437,8 @@ static int forward_common(spconv_rulebook rb, int kind, int in_dt, const void* x
                        reinterpret_cast<uintptr_t>(y);
   if ((al & 15) || (reinterpret_cast<uintptr_t>(bias) & 3)) return SPCONV_EINVAL;
   if (check_only) return SPCONV_OK;
-  return forward(rb, in_dt, x, w, bias, out_dt, y, C_in, C_out, static_cast<hipStream_t>(stream));
+  return used_on(rb, stream, forward(rb, in_dt, x, w, bias, out_dt, y, C_in, C_out,
+                                     static_cast<hipStream_t>(stream)));
 }
 
 int spconv_vsc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
@@ -433,8 +474,8 @@ int spconv_forward_fused(spconv_rulebook rb, int in_dt, const void* x, const voi
   e.scale = scale;
   e.res = residual;
   e.relu = relu;
-  return forward_view(view_of(rb), 0, in_dt, x, w, shift, out_dt, y, C_in, C_out,
-                      static_cast<hipStream_t>(stream), e);
+  return used_on(rb, stream, forward_view(view_of(rb), 0, in_dt, x, w, shift, out_dt, y, C_in,
+                                          C_out, static_cast<hipStream_t>(stream), e));
 }
 
 static bool dtype_ok(int dt) { return dt == SPCONV_F32 || dt == SPCONV_BF16; }
@@ -446,7 +487,7 @@ int spconv_pool_forward(spconv_rulebook rb, int mode, int dt, const void* x, voi
   if (mode != SPCONV_POOL_MAX && mode != SPCONV_POOL_AVG) return SPCONV_EINVAL;
   if (out_rows(rb) > 0 && (!y || (rb->n_in > 0 && !x))) return SPCONV_EINVAL;
   if (misaligned(x) || misaligned(y)) return SPCONV_EINVAL;
-  return pool_forward(rb, mode, dt, x, y, C, static_cast<hipStream_t>(stream));
+  return used_on(rb, stream, pool_forward(rb, mode, dt, x, y, C, static_cast<hipStream_t>(stream)));
 }
 
 int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* w,
@@ -461,9 +502,10 @@ int spconv_dc_forward(spconv_rulebook rb, int in_dt, const void* x, const void* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (rb->t_single && rb->n_in > 0) {
     const int r = transpose_single(rb, 0, in_dt, x, w, bias, out_dt, y, C_in, C_out, st);
-    if (r != kNotSingle) return r;
+    if (r != kNotSingle) return used_on(rb, stream, r);
   }
-  return forward_view(transpose_view(rb), 0, in_dt, x, w, bias, out_dt, y, C_in, C_out, st);
+  return used_on(rb, stream, forward_view(transpose_view(rb), 0, in_dt, x, w, bias, out_dt, y,
+                                          C_in, C_out, st));
 }
 
 // The book, view and weight mode an input gradient runs on.
@@ -506,9 +548,10 @@ int spconv_backward_data(spconv_rulebook rb, int op, int dt, const void* dy, con
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (op == SPCONV_OP_SC && rb->t_single && rb->n_in > 0) {
     const int r = transpose_single(rb, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in, st);
-    if (r != kNotSingle) return r;
+    if (r != kNotSingle) return used_on(rb, stream, r);
   }
-  return forward_view(v, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in, st);
+  return used_on(rb, stream, forward_view(v, wmode, dt, dy, w, nullptr, out_dt, dx, C_out, C_in,
+                                          st));
 }
 
 int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C_out,
@@ -535,8 +578,8 @@ int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, co
   const int64_t xr = op == SPCONV_OP_DC ? rb->n_out : rb->n_in;
   const int64_t gr = op == SPCONV_OP_SC ? rb->n_out : rb->n_in;
   if ((xr > 0 && !x) || (gr > 0 && !dy)) return SPCONV_EINVAL;
-  return backward_weight(rb, op, dt, x, dy, dw, db, C_in, C_out, workspace,
-                         static_cast<hipStream_t>(stream));
+  return used_on(rb, stream, backward_weight(rb, op, dt, x, dy, dw, db, C_in, C_out, workspace,
+                                             static_cast<hipStream_t>(stream)));
 }
 
 void spconv_rulebook_destroy(spconv_rulebook rb) { release(rb); }

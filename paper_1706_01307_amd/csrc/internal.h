@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "spconv.h"
@@ -200,6 +201,16 @@ struct spconv_rulebook_s {
   int32_t* t_chunk_off;        // [K + 1] first chunk of every offset
   spc::DeviceHeader* t_hdrs;   // [K] n_out = k_i; [K] (one more) n_out = padded length
   std::vector<int64_t> h_pair_off;   // host copy of pair_off, filled on first use
+  // Streams other than the build stream that work reading this book was
+  // enqueued on, each with an event recorded after its latest such work:
+  // the release makes the build stream wait on all of them before the
+  // memory goes back to the allocator.
+  struct Use {
+    hipStream_t stream;
+    hipEvent_t done;
+  };
+  std::vector<Use> uses;
+  std::mutex uses_mu;
   // host state after synchronisation
   bool synced;
   int status;

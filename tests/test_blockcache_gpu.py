@@ -114,3 +114,37 @@ def test_memory_stats_rejects_bad_device():
     n = torch.cuda.device_count()
     assert lib.spconv_memory_stats(n, None, None) == spc.EINVAL
     assert lib.spconv_memory_stats(-1, None, None) == spc.EINVAL
+
+
+def test_destroy_waits_for_work_on_another_stream():
+    """A book is built on stream A, read by a forward on a second stream B that
+    is still busy, and destroyed at once; the next build on A (a different
+    site set of the same size, so it asks the cache for the same block) must
+    not overwrite the book before B's forward has run.  The forward's output
+    is then checked against the oracle's forward of the first book."""
+    import oracle
+    from tests.test_parity_gpu import RTOL_F32, check_features
+    c = inputs.surfaces(1, 48, 6, 18, seed=12, variant="literal")
+    c2 = np.ascontiguousarray(c[::-1])
+    c2[:, 1:] = 47 - c2[:, 1:]                  # mirrored: other sites, same count
+    size = [1, 48, 48, 48]
+    f = [1, 3, 3, 3]
+    x = inputs.normal_f32((len(c), 16), seed=1)
+    w = inputs.normal_f32((27, 16, 16), std=0.05, seed=2)
+    rb = spc.build_rulebook(spc.VSC, _t(c), size, f)
+    xt, wt = _t(x), _t(w)
+    y = torch.zeros((len(c), 16), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(50_000_000)           # keeps B busy while A moves on
+        spc.vsc_forward(rb, xt, wt, None, out=y)
+    rb.close()                                   # released on A
+    others = [spc.build_rulebook(spc.VSC, _t(c2), size, f, sync=False) for _ in range(2)]
+    torch.cuda.synchronize()
+    for o in others:
+        assert o.status() == spc.OK
+        o.close()
+    ref = oracle.Rulebook(oracle.VSC, c, size, f)
+    yo, absb = ref.forward(x, w)
+    check_features(y.cpu().numpy(), yo, absb, RTOL_F32, "forward on stream B")
