@@ -49,8 +49,8 @@ def _args():
     p.add_argument("--workload", default="surf128x8_vsc3_c64_bf16")
     p.add_argument("--variant", default="matched", choices=["matched", "literal"])
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-samples", type=int, default=4,
-                   help="samples of the batch the oracle baseline runs on")
+    p.add_argument("--cpu-samples", type=int, default=2,
+                   help="samples of the batch the single-thread oracle baseline runs on")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one plain device copy of this many MiB (counter calibration)")
     p.add_argument("--peaks", action="store_true",
@@ -92,22 +92,53 @@ def load_traffic(kernel, workload):
     return t.get("hbm_bytes_per_launch")
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wl, x_bits, w_bits, bias, n_samples):
-    """Oracle (std::map build + double forward) on the first samples of the
-    same batch: a bounded slice of the workload (~10 s of CPU work here)."""
+    """The oracle (std::map rule book + double-precision forward, both
+    parallel over output rows on OpenMP threads) timed on this host: the whole
+    workload on every thread OpenMP is given, and the first samples of the
+    batch on one thread (a bounded slice; its rate is reported per site)."""
     import oracle
-    keep = wl.coords[:, 0] < n_samples
-    sample = wl.coords[keep]
-    rows = np.nonzero(keep)[0]
-    n = len(sample)
-    t0 = time.perf_counter()
-    rb = oracle.Rulebook(oracle.VSC, sample, wl.spatial_size, [1] + [3] * wl.d)
-    t1 = time.perf_counter()
-    rb.forward(x_bits[rows], w_bits, bias, in_dt=oracle.BF16 if wl.dtype == "bf16" else oracle.F32)
-    t2 = time.perf_counter()
-    return {"value": n / (t2 - t0), "unit": "active sites/s", "cores": 1, "kind": "oracle",
-            "sample": f"samples 0..{n_samples - 1} of the batch: {n} sites, rule book "
-                      f"{t1 - t0:.2f} s + forward {t2 - t1:.2f} s, single thread"}
+    in_dt = oracle.BF16 if wl.dtype == "bf16" else oracle.F32
+    f = [1] + [3] * wl.d
+
+    def run(rows):
+        t0 = time.perf_counter()
+        rb = oracle.Rulebook(oracle.VSC, wl.coords[rows], wl.spatial_size, f)
+        t1 = time.perf_counter()
+        rb.forward(x_bits[rows], w_bits, bias, in_dt=in_dt)
+        t2 = time.perf_counter()
+        return t1 - t0, t2 - t1
+
+    threads = oracle.set_threads(0)
+    n = len(wl.coords)
+    tb, tf = run(np.arange(n))
+    sample = np.nonzero(wl.coords[:, 0] < n_samples)[0]
+    oracle.set_threads(1)
+    try:
+        sb, sf = run(sample)
+    finally:
+        oracle.set_threads(threads)
+    return {"value": n / (tb + tf), "unit": "active sites/s", "cores": threads,
+            "kind": "oracle", "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "sample": f"the whole workload ({n} sites) on {threads} OpenMP threads: rule book "
+                      f"{tb:.2f} s + forward {tf:.2f} s",
+            "single_thread": {"value": len(sample) / (sb + sf), "unit": "active sites/s",
+                              "cores": 1,
+                              "sample": f"samples 0..{n_samples - 1} of the batch "
+                                        f"({len(sample)} sites) on one thread: rule book "
+                                        f"{sb:.2f} s + forward {sf:.2f} s"}}
 
 
 def main():
@@ -240,10 +271,15 @@ def main():
     esz = 2 if bf16 else 4
     fwd_bytes = N * Cin * esz + N * Cout * esz + 4 * K * N + K * Cin * Cout * esz + 4 * Cout
 
-    # rule-book outputs the build must write: gather map (4 K N), pairs
-    # (8 per pair), schedule (4 N), per-offset offsets; plus the coordinates
-    # it reads (4 D N)
-    rb_bytes = 4 * K * N + 8 * sum_k + 4 * N + 8 * (K + 1) + 4 * D * N
+    # rule-book algorithmic bytes (the unit cost the survey fixes for a VSC
+    # build): coordinates read (4 D N), a hash table of cap = 2^ceil(log2 2N)
+    # 8-byte slots initialised, one 12-byte insert per site, one 12-byte
+    # key + value probe per site and non-centre offset, the pairs written
+    # (8 per pair) and the K + 1 offsets
+    cap = 1 << max(0, (2 * N - 1).bit_length())
+    rb_bytes = (4 * D * N + 8 * cap + 12 * N + 12 * (K - 1) * N + 8 * sum_k + 8 * (K + 1))
+    # what this build itself must write: gather map, pairs, schedule, offsets
+    rb_out_bytes = 4 * K * N + 8 * sum_k + 4 * N + 8 * (K + 1)
 
     headline = a.workload == "surf128x8_vsc3_c64_bf16"
     out = {
@@ -268,7 +304,10 @@ def main():
         "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
         "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
         "rulebook_io": {"algorithmic_bytes": rb_bytes,
-                        "GBps": rb_bytes / (rb_ms * 1e-3) / 1e9, "peak_GBps": PEAKS["hbm"]},
+                        "GBps": rb_bytes / (rb_ms * 1e-3) / 1e9, "peak_GBps": PEAKS["hbm"],
+                        "frac": rb_bytes / (rb_ms * 1e-3) / 1e9 / PEAKS["hbm"],
+                        "output_bytes": rb_out_bytes,
+                        "output_GBps": rb_out_bytes / (rb_ms * 1e-3) / 1e9},
         "phases_ms_p10_p50_p90": {"rulebook": pct(rb_t), "forward": pct(fwd_t),
                                   "build_and_forward": pct(rb_t + fwd_t)},
         "cold_caches_ms_median": ({"steps": a.cold_steps,

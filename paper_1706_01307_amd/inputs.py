@@ -237,17 +237,31 @@ def _layer_list(spec):
     return [Layer(*t) for t in spec]
 
 
+_SITE_SETS = {}
+
+
+def _site_set(name, variant, seed):
+    """Coordinates of a named workload, generated once per process (the
+    256^3 surfaces take tens of seconds); callers get their own copy."""
+    key = (name, variant, seed)
+    if key not in _SITE_SETS:
+        spec = WORKLOADS[name]
+        if spec["family"] == "pen":
+            coords = pen_strokes(spec["batch"], spec["size"], seed=seed,
+                                 variant=variant, target=spec["target"])
+        else:
+            coords = surfaces(spec["batch"], spec["size"], spec["r_lo"],
+                              spec["r_hi"], seed=seed, variant=variant,
+                              target=spec["target"])
+        _SITE_SETS[key] = coords
+    return _SITE_SETS[key].copy()
+
+
 def make_workload(name, variant="matched", seed=None):
     """Build one named workload (site set plus layer list)."""
     spec = WORKLOADS[name]
     seed = spec["seed"] if seed is None else seed
-    if spec["family"] == "pen":
-        coords = pen_strokes(spec["batch"], spec["size"], seed=seed,
-                             variant=variant, target=spec["target"])
-    else:
-        coords = surfaces(spec["batch"], spec["size"], spec["r_lo"],
-                          spec["r_hi"], seed=seed, variant=variant,
-                          target=spec["target"])
+    coords = _site_set(name, variant, seed)
     return Workload(name=name, d=spec["d"], size=spec["size"],
                     batch=spec["batch"], layers=_layer_list(spec["layers"]),
                     dtype=spec["dtype"], coords=coords)
