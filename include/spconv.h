@@ -61,7 +61,9 @@ typedef enum {
   SPCONV_ERANGE = -3, /* a coordinate lies outside [0, spatial_size)         */
   SPCONV_ENOMEM = -4, /* device allocation failed                            */
   SPCONV_ECAP = -5,   /* hash table full (only with a forced tiny capacity)  */
-  SPCONV_EHIP = -6    /* a HIP runtime call failed                           */
+  SPCONV_EHIP = -6,   /* a HIP runtime call failed                           */
+  SPCONV_ESCRATCH = -7 /* the call needs more than the library's fixed scratch
+                        * array (spconv_backward_weight_noalloc)             */
 } spconv_status;
 
 typedef enum { SPCONV_F32 = 0, SPCONV_BF16 = 1 } spconv_dtype;
@@ -275,6 +277,30 @@ int spconv_backward_weight_workspace(spconv_rulebook rb, int op, int C_in, int C
 int spconv_backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const void* dy,
                            float* dw, float* db, int C_in, int C_out, void* workspace,
                            size_t workspace_bytes, void* stream);
+
+/* Size of the library's fixed device scratch array (one per GPU the library
+ * runs on, held until the process ends): 128 MiB. */
+#define SPCONV_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* spconv_backward_weight for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same gradients, the same kernels and the same results,
+ * bit for bit, with the partial sums kept in the library's fixed scratch
+ * array instead of a caller workspace.  Arguments as spconv_backward_weight
+ * without the workspace; the book's device must be the current device.
+ * Allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (on different streams, or from different host threads) race and must
+ * be ordered by the caller; nothing in the array needs to start at zero.  A
+ * book built with SPCONV_BUILD_ASYNC is waited for once, as in
+ * spconv_backward_weight (under graph capture, synchronise the book first).
+ * Errors: those of spconv_backward_weight; ESCRATCH when the partials
+ * (spconv_backward_weight_workspace bytes) exceed
+ * SPCONV_NOALLOC_SCRATCH_BYTES; EINVAL when the book's device is not
+ * current. */
+int spconv_backward_weight_noalloc(spconv_rulebook rb, int op, int dt, const void* x,
+                                   const void* dy, float* dw, float* db, int C_in, int C_out,
+                                   void* stream);
 
 /* Device memory of the rule books.  Every allocation the library makes (a
  * rule book's persistent block and the transient buffers of a build) comes

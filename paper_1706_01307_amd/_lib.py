@@ -13,7 +13,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libspconv.so")
 
-OK, EINVAL, EDUP, ERANGE, ENOMEM, ECAP, EHIP = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, EDUP, ERANGE, ENOMEM, ECAP, EHIP, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7
 VSC, SC = 0, 1
 OP_VSC, OP_SC, OP_DC = 0, 1, 2
 POOL_MAX, POOL_AVG = 0, 1
@@ -44,6 +44,7 @@ SIGNATURES = {
     "spconv_backward_data": (_I, [_P, _I, _I, _P, _P, _I, _P, _I, _I, _P]),
     "spconv_backward_weight_workspace": (_I, [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_size_t)]),
     "spconv_backward_weight": (_I, [_P, _I, _I, _P, _P, _P, _P, _I, _I, _P, ctypes.c_size_t, _P]),
+    "spconv_backward_weight_noalloc": (_I, [_P, _I, _I, _P, _P, _P, _P, _I, _I, _P]),
     "spconv_rulebook_destroy": (None, [_P]),
     "spconv_status_string": (ctypes.c_char_p, [_I]),
 }

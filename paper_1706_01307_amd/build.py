@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspconv.so")
 SOURCES = ["abi.hip", "rulebook.hip", "forward.hip", "forward_w0.hip", "forward_w1.hip",
-           "forward_w2.hip", "ops.hip", "sort.hip", "blockcache.hip"]
+           "forward_w2.hip", "ops.hip", "sort.hip", "blockcache.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -174,6 +174,7 @@ const char* spconv_status_string(int s) {
     case SPCONV_ENOMEM: return "device allocation failed";
     case SPCONV_ECAP: return "hash table full";
     case SPCONV_EHIP: return "HIP runtime error";
+    case SPCONV_ESCRATCH: return "request exceeds the library's fixed scratch array";
     default: return "unknown status";
   }
 }

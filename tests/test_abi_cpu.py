@@ -23,7 +23,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = _declared_symbols()
-    assert len(names) == 20, names
+    assert len(names) == 21, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     lib = _lib.load()
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
         s = lib.spconv_status_string(code).decode()
         assert s and s != "unknown status"
     assert lib.spconv_status_string(-99).decode() == "unknown status"
@@ -95,6 +95,8 @@ def test_new_entry_points_reject_bad_arguments_on_the_host():
     assert lib.spconv_backward_weight_workspace(None, 0, 1, 1, ctypes.byref(nbytes)) == E
     assert lib.spconv_backward_weight(None, 0, 0, None, None, None, None, 1, 1, None, 0,
                                       None) == E
+    assert lib.spconv_backward_weight_noalloc(None, 0, 0, None, None, None, None, 1, 1,
+                                              None) == E
     # the transposed book exists for SC only; unknown flag bits are rejected
     size = np.asarray([1, 4, 4], np.int32)
     f = np.asarray([1, 3, 3], np.int32)
