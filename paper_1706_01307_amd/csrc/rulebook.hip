@@ -25,6 +25,8 @@
 //   k_scan       per offset, exclusive scan of the per-wave pair counts
 //   k_compact    per-offset stream compaction of G into R_i, in schedule
 //                order (wave ballot + mbcnt, per-wave prefix)
+// except the grouped VSC 3x3x3 grid probe, which counts in a first pass and
+// writes G and R_i together in a second (k_probe_grid_g4<false / true>).
 // SC (output set = sites with an active input in their receptive field):
 //   the input sites go into the grid or table as above, then
 //   k_sc_mark    every input marks the output sites it feeds in a bitmap
@@ -794,14 +796,45 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
 // stay inside the grid even for neighbours off its edge (the dilated
 // addition wraps within the coordinate's bits); those are masked by the
 // coordinate range checks.  Offset i = 9 (dx + 1) + 3 (dy + 1) + (dz + 1).
+//
+// It runs twice.  WRITE = false counts, per block and offset, the positions
+// with a neighbour (and the per-wave prefixes), which k_scan turns into each
+// block's base inside every R_i.  WRITE = true repeats the same lookups and
+// writes the gather map and, at once, every pair at its final place in R_i
+// (pair_off[i] + the block's base + the waves before it + the set lanes
+// before it), so the pair lists never need a second pass over the gather
+// map.  Workgroup 0 of the writing pass also stores pair_off.
+template <bool WRITE>
 __global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
     const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
     const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g,
     const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
-    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk) {
+    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk,
+    const int64_t* __restrict__ totals, int2* __restrict__ pairs,
+    int64_t* __restrict__ pair_off) {
+  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
+  __shared__ int64_t s_off[28];
+  __shared__ uint32_t s_wp[27];
+  if constexpr (WRITE) {
+    // pair_off = exclusive prefix of the 27 totals
+    if (threadIdx.x < kWave) {
+      const int64_t t = threadIdx.x < 27 ? totals[threadIdx.x] : 0;
+      const int64_t inc = wave_incl_scan(t);
+      if (threadIdx.x < 28) s_off[threadIdx.x] = inc - t;
+    }
+    __syncthreads();
+    if (blockIdx.x == 0 && threadIdx.x < 28) pair_off[threadIdx.x] = s_off[threadIdx.x];
+  }
   const int64_t blk = probe_block(hdr->n_out, nblk);
   if (blk < 0) return;
-  __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
+  if constexpr (WRITE) {
+    if (threadIdx.x < 27) {
+      const int64_t q = static_cast<int64_t>(threadIdx.x) * nblk + blk;
+      s_off[threadIdx.x] += blk_cnt[q];
+      s_wp[threadIdx.x] = wpre[q];
+    }
+    __syncthreads();
+  }
   const int64_t n_rows = hdr->n_out;
   const int64_t p = blk * kBlock + threadIdx.x;
   const bool valid = p < n_rows;
@@ -864,11 +897,16 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
       const uint32_t val = ey ? hi : lo;
       e = (xok[dx] && yok[dy] && zok[dz]) ? static_cast<int32_t>(val) : 0;
     }
-    if (p < gstride) gmap[i * gstride + p] = e;   // 1 + input row, 0 = none
     const uint64_t m = __ballot(e != 0);
-    if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
+    if constexpr (WRITE) {
+      if (p < gstride) gmap[i * gstride + p] = e;   // 1 + input row, 0 = none
+      if (e != 0)
+        pairs[s_off[i] + wave_prefix(s_wp[i], wave) + prefix_popc(m)] = make_int2(e - 1, y);
+    } else {
+      if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(m));
+    }
   }
-  publish_counts(s_cnt, 27, blk_cnt, wpre, nblk, blk);
+  if constexpr (!WRITE) publish_counts(s_cnt, 27, blk_cnt, wpre, nblk, blk);
 }
 
 // SC 2^3 with stride 2 on a 4-D grid whose three lowest Z bits are the lowest
@@ -1211,10 +1249,18 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
   const bool sc = rb->kind == SPCONV_SC;
   if (!sc && rb->D == 4 && rb->f[1] == 3 && rb->f[2] == 3 && rb->f[3] == 3 &&
       (g.M[3] & 1u) && (g.M[2] & 2u)) {
-    k_probe_grid_g4<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
-        rows_sites, rb->perm, rb->hdr, rb->gstride, g, b.grid, static_cast<uint32_t>(cells),
-        rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk);
-    launch_scan_compact(rb);
+    // count, scan the counts into block bases, then write the gather map and
+    // the pairs in one pass (no compaction kernel re-reading the gather map)
+    auto probe = [&](auto kern) {
+      kern<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
+          rows_sites, rb->perm, rb->hdr, rb->gstride, g, b.grid, static_cast<uint32_t>(cells),
+          rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk, rb->totals,
+          reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+    };
+    probe(k_probe_grid_g4<false>);
+    k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
+                                                                    rb->totals);
+    probe(k_probe_grid_g4<true>);
     return;
   }
   if (sc && rb->D == 4 && rb->f[1] == 2 && rb->f[2] == 2 && rb->f[3] == 2 && rb->s[1] == 2 &&
