@@ -197,8 +197,8 @@ def main():
                   fa.ctypes.data, sa.ctypes.data, _lib.BUILD_ASYNC, sp, ctypes.byref(h))
     xp, wp, bp, ypt = (ctypes.c_void_p(t.data_ptr()) for t in (xt, wt, bt, yt))
 
-    def step(evs=None):
-        if evs:
+    def step(evs=None, split=True):
+        if evs and split:
             evs[0].record(stream)
         _lib.check(lib.spconv_build_rulebook(*args_build), "build")
         if evs:
@@ -229,15 +229,26 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+    # the timed steps: events around the forward only (its duration is the
+    # roofline's denominator); the build's share comes from the same steps
+    # run again untimed with an event before the build as well
+    evt = [[None] + [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+           for _ in range(a.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    host = 0.0
+    for i in range(a.steps):
+        h0 = time.perf_counter()
+        step(evt[i], split=False)
+        host += time.perf_counter() - h0
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    fwd_t = np.array([e[1].elapsed_time(e[2]) for e in evt])
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
     for i in range(a.steps):
         step(evs[i])
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
     rb_t = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    fwd_t = np.array([e[1].elapsed_time(e[2]) for e in evs])
     rb_ms, fwd_ms = float(rb_t.mean()), float(fwd_t.mean())
     ms_per_step = (t1 - t0) * 1e3 / a.steps
 
@@ -302,6 +313,7 @@ def main():
         "knobs": knobs(),
         "effective_tflops": tflops,
         "sites_per_s_rulebook_reuse": N / (fwd_ms * 1e-3),
+        "host_enqueue_ms_per_step": host * 1e3 / a.steps,
         "phases_ms": {"rulebook": rb_ms, "forward": fwd_ms},
         "rulebook_io": {"algorithmic_bytes": rb_bytes,
                         "GBps": rb_bytes / (rb_ms * 1e-3) / 1e9, "peak_GBps": PEAKS["hbm"],

@@ -20,8 +20,11 @@
 //               returns zero for absent neighbours; a 16-row block whose 16
 //               rows all lack offset i skips its MFMAs (and, for filters
 //               other than 3^3, its gathers).
-//   k_fwd_vec   any channel count: one lane per (output row, output column),
-//               fp32 FMA chain.  The low-channel path (e.g. 1 input plane).
+//   k_fwd_lowc  at most 4 input planes (e.g. the 1 plane of a pen-stroke
+//               input): one lane per (output row, 16 output columns), fp32
+//               FMA chains, weights through the scalar cache.
+//   k_fwd_vec   any other channel count: one lane per (output row, output
+//               column), fp32 FMA chain.
 #pragma once
 
 #include <cstdlib>
@@ -69,6 +72,42 @@ template <> struct ElemIO<uint16_t> {
   __device__ static void store(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
 };
 
+// Buffer loads whose hardware range check returns zero for an offset past
+// the resource (kBufOOB and up): a load that may have nothing to read needs
+// no branch (a load under a branch forces a wait for every load in flight).
+constexpr uint32_t kBufOOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes),
+                                           static_cast<int>(kBufDword3));
+}
+template <typename T> struct BufIO;
+template <> struct BufIO<float> {
+  static constexpr uint32_t kSize = 4;
+  __device__ static float load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+  }
+};
+template <> struct BufIO<uint16_t> {
+  static constexpr uint32_t kSize = 2;
+  __device__ static float load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+  }
+};
+// Gather-map entries of offsets i0 .. i0 + KB - 1 at position p, minus one
+// (-1: no neighbour, or offset past K).
+template <int KB>
+__device__ __forceinline__ void load_map(const int32_t* gmap, int64_t gstride, int K, int i0,
+                                         int64_t p, int32_t (&g)[KB]) {
+  const uint32_t bytes = static_cast<uint32_t>(gstride * 4);
+#pragma unroll
+  for (int b = 0; b < KB; ++b) {
+    const int i = i0 + b < K ? i0 + b : 0;
+    const __amdgpu_buffer_rsrc_t r = buf_rsrc(gmap + static_cast<int64_t>(i) * gstride, bytes);
+    const uint32_t off = i0 + b < K ? static_cast<uint32_t>(p) * 4u : kBufOOB;
+    g[b] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0)) - 1;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Generic (vector ALU) path
 // ---------------------------------------------------------------------------
@@ -85,28 +124,59 @@ __device__ __forceinline__ int64_t w_index(int i, int K, int c, int n, int C_in,
   return (static_cast<int64_t>(iw) * C_out + n) * C_in + c;
 }
 
+// Positions run over the capacity n_cap (known on the host) so that the
+// loads of the gather map do not wait for the device-side row count; a
+// position at or past the count contributes nothing and stores nothing.
+// The map entries of 8 offsets are loaded together (and, for one input
+// plane, their input values and weights), then accumulated in offset order.
 template <typename TIn, typename TOut, int WT>
 __global__ __launch_bounds__(256) void k_fwd_vec(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
-    const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
+    int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
     const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
     int C_out, Epilogue epi) {
+  constexpr int KB = 8;
   const int64_t n_rows = hdr->n_out;
-  const int64_t total = n_rows * C_out;
+  const int64_t total = n_cap * C_out;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   for (int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; idx < total;
        idx += stride) {
     const int64_t p = idx / C_out;                 // schedule position
     const int col = static_cast<int>(idx - p * C_out);
+    const bool live = p < n_rows;
     float acc = 0.0f;
-    for (int i = 0; i < K; ++i) {
-      const int32_t g = gmap[i * gstride + p] - 1;
-      if (g < 0) continue;
-      const int64_t xb = static_cast<int64_t>(g) * C_in;
-      for (int c = 0; c < C_in; ++c)
-        acc = fmaf(ElemIO<TIn>::load(x, xb + c),
-                   ElemIO<TIn>::load(w, w_index<WT>(i, K, c, col, C_in, C_out)), acc);
+    for (int i0 = 0; i0 < K; i0 += KB) {
+      int32_t g[KB];
+#pragma unroll
+      for (int b = 0; b < KB; ++b) {          // in bounds for every b: no branch
+        const int i = i0 + b < K ? i0 + b : K - 1;
+        g[b] = gmap[static_cast<int64_t>(i) * gstride + p] - 1;
+      }
+#pragma unroll
+      for (int b = 0; b < KB; ++b) g[b] = (live && i0 + b < K) ? g[b] : -1;
+      if (C_in == 1) {
+        float xv[KB], wv[KB];
+#pragma unroll
+        for (int b = 0; b < KB; ++b) {
+          xv[b] = g[b] >= 0 ? ElemIO<TIn>::load(x, g[b]) : 0.0f;
+          wv[b] = i0 + b < K ? ElemIO<TIn>::load(w, w_index<WT>(i0 + b, K, 0, col, 1, C_out))
+                             : 0.0f;
+        }
+#pragma unroll
+        for (int b = 0; b < KB; ++b)
+          if (g[b] >= 0) acc = fmaf(xv[b], wv[b], acc);
+      } else {
+#pragma unroll
+        for (int b = 0; b < KB; ++b) {
+          if (g[b] < 0) continue;
+          const int64_t xb = static_cast<int64_t>(g[b]) * C_in;
+          for (int c = 0; c < C_in; ++c)
+            acc = fmaf(ElemIO<TIn>::load(x, xb + c),
+                       ElemIO<TIn>::load(w, w_index<WT>(i0 + b, K, c, col, C_in, C_out)), acc);
+        }
+      }
     }
+    if (!live) continue;
     const int64_t o = static_cast<int64_t>(perm[p]) * C_out + col;
     if (epi.scale)
       acc = fmaf(acc, epi.scale[col], bias ? bias[col] : 0.0f);
@@ -115,6 +185,93 @@ __global__ __launch_bounds__(256) void k_fwd_vec(
     if (epi.res) acc += ElemIO<TOut>::load(static_cast<const TOut*>(epi.res), o);
     if (epi.relu) acc = acc < 0.0f ? 0.0f : acc;
     ElemIO<TOut>::store(y, o, acc);
+  }
+}
+
+// Few input planes (C_in <= kLowCin, C_out a multiple of kLowCols): one
+// thread per output position and kLowCols output columns, a block of threads
+// on one column group.  The gather-map entries and input values of 16 offsets
+// at a time are loaded together into registers; meanwhile the block stages
+// those offsets' weights of its columns in LDS, which every lane then reads
+// at the same address (a broadcast).  Same per-element summation order as
+// k_fwd_vec.
+constexpr int kLowCin = 4;
+constexpr int kLowCols = 16;
+template <typename TIn, typename TOut, int WT>
+__global__ __launch_bounds__(256) void k_fwd_lowc(
+    const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
+    int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
+    const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
+    int C_out, uint32_t x_bytes, Epilogue epi) {
+  constexpr int KB = 16;
+  __shared__ float s_w[KB][kLowCin][kLowCols];
+  const int64_t p = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+  const int n0 = blockIdx.y * kLowCols;           // first column of the block
+  const __amdgpu_buffer_rsrc_t xr = buf_rsrc(x, x_bytes);
+  const bool live = p < n_cap && p < hdr->n_out;
+  const int64_t pc = p < n_cap ? p : 0;           // a position the map holds
+  // the output row and the epilogue's per-column values, loaded up front
+  const int64_t o = static_cast<int64_t>(perm[pc]) * C_out;
+  float sc[kLowCols], sh[kLowCols];
+#pragma unroll
+  for (int n = 0; n < kLowCols; ++n) {
+    sc[n] = epi.scale ? epi.scale[n0 + n] : 1.0f;
+    sh[n] = bias ? bias[n0 + n] : 0.0f;
+  }
+  float acc[kLowCols];
+#pragma unroll
+  for (int n = 0; n < kLowCols; ++n) acc[n] = 0.0f;
+  for (int i0 = 0; i0 < K; i0 += KB) {
+    int32_t g[KB];
+    load_map<KB>(gmap, gstride, K, i0, pc, g);
+    float xv[KB][kLowCin];
+#pragma unroll
+    for (int b = 0; b < KB; ++b)
+#pragma unroll
+      for (int c = 0; c < kLowCin; ++c) {
+        xv[b][c] = 0.0f;
+        if (c < C_in && i0 + b < K) {             // block-uniform
+          const uint32_t off = (live && g[b] >= 0)
+                                   ? (static_cast<uint32_t>(g[b]) * C_in + c) * BufIO<TIn>::kSize
+                                   : kBufOOB;
+          xv[b][c] = BufIO<TIn>::load(xr, off);
+        }
+      }
+    if (i0 > 0) __syncthreads();                  // the last batch's weights are read
+    for (int e = threadIdx.x; e < KB * kLowCin * kLowCols; e += blockDim.x) {
+      const int b = e / (kLowCin * kLowCols), c = (e / kLowCols) % kLowCin, n = e % kLowCols;
+      s_w[b][c][n] = (i0 + b < K && c < C_in)
+                         ? ElemIO<TIn>::load(w, w_index<WT>(i0 + b, K, c, n0 + n, C_in, C_out))
+                         : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < KB; ++b) {
+      if (i0 + b < K) {
+        const bool has = live && g[b] >= 0;
+#pragma unroll
+        for (int c = 0; c < kLowCin; ++c) {
+          if (c < C_in) {
+#pragma unroll
+            for (int n = 0; n < kLowCols; ++n)
+              acc[n] = has ? fmaf(xv[b][c], s_w[b][c][n], acc[n]) : acc[n];
+          }
+        }
+      }
+    }
+  }
+  if (!live) return;
+#pragma unroll
+  for (int n = 0; n < kLowCols; ++n) {
+    const int col = n0 + n;
+    float v = acc[n];
+    if (epi.scale)
+      v = fmaf(v, sc[n], sh[n]);
+    else if (bias)
+      v += sh[n];
+    if (epi.res) v += ElemIO<TOut>::load(static_cast<const TOut*>(epi.res), o + col);
+    if (epi.relu) v = v < 0.0f ? 0.0f : v;
+    ElemIO<TOut>::store(y, o + col, v);
   }
 }
 
@@ -572,9 +729,14 @@ constexpr int rows_blocks() { return NCH <= 2 ? 4 : (NCH <= 4 ? 2 : 1); }
 
 using Call = FwdCall;
 
-template <typename TIn, int NCH, int NCB, typename TOut, int WT>
-void launch_mfma(const Call& c) {
-  constexpr int RB = rows_blocks<NCH>();
+// Tiles of fewer rows (one 16-row block per wave) when a layer is too small
+// to give every compute unit two tiles of the usual size: a 64-row tile per
+// workgroup keeps all of them busy on small layers (filters other than the
+// unrolled 3^3 / 2^3 / 1^d ones).
+constexpr int64_t kSmallLayerTiles = 512;
+
+template <typename TIn, int NCH, int NCB, typename TOut, int WT, int RB, bool SMALL = false>
+void launch_mfma_rb(const Call& c) {
   constexpr int kTileRows = 4 * RB * 16;
   const int64_t ntiles = (c.v.n_cap + kTileRows - 1) / kTileRows;
   const int64_t per = (ntiles + 7) / 8;
@@ -585,21 +747,40 @@ void launch_mfma(const Call& c) {
   // blocks take one offset only) also skip the blocks' gathers.
   // Single-offset views (f = s transposed runs, 1^d filters) unroll to one
   // step with a third of the registers, so more workgroups share a CU.
-  auto kern = c.v.K == 27  ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
-              : c.v.K == 1 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 1, true, WT>
-              : c.v.K == 8 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 8, true, WT, true>
-                           : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
+  auto kern = k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true>;
+  if constexpr (!SMALL) {
+    kern = c.v.K == 27  ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT>
+           : c.v.K == 1 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 1, true, WT>
+           : c.v.K == 8 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 8, true, WT, true>
+                        : kern;
+  }
   // The block epilogue (scale / residual / ReLU) is compiled into its own
   // kernels, so that the plain forward keeps its register count.
   if constexpr (WT == 0) {
-    if (c.epi.scale || c.epi.res || c.epi.relu)
-      kern = c.v.K == 27 ? k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT, false, true>
-                         : k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true, true>;
+    if (c.epi.scale || c.epi.res || c.epi.relu) {
+      kern = k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 0, true, WT, true, true>;
+      if constexpr (!SMALL)
+        if (c.v.K == 27) kern = k_fwd_mfma<TIn, NCH, NCB, RB, TOut, 27, true, WT, false, true>;
+    }
   }
   kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), c.x_bytes, static_cast<const TIn*>(c.w), c.bias,
       static_cast<TOut*>(c.y), c.C_out, ntiles, c.v.seg, c.epi);
+}
+
+template <typename TIn, int NCH, int NCB, typename TOut, int WT>
+void launch_mfma(const Call& c) {
+  constexpr int RB = rows_blocks<NCH>();
+  const bool generic_k = c.v.K != 27 && c.v.K != 1 && c.v.K != 8;
+  const int64_t tiles = (c.v.n_cap + 4 * RB * 16 - 1) / (4 * RB * 16);
+  if constexpr (RB > 1) {
+    if (generic_k && !c.v.seg && tiles < kSmallLayerTiles) {
+      launch_mfma_rb<TIn, NCH, NCB, TOut, WT, 1, true>(c);
+      return;
+    }
+  }
+  launch_mfma_rb<TIn, NCH, NCB, TOut, WT, RB>(c);
 }
 
 template <typename TIn, int NCH, typename TOut, int WT>
@@ -648,9 +829,36 @@ void launch_vec(const Call& c, int C_in) {
   if (blocks > 65536) blocks = 65536;
   if (blocks < 1) blocks = 1;
   k_fwd_vec<TIn, TOut, WT><<<static_cast<unsigned>(blocks), 256, 0, c.stream>>>(
-      c.v.gmap, c.v.perm, c.v.gstride, c.v.hdr, static_cast<int>(c.v.K),
+      c.v.gmap, c.v.perm, c.v.gstride, c.v.n_cap, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), static_cast<const TIn*>(c.w), c.bias, static_cast<TOut*>(c.y),
       C_in, c.C_out, c.epi);
+}
+
+template <typename TIn, typename TOut, int WT>
+void launch_lowc(const Call& c, int C_in, uint32_t x_bytes) {
+  const dim3 grid(static_cast<unsigned>((c.v.n_cap + 255) / 256),
+                  static_cast<unsigned>((c.C_out + kLowCols - 1) / kLowCols));
+  k_fwd_lowc<TIn, TOut, WT><<<grid, 256, 0, c.stream>>>(
+      c.v.gmap, c.v.perm, c.v.gstride, c.v.n_cap, c.v.hdr, static_cast<int>(c.v.K),
+      static_cast<const TIn*>(c.x), static_cast<const TIn*>(c.w), c.bias, static_cast<TOut*>(c.y),
+      C_in, c.C_out, x_bytes, c.epi);
+}
+
+template <typename TIn, typename TOut, int WT>
+void launch_generic(const Call& c, int C_in) {
+  // one grid row of blocks per kLowCols columns (at most 65535), the inputs
+  // and one offset's map row addressable by a buffer resource (< 2^31 bytes).
+  // Below kLowMinRows positions the one-lane-per-column kernel finishes
+  // first (measured: 460 rows of 16 columns 6.1 us against 7.7 us; 29759
+  // rows of 32 columns 16.4 us against 12.7 us).
+  constexpr int64_t kLowMinRows = 2048;
+  const uint64_t xb = static_cast<uint64_t>(c.v.n_src) * C_in * sizeof(TIn);
+  if (C_in <= kLowCin && c.v.n_cap >= kLowMinRows && c.C_out % kLowCols == 0 &&
+      c.C_out / kLowCols <= 65535 &&
+      xb < kBufOOB && static_cast<uint64_t>(c.v.gstride) * 4 < kBufOOB)
+    launch_lowc<TIn, TOut, WT>(c, C_in, static_cast<uint32_t>(xb));
+  else
+    launch_vec<TIn, TOut, WT>(c, C_in);
 }
 
 template <int WT>
@@ -663,13 +871,13 @@ bool run(const Call& c, int in_dt, int out_dt, int C_in) {
   if (done) return true;
   if (c.v.seg) return false;               // segmented views run on the matrix cores only
   if (in_dt == SPCONV_F32 && out_dt == SPCONV_F32)
-    launch_vec<float, float, WT>(c, C_in);
+    launch_generic<float, float, WT>(c, C_in);
   else if (in_dt == SPCONV_F32)
-    launch_vec<float, uint16_t, WT>(c, C_in);
+    launch_generic<float, uint16_t, WT>(c, C_in);
   else if (out_dt == SPCONV_F32)
-    launch_vec<uint16_t, float, WT>(c, C_in);
+    launch_generic<uint16_t, float, WT>(c, C_in);
   else
-    launch_vec<uint16_t, uint16_t, WT>(c, C_in);
+    launch_generic<uint16_t, uint16_t, WT>(c, C_in);
   return true;
 }
 

@@ -38,6 +38,7 @@
 //   and the sort), and probe / scan / compact on input site s*y + o.
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -190,6 +191,267 @@ __global__ void k_init_header(DeviceHeader* h, int64_t n_out) {
     h->status = 0;
     h->pad = 0;
     h->n_out = n_out;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Small VSC layers (at most kSmallN sites on at most 2^kSmallCellBits cells):
+// the whole build in one workgroup, one launch instead of the eight of the
+// grid path, whose launch latencies dominate a layer of a few hundred sites.
+// Cells are numbered along the Z-order curve (sample on top, then the
+// coordinates' bits level by level from the most significant, coordinate 1
+// first inside a level); an occupancy bitmap over those cells sits in LDS,
+// and the exclusive popcount prefix of its words ranks every occupied cell,
+// which is the site's schedule position.  A neighbour lookup is one bit test
+// plus that rank.  One wave per (offset, 64 positions) counts the chunk's
+// pairs, a block scan of the counts in (offset, chunk) order places every
+// chunk's first pair (and so R_i's offset and the bases of its 256-position
+// blocks), and a second pass over the chunks writes G and the pairs.
+// ---------------------------------------------------------------------------
+constexpr int kSmallN = 2048;
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallCellBits = 18;
+constexpr int kSmallWords = (1 << kSmallCellBits) / 32;
+constexpr int kSmallK = 128;      // filter offsets (at most 125 = 5^3)
+
+// Coordinate v (< 2^(kSmallCellBits / d)) spread to every d-th bit, d = 1, 2, 3.
+__device__ __forceinline__ uint32_t spread_bits(uint32_t v, int d) {
+  uint32_t x = v;
+  if (d == 2) {
+    x = (x | (x << 8)) & 0x00ff00ffu;
+    x = (x | (x << 4)) & 0x0f0f0f0fu;
+    x = (x | (x << 2)) & 0x33333333u;
+    x = (x | (x << 1)) & 0x55555555u;
+  } else if (d == 3) {
+    x = (x | (x << 16)) & 0xff0000ffu;
+    x = (x | (x << 8)) & 0x0300f00fu;
+    x = (x | (x << 4)) & 0x030c30c3u;
+    x = (x | (x << 2)) & 0x09249249u;
+  }
+  return x;
+}
+
+// Z-order cell of site c (c[0] = sample, c[1..D-1] in range): the spatial
+// bits interleaved with coordinate 1 on top inside a level, the sample above
+// the sbits spatial bits.
+template <int D>
+__device__ __forceinline__ uint32_t zcell(const int32_t* c, int sbits) {
+  constexpr int d = D - 1;
+  uint32_t z = 0;
+#pragma unroll
+  for (int j = 1; j < D; ++j) z |= spread_bits(static_cast<uint32_t>(c[j]), d) << (D - 1 - j);
+  return (static_cast<uint32_t>(c[0]) << sbits) | z;
+}
+
+// Moves cell z by a signed offset along the dimension whose bits are m, by
+// dilated-integer arithmetic: the field gains (or loses) dz, the spread
+// offset, modulo its 2^B values, and the other fields keep their bits.
+__device__ __forceinline__ uint32_t zmove(uint32_t z, uint32_t m, uint32_t dz, bool neg) {
+  const uint32_t f = neg ? (z & m) - dz : (z | ~m) + dz;
+  return (z & ~m) | (f & m);
+}
+
+// The cells are numbered with B bits per spatial coordinate, 2^B at least
+// extent + (f - 1) / 2 in every dimension, so a neighbour off the grid wraps
+// (modulo 2^B) onto a cell past the extent, which no site occupies: no range
+// test is needed on the way to the occupancy bit.
+template <int D>
+__global__ __launch_bounds__(kSmallThreads) void k_build_small(
+    const int32_t* __restrict__ coords, int N, int sbits, int nwords, OffsetTable ot, Extents E,
+    int32_t* __restrict__ out_coords, int32_t* __restrict__ perm, int32_t* __restrict__ gmap,
+    int64_t gstride, int32_t* __restrict__ blk_base, int64_t nblk, int64_t* __restrict__ totals,
+    int64_t* __restrict__ pair_off, int2* __restrict__ pairs, DeviceHeader* __restrict__ hdr) {
+  constexpr int d = D - 1;
+  constexpr int PER = kSmallN / kSmallThreads;     // sites per thread
+  constexpr int WPT = kSmallWords / kSmallThreads;  // bitmap words per thread in the scan
+  constexpr int NW = kSmallThreads / kWave;
+  constexpr int CPT = kSmallK * (kSmallN / kWave) / kSmallThreads;   // chunk counts per thread
+  __shared__ uint32_t s_bits[kSmallWords];
+  __shared__ uint16_t s_pre[kSmallWords];
+  __shared__ int32_t s_row[kSmallN];               // schedule position -> row
+  __shared__ uint32_t s_z[kSmallN];                // schedule position -> cell
+  __shared__ uint32_t s_dz[kSmallK][kMaxD];        // spread |o_j| of offset i
+  __shared__ uint32_t s_neg[kSmallK];              // bit j: o_j < 0
+  __shared__ int32_t s_cnt[kSmallK * (kSmallN / kWave)];   // pairs per (offset, 64 positions)
+  __shared__ int32_t s_wsum[NW];
+  __shared__ uint32_t s_status;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave;
+  const int lane = lane_id();
+  const int B = sbits / d;
+  uint32_t m[kMaxD] = {0, 0, 0, 0};                // bits of spatial coordinate j
+#pragma unroll
+  for (int j = 1; j < D; ++j) m[j] = spread_bits((1u << B) - 1u, d) << (D - 1 - j);
+  for (int w = tid; w < nwords; w += kSmallThreads) s_bits[w] = 0;
+  for (int p = tid; p < kSmallN; p += kSmallThreads) {
+    s_row[p] = 0;
+    s_z[p] = 0;
+  }
+  for (int i = tid; i < ot.K; i += kSmallThreads) {
+    int rem = i;
+    uint32_t neg = 0;
+#pragma unroll
+    for (int j = D - 1; j >= 0; --j) {
+      const int o = rem % ot.f[j] - ot.r[j];
+      rem /= ot.f[j];
+      s_dz[i][j] = j > 0 ? spread_bits(static_cast<uint32_t>(o < 0 ? -o : o), d) << (D - 1 - j) : 0u;
+      neg |= static_cast<uint32_t>(o < 0) << j;
+    }
+    s_neg[i] = neg;
+  }
+  if (tid == 0) s_status = 0;
+  __syncthreads();
+  // Block-wide exclusive scan of one value per thread; *total = the sum.
+  auto block_scan = [&](int v, int* total) {
+    const int inc = wave_incl_scan(v);
+    if (lane == kWave - 1) s_wsum[wave] = inc;
+    __syncthreads();
+    int ex = inc - v, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      if (w < wave) ex += s_wsum[w];
+      tot += s_wsum[w];
+    }
+    __syncthreads();
+    *total = tot;
+    return ex;
+  };
+  // 1. every site sets its cell's bit (a bit already set: a duplicate site;
+  // a coordinate out of range: status, and no cell)
+  uint32_t cell[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int p = tid + u * kSmallThreads;
+    cell[u] = ~0u;
+    if (p < N) {
+      int32_t c[kMaxD] = {0, 0, 0, 0};
+      bool ok = true;
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        c[j] = coords[static_cast<int64_t>(p) * D + j];
+        out_coords[static_cast<int64_t>(p) * D + j] = c[j];
+        ok = ok && c[j] >= 0 && c[j] < E.e[j];
+      }
+      if (ok) {
+        cell[u] = zcell<D>(c, sbits);
+        const uint32_t bit = 1u << (cell[u] & 31);
+        if (atomicOr(&s_bits[cell[u] >> 5], bit) & bit) atomicOr(&s_status, kStDup);
+      } else {
+        atomicOr(&s_status, kStRange);
+      }
+    }
+  }
+  __syncthreads();
+  // 2. exclusive prefix of the words' popcounts (each thread WPT words)
+  {
+    uint32_t cnt[WPT];
+    int sum = 0;
+#pragma unroll
+    for (int k = 0; k < WPT; ++k) {
+      const int w = tid * WPT + k;
+      cnt[k] = w < nwords ? __popc(s_bits[w]) : 0u;
+      sum += static_cast<int>(cnt[k]);
+    }
+    int tot;
+    int ex = block_scan(sum, &tot);
+#pragma unroll
+    for (int k = 0; k < WPT; ++k) {
+      const int w = tid * WPT + k;
+      if (w < nwords) s_pre[w] = static_cast<uint16_t>(ex);
+      ex += static_cast<int>(cnt[k]);
+    }
+  }
+  __syncthreads();
+  // 3. the rank of a site's cell is its schedule position
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    if (cell[u] == ~0u) continue;
+    const uint32_t w = cell[u] >> 5;
+    const int pos = s_pre[w] + __popc(s_bits[w] & ((1u << (cell[u] & 31)) - 1u));
+    s_row[pos] = tid + u * kSmallThreads;
+    s_z[pos] = cell[u];
+  }
+  __syncthreads();
+  for (int p = tid; p < N; p += kSmallThreads) perm[p] = s_row[p];
+  // Neighbour of schedule position p at offset i: 1 + its row, 0 if none.
+  // With RANK false only whether there is one (0 / 1).
+  auto neighbour = [&](int p, int i, auto rank) -> int32_t {
+    uint32_t z = s_z[p];
+    const uint32_t neg = s_neg[i];
+#pragma unroll
+    for (int j = 1; j < D; ++j) z = zmove(z, m[j], s_dz[i][j], (neg >> j) & 1u);
+    const uint32_t word = s_bits[z >> 5];
+    const uint32_t bit = 1u << (z & 31);
+    if (!(word & bit)) return 0;
+    if constexpr (!decltype(rank)::value) return 1;
+    else return s_row[s_pre[z >> 5] + __popc(word & (bit - 1u))] + 1;
+  };
+  // Visits the (offset, chunk of 64 positions) tasks of nchunk chunks per
+  // offset, wave by wave in steps of NW, without a division per task.
+  auto for_tasks = [&](int nchunk, auto fn) {
+    if (nchunk == 0) return;
+    int i = wave / nchunk, c = wave % nchunk;
+    for (; i < ot.K;) {
+      fn(i, c);
+      c += NW;
+      while (c >= nchunk) {
+        c -= nchunk;
+        ++i;
+      }
+    }
+  };
+  // 4. pairs per (offset, chunk of 64 positions), one wave per chunk
+  const int nch = (N + kWave - 1) / kWave;
+  const int ntask = ot.K * nch;
+  for_tasks(nch, [&](int i, int c) {
+    const int p = c * kWave + lane;
+    const bool hit = p < N && neighbour(p, i, std::false_type{});
+    const int n = __popcll(__ballot(hit));
+    if (lane == 0) s_cnt[i * nch + c] = n;
+  });
+  __syncthreads();
+  // 5. exclusive scan of the chunk counts in (offset, chunk) order: the first
+  // pair of every chunk
+  int tot;
+  {
+    int v[CPT], sum = 0;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int t = tid * CPT + k;
+      v[k] = t < ntask ? s_cnt[t] : 0;
+      sum += v[k];
+    }
+    int ex = block_scan(sum, &tot);
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int t = tid * CPT + k;
+      if (t < ntask) s_cnt[t] = ex;
+      ex += v[k];
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < ot.K; i += kSmallThreads) {
+    const int first = s_cnt[i * nch];
+    pair_off[i] = first;
+    totals[i] = (i + 1 < ot.K ? s_cnt[(i + 1) * nch] : tot) - first;
+  }
+  for (int t = tid; t < ot.K * nblk; t += kSmallThreads) {
+    const int i = static_cast<int>(t / nblk), b = static_cast<int>(t % nblk);
+    blk_base[t] = s_cnt[i * nch + b * (kBlock / kWave)] - s_cnt[i * nch];
+  }
+  // 6. gather map (zeros up to the padded stride) and pairs, one wave per chunk
+  for_tasks(static_cast<int>(gstride / kWave), [&](int i, int c) {
+    const int p = c * kWave + lane;
+    const int32_t e = p < N ? neighbour(p, i, std::true_type{}) : 0;
+    gmap[static_cast<int64_t>(i) * gstride + p] = e;
+    const uint64_t mk = __ballot(e != 0);
+    if (e) pairs[s_cnt[i * nch + c] + prefix_popc(mk)] = make_int2(e - 1, s_row[p]);
+  });
+  if (tid == 0) {
+    pair_off[ot.K] = tot;
+    hdr->status = s_status;
+    hdr->pad = 0;
+    hdr->n_out = N;
   }
 }
 
@@ -504,22 +766,41 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
 }
 
 // Emit the marked output sites in rank order: coordinates and packed keys.
-// One bitmap word (32 cells) per thread, 256 words per block.
+// Block b works on bitmap block b / kEmitParts (256 words, whose rank base is
+// bbase[b / kEmitParts]) and, of it, the 32 words of part b % kEmitParts;
+// kEmitParts threads share a word, 32 / kEmitParts cells each, so a dense
+// word is not emitted by one thread in 32 serial steps.
+constexpr int kEmitParts = 8;
+constexpr int kEmitBits = 32 / kEmitParts;
 __global__ __launch_bounds__(kBlock) void k_sc_emit(
     const uint32_t* __restrict__ bitmap, uint64_t nwords, const uint32_t* __restrict__ bbase,
     Codec cout, Extents E, int32_t* __restrict__ out_coords,
     uint64_t* __restrict__ out_keys) {
-  const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
-  uint32_t word = w < nwords ? bitmap[w] : 0u;
-  uint32_t tot;
-  uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
+  __shared__ uint32_t s_pre[kBlock];
+  const uint64_t bw = blockIdx.x / kEmitParts;
+  const int part = blockIdx.x % kEmitParts;
+  {
+    // exclusive popcount prefix over the 256 words of the bitmap block
+    const uint64_t w = bw * kBlock + threadIdx.x;
+    uint32_t tot;
+    s_pre[threadIdx.x] = block_excl_scan<uint32_t>(w < nwords ? __popc(bitmap[w]) : 0u, &tot);
+  }
+  __syncthreads();
+  const int wi = part * (kBlock / kEmitParts) + threadIdx.x / kEmitParts;   // word in block
+  const int sub = threadIdx.x % kEmitParts;
+  const uint64_t w = bw * kBlock + wi;
+  if (w >= nwords) return;
+  const uint32_t full = bitmap[w];
+  const uint32_t below = (1u << (sub * kEmitBits)) - 1u;
+  uint32_t word = (full >> (sub * kEmitBits)) & ((1u << kEmitBits) - 1u);
   if (!word) return;
-  // coordinates of the word's first cell (one division per dimension); a set
-  // bit b adds b to the last coordinate, carried into the others only when
-  // it passes the extent
+  uint32_t rank = bbase[bw] + s_pre[wi] + __popc(full & below);
+  // coordinates of the thread's first cell (one division per dimension); a
+  // set bit b adds b to the last coordinate, carried into the others only
+  // when it passes the extent
   int32_t y0[kMaxD];
   {
-    uint32_t L = static_cast<uint32_t>(w * 32);
+    uint32_t L = static_cast<uint32_t>(w * 32 + sub * kEmitBits);
     for (int j = cout.D - 1; j >= 0; --j) {
       y0[j] = static_cast<int32_t>(L % static_cast<uint32_t>(E.e[j]));
       L /= static_cast<uint32_t>(E.e[j]);
@@ -1330,7 +1611,7 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, rb->in_count, cin, ot, E, lex);
   k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
   k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1, nullptr);
-  k_sc_emit<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
+  k_sc_emit<<<static_cast<unsigned>(lnbw * kEmitParts), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
                                                                      rb->out_coords, nullptr);
   launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
                       cout, nullptr, false);
@@ -1360,8 +1641,47 @@ bool grid_build(spconv_rulebook rb) {
   return make_grid_geom(rb->D, rb->out_size, &go, &co);
 }
 
+// Whether a VSC build takes the one-workgroup path: a few sites on a few
+// cells (*sbits = spatial bits of a cell number, *nwords = bitmap words), a
+// site count known on the host (not a book chained on device counts), and no
+// site map forced by SPCONV_RULEBOOK (=small forces it where it applies).
+bool small_build(spconv_rulebook rb, int* sbits, int* nwords) {
+  const int64_t N = rb->n_in;
+  if (rb->in_count || N <= 0 || N > kSmallN || rb->K > kSmallK) return false;
+  int B = 0;                       // 2^B >= extent + (f - 1) / 2 in every dimension
+  for (int j = 1; j < rb->D; ++j) {
+    const int64_t span = int64_t{rb->size[j]} + (rb->f[j] - 1) / 2;
+    while ((int64_t{1} << B) < span) ++B;
+  }
+  if (B > kSmallCellBits) return false;
+  *sbits = (rb->D - 1) * B;
+  if (*sbits > kSmallCellBits) return false;
+  const uint64_t cells = static_cast<uint64_t>(rb->size[0]) << *sbits;
+  if (cells > (uint64_t{1} << kSmallCellBits)) return false;
+  *nwords = static_cast<int>((cells + 31) / 32);
+  if (const char* e = std::getenv("SPCONV_RULEBOOK")) return std::strcmp(e, "small") == 0;
+  return true;
+}
+
 int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   const int64_t N = rb->n_in;
+  int sbits = 0, nwords = 0;
+  if (small_build(rb, &sbits, &nwords)) {
+    Extents E{};
+    for (int j = 0; j < rb->D; ++j) E.e[j] = rb->size[j];
+    auto launch = [&](auto kern) {
+      kern<<<1, kSmallThreads, 0, rb->stream>>>(
+          coords, static_cast<int>(N), sbits, nwords, make_offsets(rb), E, rb->out_coords, rb->perm, rb->gmap,
+          rb->gstride, rb->blk_cnt, rb->nblk, rb->totals, rb->pair_off,
+          reinterpret_cast<int2*>(rb->pairs), rb->hdr);
+    };
+    switch (rb->D) {
+      case 2: launch(k_build_small<2>); break;
+      case 3: launch(k_build_small<3>); break;
+      default: launch(k_build_small<4>); break;
+    }
+    return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+  }
   GridGeom g;
   uint64_t cells = 0;
   if (N > 0 && make_grid_geom(rb->D, rb->size, &g, &cells) && use_grid(cells, N))
@@ -1421,7 +1741,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(tr.keys, N, nullptr, cin, ot, E, bitmap);
     k_bitsum<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(bitmap, nwords, bsum);
     k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1, nullptr);
-    k_sc_emit<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(
+    k_sc_emit<<<static_cast<unsigned>(nbw * kEmitParts), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
     launch_schedule(rb, out_keys, cout, &cv);
     launch_probe_scan_compact(rb, out_keys, cout, cin, tr);

@@ -172,6 +172,11 @@ GRAD_CASES = [
     ("dc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 64, 32, "bf16"),
     ("vsc", "surf", [1, 3, 3, 3], None, 32, 96, "bf16"),
     ("sc", "pen", [1, 2, 2], [1, 2, 2], 3, 5, "f32"),
+    # input gradients with at most 4 gradient planes on 16-column outputs
+    # (the few-input-plane kernel, transposed weights)
+    ("vsc", "pen", [1, 3, 3], None, 16, 2, "f32"),
+    ("sc", "pen", [1, 2, 2], [1, 2, 2], 32, 4, "bf16"),
+    ("dc", "pen", [1, 2, 2], [1, 2, 2], 3, 16, "f32"),
 ]
 
 
@@ -234,7 +239,8 @@ FUSED_CASES = [
     # kind, case, f, s, C_in, C_out, dtype, out dtype
     ("vsc", "surf", [1, 3, 3, 3], [1, 1, 1, 1], 64, 64, "bf16", "bf16"),
     ("vsc", "surf", [1, 3, 3, 3], [1, 1, 1, 1], 32, 32, "f32", "f32"),
-    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 1, 16, "f32", "f32"),        # vector path
+    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 1, 16, "f32", "f32"),        # few input planes
+    ("vsc", "pen", [1, 3, 3], [1, 1, 1], 3, 32, "bf16", "f32"),       # few input planes
     ("vsc", "pen", [1, 3, 3], [1, 1, 1], 16, 24, "bf16", "f32"),      # vector path
     ("vsc", "pen", [1, 3, 3], [1, 1, 1], 32, 32, "bf16", "bf16"),     # 2 column blocks
     ("sc", "surf", [1, 2, 2, 2], [1, 2, 2, 2], 32, 64, "bf16", "bf16"),

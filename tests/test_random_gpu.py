@@ -87,3 +87,79 @@ def test_random_fused_forward(seed):
                                       relu, _odt(out_dtype))
     rtol = RTOL_F32 if dtype == "f32" and out_dtype == "f32" else RTOL_BF16
     check_features(_to_np(y), zo, bound, rtol, "fused")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_small_vsc_build(monkeypatch, seed):
+    """The one-workgroup build of small VSC layers (SPCONV_RULEBOOK=small):
+    random extents, filters 1/3/5 per dimension, densities and channel
+    counts, at most 2048 sites on at most 2^18 cells of 2^B per dimension,
+    2^B >= extent + (f - 1) / 2 (the workgroup's capacity: 3 samples of
+    29^3, of 200^2), against the oracle (rule book bit for bit, forward
+    within the parity bounds)."""
+    rng = np.random.default_rng(5000 + seed)
+    D = int(rng.integers(2, 5))
+    ext = [1, 2, 3, 7, 16, 29] + ([64, 200] if D < 4 else [])
+    size = [int(rng.integers(1, 4))] + [int(rng.choice(ext)) for _ in range(D - 1)]
+    f = [1] + [int(rng.choice([1, 3, 3, 5])) for _ in range(D - 1)]
+    c = dense_ref.random_sites(rng, size, float(rng.choice([0.01, 0.1, 0.5, 1.0])))
+    if len(c) == 0:
+        c = np.array([[int(rng.integers(0, e)) for e in size]], np.int32)
+    if len(c) > 2048:
+        c = c[np.sort(rng.choice(len(c), 2048, replace=False))]
+    ci, co = CHANNELS[int(rng.integers(0, len(CHANNELS)))]
+    dtype = "bf16" if (ci % 32 == 0 and rng.random() < 0.5) else "f32"
+    monkeypatch.setenv("SPCONV_RULEBOOK", "small")
+    _say(f"[small {seed}] N={len(c)}")
+    compare_layer(spc.VSC, c, size, f, [1] * D, ci, co, dtype=dtype, seed=seed,
+                  what=f"small {seed}")
+
+
+def test_small_build_errors_and_boundary(monkeypatch):
+    """Duplicates and out-of-range sites through the small build, and a layer
+    of exactly 2048 sites (the largest it takes) next to one of 2049 (which
+    takes the grid path)."""
+    from tests.test_parity_gpu import _t
+    import oracle
+    monkeypatch.setenv("SPCONV_RULEBOOK", "small")
+    dup = np.array([[0, 3, 4], [0, 5, 5], [0, 3, 4]], np.int32)
+    with pytest.raises(spc.SpconvError) as e:
+        spc.build_rulebook(spc.VSC, _t(dup), [1, 8, 8], [1, 3, 3])
+    assert e.value.status == spc.EDUP
+    oor = np.array([[0, 3, 4], [0, 8, 5]], np.int32)
+    with pytest.raises(spc.SpconvError) as e:
+        spc.build_rulebook(spc.VSC, _t(oor), [1, 8, 8], [1, 3, 3])
+    assert e.value.status == spc.ERANGE == oracle.status_of_build(oracle.VSC, oor, [1, 8, 8],
+                                                                   [1, 3, 3])
+    rng = np.random.default_rng(3)
+    full = dense_ref.random_sites(rng, [2, 64, 64], 0.5)
+    for n in (2048, 2049):
+        c = full[np.sort(rng.choice(len(full), n, replace=False))]
+        compare_layer(spc.VSC, c, [2, 64, 64], [1, 3, 3], [1, 1, 1], 16, 16, seed=n,
+                      what=f"boundary {n}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_few_input_planes(seed):
+    """Layers of 1-4 input planes and 16/32/48 output planes on at least
+    2048 input sites (where the output count is as large: the
+    one-lane-per-16-columns kernel), f32 and bf16, VSC and SC, against the
+    oracle."""
+    rng = np.random.default_rng(7000 + seed)
+    D = int(rng.integers(3, 5))
+    kind = int(rng.integers(0, 2))
+    ext = [24, 31, 40] if D == 4 else [64, 80, 96]
+    size = [int(rng.integers(1, 3))] + [int(rng.choice(ext)) for _ in range(D - 1)]
+    if kind == spc.VSC:
+        f, s = [1] + [3] * (D - 1), [1] * D
+    else:
+        f, s = [1] + [2] * (D - 1), [1] + [int(rng.choice([1, 2]))] * (D - 1)
+    c = dense_ref.random_sites(rng, size, 0.5 if D == 3 else 0.08)
+    ci = int(rng.integers(1, 5))
+    co = int(rng.choice([16, 32, 48]))
+    dtype = "bf16" if rng.random() < 0.5 else "f32"
+    out_dtype = dtype if rng.random() < 0.5 else ("f32" if dtype == "bf16" else "bf16")
+    _say(f"[few planes {seed}] N={len(c)}")
+    assert len(c) >= 2048
+    compare_layer(kind, c, size, f, s, ci, co, dtype=dtype, out_dtype=out_dtype, seed=seed,
+                  what=f"few planes {seed}")
