@@ -410,32 +410,38 @@ def run_stack(a, wl, torch, dev, lib, _lib, inputs):
                    "query")
         return n_out.value
 
+    # per-layer arguments that do not change from step to step
+    size0 = np.array(wl.spatial_size, np.int32)
+    largs = []
+    for j, L in enumerate(wl.layers):
+        f = np.array([1] + [L.f] * wl.d, np.int32)
+        s = np.array([1] + [L.s] * wl.d, np.int32)
+        wt, bt = params[j]
+        largs.append((f, s, f.ctypes.data, s.ctypes.data,
+                      _lib.VSC if L.kind == "vsc" else _lib.SC,
+                      _lib.BUILD_ASYNC if (chain or L.kind == "vsc") else 0,
+                      lib.spconv_vsc_forward if L.kind == "vsc" else lib.spconv_sc_forward,
+                      ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(bt.data_ptr())))
+    coords0 = ctypes.c_void_p(ct.data_ptr())
+
     def step(record=False):
-        coords, N = ctypes.c_void_p(ct.data_ptr()), N0
-        size = np.array(wl.spatial_size, np.int32)
+        coords, N, size = coords0, N0, size0
         x, rb, parent, handles = x0, None, None, []
         for j, L in enumerate(wl.layers):
-            wt, bt = params[j]
-            f = np.array([1] + [L.f] * wl.d, np.int32)
-            s = np.array([1] + [L.s] * wl.d, np.int32)
-            kind = _lib.VSC if L.kind == "vsc" else _lib.SC
+            _, _, fp, spp, kind, flags, fwd, wp, bp = largs[j]
             h = rb if L.kind == "vsc" else None
             if h is None:
                 h = ctypes.c_void_p()
-                flags = _lib.BUILD_ASYNC if (chain or L.kind == "vsc") else 0
                 if chain and parent is not None:
-                    _lib.check(lib.spconv_build_rulebook_on(parent, kind, f.ctypes.data,
-                                                            s.ctypes.data, flags, sp,
+                    _lib.check(lib.spconv_build_rulebook_on(parent, kind, fp, spp, flags, sp,
                                                             ctypes.byref(h)), "build on")
                 else:
                     _lib.check(lib.spconv_build_rulebook(kind, D, coords, N, size.ctypes.data,
-                                                         f.ctypes.data, s.ctypes.data, flags, sp,
+                                                         fp, spp, flags, sp,
                                                          ctypes.byref(h)), "build")
                 handles.append(h)
             y = torch.empty((rows_out(h), L.c_out), dtype=tdt, device=dev)
-            fwd = lib.spconv_vsc_forward if L.kind == "vsc" else lib.spconv_sc_forward
-            _lib.check(fwd(h, dt_code, ctypes.c_void_p(x.data_ptr()),
-                           ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(bt.data_ptr()),
+            _lib.check(fwd(h, dt_code, ctypes.c_void_p(x.data_ptr()), wp, bp,
                            dt_code, ctypes.c_void_p(y.data_ptr()), L.c_in, L.c_out, sp),
                        "forward")
             if L.kind == "vsc":

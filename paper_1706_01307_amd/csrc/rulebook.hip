@@ -893,12 +893,16 @@ __device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* 
 // Optionally copies the coordinates (VSC output sites) and writes packed
 // keys (SC marking).  With `count` set, only the first *count (<= N) rows
 // exist.
+// With `bitmap` set, the cell's occupancy bit is set too (the bitmap cleared
+// with the grid) and cellrow[r] receives r's cell (~0: out of range), for the
+// one-workgroup ranking of small grids.
 template <bool CAS>
 __global__ __launch_bounds__(kBlock) void k_grid_scatter(
     const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
     GridGeom g, uint32_t* __restrict__ grid, int32_t* __restrict__ copy_out, Codec ckey,
     uint64_t* __restrict__ keys_out, uint32_t* __restrict__ status,
-    int64_t* __restrict__ count_copy) {
+    int64_t* __restrict__ count_copy, uint32_t* __restrict__ bitmap,
+    uint32_t* __restrict__ cellrow) {
   const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   if (count_copy && r == 0) *count_copy = *count;   // the book's own copy of the row count
   if (r >= N || (count && r >= *count)) return;
@@ -911,11 +915,16 @@ __global__ __launch_bounds__(kBlock) void k_grid_scatter(
   }
   if (!ok) {
     if (keys_out) keys_out[r] = kEmpty;
+    if (cellrow) cellrow[r] = ~0u;
     atomicOr(status, kStRange);
     return;
   }
   if (keys_out) keys_out[r] = pack_site(ckey, x);
   const uint32_t cell = grid_cell(g, x);
+  if (bitmap) {
+    atomicOr(&bitmap[cell >> 5], 1u << (cell & 31));
+    cellrow[r] = cell;
+  }
   if (!CAS)
     grid[cell] = static_cast<uint32_t>(r + 1);
   else if (atomicCAS(&grid[cell], 0u, static_cast<uint32_t>(r + 1)) != 0u)
@@ -984,6 +993,95 @@ __global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict
 #pragma unroll
   for (int k = 0; k < 32; ++k)
     if ((word >> k) & 1u) perm[rank++] = static_cast<int32_t>(v[k]) - 1;
+}
+
+// Small grids (at most kRankWords bitmap words, at most kRankRows rows): one
+// workgroup replaces the bitmap, block-sum, scan and emit launches.  The
+// bitmap (set by the scatter) is ranked by a popcount prefix in LDS, every
+// thread taking a run of ceil(words / threads) words; then every row finds
+// its cell's rank, which is its schedule position.  The schedule is gathered
+// in LDS, kRankStage positions per pass, and stored in order: one compute
+// unit storing rows to scattered positions would spend a cycle per lane.
+// n_out = the occupied cells; a count other than `expect` (when >= 0), or
+// than *expect_dev (when given), flags duplicate sites.
+constexpr int kRankThreads = 1024;
+constexpr int kRankWords = 8192;
+constexpr int64_t kRankRows = 65535;
+constexpr int kRankStage = 24576;
+__global__ __launch_bounds__(kRankThreads) void k_grid_rank(
+    const uint32_t* __restrict__ bitmap, int nwords, const uint32_t* __restrict__ cellrow,
+    int64_t N, const int64_t* __restrict__ count, DeviceHeader* __restrict__ hdr, int64_t expect,
+    const int64_t* __restrict__ expect_dev, int32_t* __restrict__ perm) {
+  constexpr int WPT = kRankWords / kRankThreads;   // at most; wpt words per thread in fact
+  constexpr int NW = kRankThreads / kWave;
+  constexpr int RB = 16;                            // rows per thread in flight
+  __shared__ uint32_t s_bits[kRankWords];
+  __shared__ uint16_t s_pre[kRankWords];
+  __shared__ int32_t s_perm[kRankStage];
+  __shared__ uint32_t s_wsum[NW];
+  const int tid = threadIdx.x, wave = tid / kWave;
+  const int wpt = (nwords + kRankThreads - 1) / kRankThreads;
+  uint32_t cnt[WPT], sum = 0;
+  uint32_t v[WPT];
+#pragma unroll
+  for (int k = 0; k < WPT; ++k) {           // every load in flight at once (no branch)
+    const int w = tid * wpt + k;
+    v[k] = bitmap[w < nwords ? w : nwords - 1];
+  }
+#pragma unroll
+  for (int k = 0; k < WPT; ++k) {
+    const int w = tid * wpt + k;
+    const bool mine = k < wpt && w < nwords;
+    if (mine) s_bits[w] = v[k];
+    cnt[k] = mine ? __popc(v[k]) : 0u;
+    sum += cnt[k];
+  }
+  const uint32_t inc = wave_incl_scan(sum);
+  if (lane_id() == kWave - 1) s_wsum[wave] = inc;
+  __syncthreads();
+  uint32_t ex = inc - sum, total = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if (w < wave) ex += s_wsum[w];
+    total += s_wsum[w];
+  }
+#pragma unroll
+  for (int k = 0; k < WPT; ++k) {
+    const int w = tid * wpt + k;
+    if (k < wpt && w < nwords) s_pre[w] = static_cast<uint16_t>(ex);
+    ex += cnt[k];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int64_t t = total;
+    if ((expect >= 0 && t != expect) || (expect_dev && t != *expect_dev))
+      atomicOr(&hdr->status, kStDup);
+    hdr->n_out = t;
+  }
+  const int64_t n = count ? *count : N;
+  for (uint32_t base = 0; base < total; base += kRankStage) {
+    for (int64_t r0 = 0; r0 < n; r0 += int64_t{RB} * kRankThreads) {
+      uint32_t cell[RB];
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {         // the batch's loads first
+        const int64_t r = r0 + u * kRankThreads + tid;
+        cell[u] = r < n ? cellrow[r] : ~0u;
+      }
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        if (cell[u] == ~0u) continue;
+        const uint32_t w = cell[u] >> 5;
+        const uint32_t pos = s_pre[w] + __popc(s_bits[w] & ((1u << (cell[u] & 31)) - 1u)) - base;
+        if (pos < static_cast<uint32_t>(kRankStage))
+          s_perm[pos] = static_cast<int32_t>(r0 + u * kRankThreads + tid);
+      }
+    }
+    __syncthreads();
+    const uint32_t m = total - base < static_cast<uint32_t>(kRankStage) ? total - base
+                                                                         : kRankStage;
+    for (uint32_t t = tid; t < m; t += kRankThreads) perm[base + t] = s_perm[t];
+    __syncthreads();
+  }
 }
 
 typedef uint32_t dw4 __attribute__((ext_vector_type(4)));
@@ -1471,25 +1569,38 @@ bool use_grid(uint64_t cells, int64_t N) {
 
 struct GridBufs {
   uint32_t* grid;     // [cells] 1 + row, 0 = empty
-  uint32_t* bitmap;   // [nwords] occupancy
+  uint32_t* bitmap;   // [nwords] occupancy (right after the grid)
   uint32_t* bsum;     // [nbw] occupied cells per 256 words, then their bases
+  uint32_t* cellrow;  // [rows] cell of every row, for a one-workgroup ranking; else NULL
   uint64_t nwords;
   int64_t nbw;
 };
 
-size_t grid_bytes(uint64_t cells) {
-  const uint64_t nwords = (cells + 31) / 32;
-  const uint64_t nbw = (nwords + kBlock - 1) / kBlock;
-  return align_up(cells * 4, 256) + align_up(nwords * 4, 256) + align_up(nbw * 4, 256);
+// Whether a grid of `cells` cells scheduled for at most `rows` rows is ranked
+// by one workgroup (k_grid_rank) rather than by three launches.
+bool rank_in_one(uint64_t cells, int64_t rows) {
+  if (const char* e = std::getenv("SPCONV_RULEBOOK"))
+    if (std::strcmp(e, "grid3") == 0) return false;    // test knob: the three-launch ranking
+  return (cells + 31) / 32 <= static_cast<uint64_t>(kRankWords) && rows <= kRankRows;
 }
 
-GridBufs take_grid(Carver* cv, uint64_t cells) {
+size_t grid_bytes(uint64_t cells, int64_t rows = -1) {
+  const uint64_t nwords = (cells + 31) / 32;
+  const uint64_t nbw = (nwords + kBlock - 1) / kBlock;
+  const size_t cr = rows >= 0 && rank_in_one(cells, rows) ? align_up(rows * 4, 256) : 0;
+  return align_up(cells * 4, 256) + align_up(nwords * 4, 256) + align_up(nbw * 4, 256) + cr;
+}
+
+// rows >= 0: the grid will be scheduled for at most that many rows.
+GridBufs take_grid(Carver* cv, uint64_t cells, int64_t rows = -1) {
   GridBufs b{};
   b.nwords = (cells + 31) / 32;
   b.nbw = static_cast<int64_t>((b.nwords + kBlock - 1) / kBlock);
   b.grid = cv->take<uint32_t>(cells);
   b.bitmap = cv->take<uint32_t>(b.nwords);
   b.bsum = cv->take<uint32_t>(static_cast<size_t>(b.nbw));
+  b.cellrow = rows >= 0 && rank_in_one(cells, rows)
+                  ? cv->take<uint32_t>(static_cast<size_t>(rows > 0 ? rows : 1)) : nullptr;
   return b;
 }
 
@@ -1500,18 +1611,30 @@ void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
                          const int64_t* count, const GridGeom& g, uint64_t cells,
                          const GridBufs& b, int32_t* copy_out, const Codec& ckey,
                          uint64_t* keys_out, bool cas, int64_t init_n = -1) {
-  launch_zero(b.grid, cells, rb->stream, init_n >= 0 ? rb->hdr : nullptr, init_n);
+  // with a one-workgroup ranking the scatter sets the bitmap as well, which
+  // lies right after the grid and is cleared with it
+  const uint64_t nclear =
+      b.cellrow ? static_cast<uint64_t>(b.bitmap + b.nwords - b.grid) : cells;
+  launch_zero(b.grid, nclear, rb->stream, init_n >= 0 ? rb->hdr : nullptr, init_n);
   auto kern = cas ? k_grid_scatter<true> : k_grid_scatter<false>;
   // a book on another book's outputs keeps its own copy of their count
   int64_t* cc = count && count == rb->in_count ? rb->n_in_dev : nullptr;
   kern<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out, ckey,
-                                               keys_out, &rb->hdr->status, cc);
+                                               keys_out, &rb->hdr->status, cc,
+                                               b.cellrow ? b.bitmap : nullptr, b.cellrow);
 }
 
 // Z-order schedule from the grid; also sets n_out to the number of occupied
 // cells, flagging duplicates when that is not `expect` (>= 0).
 void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
-                          int64_t expect, const int64_t* expect_dev = nullptr) {
+                          int64_t expect, const int64_t* expect_dev = nullptr,
+                          int64_t rows = 0, const int64_t* count = nullptr) {
+  if (b.cellrow) {
+    k_grid_rank<<<1, kRankThreads, 0, rb->stream>>>(b.bitmap, static_cast<int>(b.nwords),
+                                                    b.cellrow, rows, count, rb->hdr, expect,
+                                                    expect_dev, rb->perm);
+    return;
+  }
   k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
                                                                         b.bitmap, b.bsum);
   k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect, expect_dev);
@@ -1567,13 +1690,14 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
                    uint64_t cells) {
   const int64_t N = rb->n_in;
   void* mem = nullptr;
-  if (dev_alloc(rb, grid_bytes(cells) + 256, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
+  if (dev_alloc(rb, grid_bytes(cells, N) + 256, rb->stream, &mem) != SPCONV_OK)
+    return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
-  const GridBufs b = take_grid(&cv, cells);
+  const GridBufs b = take_grid(&cv, cells, N);
   // rows [0, N), or [0, *in_count) for a book on another book's outputs
   launch_grid_scatter(rb, coords, N, rb->in_count, g, cells, b, rb->out_coords, Codec{}, nullptr,
                       false, rb->in_count ? 0 : N);
-  launch_grid_schedule(rb, b, cells, rb->in_count ? -1 : N, rb->in_count);
+  launch_grid_schedule(rb, b, cells, rb->in_count ? -1 : N, rb->in_count, N, rb->in_count);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
   if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -1592,14 +1716,15 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   for (int j = 0; j < rb->D; ++j) lex_cells *= static_cast<uint64_t>(rb->out_size[j]);
   const uint64_t lwords = (lex_cells + 31) / 32;
   const int64_t lnbw = static_cast<int64_t>((lwords + kBlock - 1) / kBlock);
-  const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out) + align_up(lwords * 4, 256) +
+  const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out, rb->n_cap) +
+                       align_up(lwords * 4, 256) +
                        align_up(static_cast<size_t>(lnbw) * 4, 256) +
                        align_up(static_cast<size_t>(N) * 8, 256) + 256;
   void* mem = nullptr;
   if (dev_alloc(rb, bytes, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
   const GridBufs bi = take_grid(&cv, cells_in);
-  const GridBufs bo = take_grid(&cv, cells_out);
+  const GridBufs bo = take_grid(&cv, cells_out, rb->n_cap);
   uint32_t* lex = cv.take<uint32_t>(lwords);
   uint32_t* lsum = cv.take<uint32_t>(static_cast<size_t>(lnbw));
   uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
@@ -1611,11 +1736,11 @@ int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
   k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, rb->in_count, cin, ot, E, lex);
   k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
   k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1, nullptr);
-  k_sc_emit<<<static_cast<unsigned>(lnbw * kEmitParts), kBlock, 0, rb->stream>>>(lex, lwords, lsum, cout, E,
-                                                                     rb->out_coords, nullptr);
+  k_sc_emit<<<static_cast<unsigned>(lnbw * kEmitParts), kBlock, 0, rb->stream>>>(
+      lex, lwords, lsum, cout, E, rb->out_coords, nullptr);
   launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
                       cout, nullptr, false);
-  launch_grid_schedule(rb, bo, cells_out, -1);
+  launch_grid_schedule(rb, bo, cells_out, -1, nullptr, rb->n_cap, &rb->hdr->n_out);
   launch_probe_grid(rb, rb->out_coords, gi, bi, cells_in);
   if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;

@@ -76,7 +76,7 @@ def _forward(rb, x, w, C_out, out_rows):
     return fwd(rb, x, w, None, out=y)
 
 
-@pytest.mark.parametrize("path", ["grid", "hash"])
+@pytest.mark.parametrize("path", ["grid", "grid3", "hash"])
 @pytest.mark.parametrize("kind,f,s", [(spc.VSC, [1, 3, 3, 3], None),
                                       (spc.SC, [1, 2, 2, 2], [1, 2, 2, 2]),
                                       (spc.SC, [1, 3, 3, 3], [1, 2, 2, 2])])

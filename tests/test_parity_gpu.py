@@ -298,10 +298,12 @@ def _rulebook_case_sites(name):
     return dense_ref.random_sites(rng, size, 0.3), size
 
 
-@pytest.mark.parametrize("path", ["hash", "grid"])
+@pytest.mark.parametrize("path", ["hash", "grid", "grid3"])
 @pytest.mark.parametrize("case", range(len(RULEBOOK_CASES)))
 def test_rulebook_paths(monkeypatch, path, case):
-    """Hash-table and dense-grid rule books give the same (oracle) result."""
+    """Hash-table and dense-grid rule books give the same (oracle) result;
+    grid3 ranks a small grid's cells with the three-launch multi-block path
+    instead of one workgroup."""
     monkeypatch.setenv("SPCONV_RULEBOOK", path)
     kind, name, f, s, ci, co, dt = RULEBOOK_CASES[case]
     coords, size = _rulebook_case_sites(name)
