@@ -593,6 +593,393 @@ __global__ __launch_bounds__(kBlock) void k_probe(
   publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk, blk);
 }
 
+// ---------------------------------------------------------------------------
+// Sorted-brick site map (VSC layers on grids too large or too sparse for the
+// dense grid).  A site's cell is its Z-order code (the Morton code the
+// schedule sorts: sample on top, then the coordinates' bits level by level);
+// its lowest lb bits, levels 0 .. b-1, place it inside a brick, an aligned
+// block of 2^b_j cells along coordinate j.  In the sorted order the sites of
+// a brick are one run, so the runs number the occupied bricks in Z-order.  A
+// hash directory maps a brick (cell >> lb) to its number, inserted once per
+// brick (no two inserts of one key, hence no contention), and a pool holds
+// 2^lb entries per brick (1 + row, 0 = empty), bricks in Z-order: a compacted
+// Z-ordered grid.  A lookup is a pool load at the brick found in the
+// directory; a brick of side 2^b_j >= f_j - 1 lets the neighbours of a site
+// touch at most 2^d bricks, whose directory entries the probe fetches once
+// per site, all at once.
+// ---------------------------------------------------------------------------
+constexpr int kBrickK = 128;         // offsets the brick probe takes (5^3 = 125)
+constexpr int kBrickCells = 64;      // cells per brick, at most
+
+struct BrickMap {
+  ulonglong2* dir;       // directory slots: x = brick (kEmpty = free), y = brick number
+  uint64_t dslots;       // allocated slots (power of two)
+  int32_t* pool;         // [bricks][2^lb] 1 + row, 0 = empty
+  int lb;                // cell bits inside a brick
+  int D;
+  uint64_t M[kMaxD];     // cell bits of spatial coordinate j
+  uint64_t BM[kMaxD];    // brick-number bits of coordinate j (M[j] above lb, shifted down)
+  int32_t side[kMaxD];   // 2^b_j
+  const DeviceHeader* nbricks;   // n_out = occupied bricks (device)
+};
+
+// Directory size in use: a power of two >= 2 x bricks (at least 64) within
+// the allocation, so the table is at most half full.
+__device__ __forceinline__ uint64_t dir_mask(const BrickMap& m) {
+  const uint64_t need = 2 * static_cast<uint64_t>(m.nbricks->n_out);
+  const uint64_t want = need > 64 ? 1ull << (64 - __clzll(need - 1)) : 64;
+  return (want < m.dslots ? want : m.dslots) - 1;
+}
+
+// Slow path of a directory lookup: on from the slot after `sl` (the first
+// slot held another brick).
+__device__ __noinline__ int32_t dir_find_after(const BrickMap& m, uint64_t dmask, uint64_t sl,
+                                               uint64_t key) {
+  for (uint64_t t = 0; t < dmask; ++t) {
+    sl = (sl + 1) & dmask;
+    const ulonglong2 v = m.dir[sl];
+    if (v.x == key) return static_cast<int32_t>(v.y);
+    if (v.x == kEmpty) return -1;
+  }
+  return -1;
+}
+
+__device__ __forceinline__ uint64_t zmove64(uint64_t z, uint64_t m, uint64_t dz, bool neg) {
+  const uint64_t f = neg ? (z & m) - dz : (z | ~m) + dz;
+  return (z & ~m) | (f & m);
+}
+
+// Bits of v spread over the set bits of m, lowest first.
+__host__ __device__ inline uint64_t deposit64(uint64_t v, uint64_t m) {
+  uint64_t r = 0;
+  for (uint64_t bb = 1; m; bb <<= 1) {
+    const uint64_t low = m & (0ull - m);
+    if (v & bb) r |= low;
+    m &= m - 1;
+  }
+  return r;
+}
+
+// Packed key of input row r (kEmpty: out of range), the coordinates copied.
+__global__ __launch_bounds__(kBlock) void k_site_keys(
+    const int32_t* __restrict__ coords, int64_t N, Codec c, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ copy_out, uint32_t* __restrict__ status) {
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (r >= N) return;
+  int32_t x[kMaxD];
+  bool ok = true;
+  for (int j = 0; j < c.D; ++j) {
+    x[j] = coords[r * c.D + j];
+    ok = ok && x[j] >= 0 && x[j] < c.size[j];
+    if (copy_out) copy_out[r * c.D + j] = x[j];
+  }
+  keys[r] = ok ? pack_site(c, x) : kEmpty;
+  if (!ok) atomicOr(status, kStRange);
+}
+
+// Bits of v at the set positions of m, packed from the lowest.
+__device__ __forceinline__ uint32_t extract_bits(uint32_t v, uint32_t m) {
+  uint32_t r = 0;
+  for (uint32_t bb = 1; m; bb <<= 1) {
+    const uint32_t low = m & (0u - m);
+    if (v & low) r |= bb;
+    m &= m - 1;
+  }
+  return r;
+}
+
+// Entry e = l * K + i of the bricks' neighbourhood table: for a site at
+// local cell l (the lowest lb bits of its cell) and offset i, the
+// neighbour's local cell | (the faces it crossed, bit j-1 for coordinate j)
+// << 6.  The same for every brick, so one small table serves the probe.
+__device__ uint16_t brick_table_entry(const OffsetTable& ot, const BrickMap& m, int e) {
+  const uint32_t lowmask = (1u << m.lb) - 1u;
+  const int l = e / ot.K, i = e % ot.K;
+  int rem = i;
+  int o[kMaxD] = {0, 0, 0, 0};
+  for (int j = m.D - 1; j >= 0; --j) {
+    o[j] = rem % ot.f[j] - ot.r[j];
+    rem /= ot.f[j];
+  }
+  uint32_t loc = 0, S = 0;
+  for (int j = 1; j < m.D; ++j) {
+    const uint32_t lm = static_cast<uint32_t>(m.M[j]) & lowmask;
+    int v = static_cast<int>(extract_bits(static_cast<uint32_t>(l), lm)) + o[j];
+    if (v < 0 || v >= m.side[j]) {
+      S |= 1u << (j - 1);
+      v = v < 0 ? v + m.side[j] : v - m.side[j];
+    }
+    loc |= static_cast<uint32_t>(deposit64(static_cast<uint64_t>(v), lm));
+  }
+  return static_cast<uint16_t>(loc | (S << 6));
+}
+
+// Per sorted position: first of its brick?  The block's flags as four 64-bit
+// wave masks and their count; equal cells next to each other are duplicate
+// sites; a second mask marks the positions whose rows are in range.  Rows
+// out of range (key kEmpty) take part in nothing.  The first
+// 2^lb K threads also write the neighbourhood table (the grid has at least
+// that many; blocks past the nblk of positions do only that).
+__global__ __launch_bounds__(kBlock) void k_brick_flags(
+    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    const uint64_t* __restrict__ rowkeys, int64_t n, int64_t nblk, int lb,
+    uint64_t* __restrict__ flagbits, uint64_t* __restrict__ validbits, uint32_t* __restrict__ bsum,
+    uint32_t* __restrict__ status, OffsetTable ot, BrickMap bm, uint16_t* __restrict__ tab) {
+  __shared__ uint32_t s_c[kBlock / kWave];
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (p < (int64_t{1} << bm.lb) * ot.K) tab[p] = brick_table_entry(ot, bm, static_cast<int>(p));
+  if (blockIdx.x >= nblk) return;
+  const int wave = threadIdx.x / kWave;
+  bool flag = false;
+  const bool valid = p < n && rowkeys[perm[p]] != kEmpty;
+  if (valid) {
+    const uint64_t key = mk[p];
+    flag = true;
+    if (p > 0 && rowkeys[perm[p - 1]] != kEmpty) {
+      const uint64_t pk = mk[p - 1];
+      flag = (pk >> lb) != (key >> lb);
+      if (pk == key) atomicOr(status, kStDup);
+    }
+  }
+  const uint64_t m = __ballot(flag);
+  const uint64_t mv = __ballot(valid);
+  if (lane_id() == 0) {
+    flagbits[p >> 6] = m;
+    validbits[p >> 6] = mv;
+    s_c[wave] = static_cast<uint32_t>(__popcll(m));
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < kBlock / kWave; ++w) t += s_c[w];
+    bsum[blockIdx.x] = t;
+  }
+}
+
+// Brick number of every sorted position (its brick's rank among the flags);
+// the first position of a brick inserts it into the directory and records
+// where its run starts.
+__global__ __launch_bounds__(kBlock) void k_bricks(
+    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    int64_t n, const uint64_t* __restrict__ flagbits, const uint64_t* __restrict__ validbits,
+    const uint32_t* __restrict__ bbase, BrickMap m, int32_t* __restrict__ brickidx,
+    int64_t* __restrict__ starts) {
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (p >= n) return;
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const uint64_t w64 = flagbits[p >> 6];
+  uint32_t before = bbase[blockIdx.x];
+  for (int w = 0; w < wave; ++w) before += __popcll(flagbits[(blockIdx.x * (kBlock / kWave)) + w]);
+  const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
+  const int64_t bi = static_cast<int64_t>(before) + __popcll(w64 & upto) - 1;
+  const bool valid = (validbits[p >> 6] >> lane) & 1ull;
+  brickidx[p] = valid ? static_cast<int32_t>(bi) : -1;
+  if (!((w64 >> lane) & 1ull)) return;
+  starts[bi] = p;
+  const uint64_t brick = mk[p] >> m.lb;
+  const uint64_t dmask = dir_mask(m);
+  uint64_t sl = mix64(brick) & dmask;
+  for (uint64_t t = 0; t <= dmask; ++t) {
+    const uint64_t old = atomicCAS(reinterpret_cast<unsigned long long*>(&m.dir[sl].x),
+                                   static_cast<unsigned long long>(kEmpty),
+                                   static_cast<unsigned long long>(brick));
+    if (old == kEmpty) {
+      m.dir[sl].y = static_cast<uint64_t>(bi);
+      break;
+    }
+    if (old == brick) break;          // (only after an out-of-range site split a run)
+    sl = (sl + 1) & dmask;
+  }
+}
+
+// Pool entries of every brick, one wave per brick (bricks dealt out in steps
+// of the grid's waves): the run's sites go into an LDS image of the brick,
+// which the wave then stores whole (zeros included) in one coalesced pass.
+constexpr int kPoolBlocks = 2048;
+__global__ __launch_bounds__(kBlock) void k_pool_fill(
+    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    const uint64_t* __restrict__ validbits, int64_t n, const int64_t* __restrict__ starts,
+    BrickMap m) {
+  __shared__ int32_t s_img[kBlock / kWave][kBrickCells];
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const int64_t nbr = m.nbricks->n_out;
+  const int cells = 1 << m.lb;
+  const uint64_t lowmask = static_cast<uint64_t>(cells - 1);
+  const int64_t nw = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  for (int64_t bi = blockIdx.x * static_cast<int64_t>(kBlock / kWave) + wave; bi < nbr; bi += nw) {
+    const int64_t first = starts[bi];
+    const int64_t last = bi + 1 < nbr ? starts[bi + 1] : n;
+    s_img[wave][lane] = 0;
+    for (int64_t q0 = first; q0 < last; q0 += kWave) {
+      const int64_t q = q0 + lane;
+      if (q < last && ((validbits[q >> 6] >> (q & 63)) & 1ull))
+        s_img[wave][mk[q] & lowmask] = perm[q] + 1;
+    }
+    if (lane < cells) m.pool[(bi << m.lb) + lane] = s_img[wave][lane];
+  }
+}
+
+// Neighbour bricks of every brick: entry [bi][t] = the number of the brick
+// at brick offset t (digit j-1 of t in base 3 = the step along coordinate j
+// plus one), -1 if absent or off the grid, so the probe, whose sites read
+// their brick's row, hashes nothing.  One thread per (brick, offset in the
+// upper half t >= NB/2): brick B at offset t of brick A has A at offset
+// NB-1-t, so each lookup fills both entries (the lower halves start at -1,
+// cleared with the directory).  Pairs are dealt out in steps of the grid.
+__global__ __launch_bounds__(kBlock) void k_brick_nbrs(
+    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    const uint64_t* __restrict__ rowkeys, const int64_t* __restrict__ starts, Codec crow,
+    BrickMap m, int nb3, int32_t* __restrict__ nbr) {
+  const int half = nb3 / 2;
+  const int per = nb3 - half;                 // offsets half .. nb3-1
+  const int64_t total = m.nbricks->n_out * per;
+  const uint64_t dmask = dir_mask(m);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; e < total;
+       e += stride) {
+    const int64_t bi = e / per;
+    const int t0 = half + static_cast<int>(e - bi * per);
+    if (t0 == half) {                         // the brick itself
+      nbr[bi * nb3 + half] = static_cast<int32_t>(bi);
+      continue;
+    }
+    const int64_t p = starts[bi];
+    const uint64_t rk = rowkeys[perm[p]];
+    uint64_t k = mk[p] >> m.lb;
+    bool ok = true;
+    int t = t0;
+    for (int j = 1; j < m.D; ++j) {
+      const int dj = t % 3 - 1;
+      t /= 3;
+      if (dj == 0) continue;
+      const int32_t c = static_cast<int32_t>((rk >> crow.shift[j]) & crow.fmask[j]);
+      const int32_t bc = c / m.side[j] + dj, bmax = (crow.size[j] - 1) / m.side[j];
+      ok = ok && m.BM[j] != 0 && bc >= 0 && bc <= bmax;
+      k = zmove64(k, m.BM[j], m.BM[j] & (0ull - m.BM[j]), dj < 0);
+    }
+    int32_t r = -1;
+    if (ok) {
+      const uint64_t sl = mix64(k) & dmask;
+      const ulonglong2 v = m.dir[sl];
+      if (v.x == k) r = static_cast<int32_t>(v.y);
+      else if (v.x != kEmpty) r = dir_find_after(m, dmask, sl, k);
+    }
+    nbr[bi * nb3 + t0] = r;
+    if (r >= 0) nbr[static_cast<int64_t>(r) * nb3 + (nb3 - 1 - t0)] = static_cast<int32_t>(bi);
+  }
+}
+
+// Clears the directory slots in use (dir_mask), kEmpty in both halves, and
+// sets the bricks' neighbour rows to -1.
+__global__ __launch_bounds__(kBlock) void k_dir_clear(BrickMap m, int32_t* __restrict__ nbr,
+                                                      int nb3) {
+  const uint64_t n = dir_mask(m) + 1;
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
+  for (uint64_t i = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x; i < n; i += stride)
+    m.dir[i] = make_ulonglong2(kEmpty, kEmpty);
+  const uint64_t nn = static_cast<uint64_t>(m.nbricks->n_out) * nb3;
+  for (uint64_t i = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x; i < nn; i += stride)
+    nbr[i] = -1;
+}
+
+// Neighbour probe on the brick map (VSC).  Thread = sorted position p, which
+// is the schedule position; its cell is mk[p].  The bricks the neighbours can
+// fall in are the site's own and, per coordinate where the site lies within
+// (f-1)/2 of its brick's face, the brick across that face (none where that
+// face is the grid's): at most 2^(D-1) combinations, whose directory slots
+// are loaded together before any pool load.  The neighbourhood table gives
+// each offset's local cell and combination, so a lookup is one LDS read, a
+// select and one pool load; a neighbour past an extent lands on a cell no
+// site occupies.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_probe_brick(
+    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ brickidx, const uint64_t* __restrict__ rowkeys,
+    const DeviceHeader* __restrict__ hdr, int64_t gstride, Codec crow, OffsetTable ot,
+    BrickMap m, const uint16_t* __restrict__ tab, const int32_t* __restrict__ nbr, int nb3,
+    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre,
+    int64_t nblk) {
+  const int64_t blk = probe_block(hdr->n_out, nblk);
+  if (blk < 0) return;
+  constexpr int NS = 1 << (D - 1);    // brick combinations
+  __shared__ uint16_t s_tab[kBrickCells * kBrickK];
+  __shared__ uint8_t s_cnt[kBrickK][kBlock / kWave];
+  const int ntab = (1 << m.lb) * ot.K;
+  for (int e = threadIdx.x; e < ntab; e += kBlock) s_tab[e] = tab[e];
+  __syncthreads();
+
+  const int64_t n_rows = hdr->n_out;
+  const int64_t p = blk * kBlock + threadIdx.x;
+  const bool valid = p < n_rows && brickidx[p] >= 0;
+  const int wave = threadIdx.x / kWave;
+  const int32_t y = p < n_rows ? perm[p] : 0;
+  const uint64_t cell0 = p < n_rows ? mk[p] : 0;
+  const uint64_t rk = rowkeys[y];
+  const uint64_t lowmask = (1ull << m.lb) - 1;
+  // per coordinate: the face the neighbours can cross (e = -1 / +1, 0 none),
+  // 0 as well where the brick across it would be off the grid
+  int e[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    e[j] = 0;
+    if (j > 0 && m.BM[j] != 0) {
+      const int32_t c = static_cast<int32_t>((rk >> crow.shift[j]) & crow.fmask[j]);
+      const int low = c & (m.side[j] - 1);
+      const int32_t bc = c / m.side[j], bmax = (crow.size[j] - 1) / m.side[j];
+      if (low < ot.r[j] && bc > 0) e[j] = -1;
+      else if (low >= m.side[j] - ot.r[j] && bc < bmax) e[j] = 1;
+    }
+  }
+  // the site's brick row of the neighbour table: combination S of the faces
+  // the site can cross is brick offset sum_j (S_j ? e_j + 1 : 1) 3^(j-1)
+  const int64_t brow = static_cast<int64_t>(valid ? brickidx[p] : 0) * nb3;
+  int32_t idx[NS];
+  idx[0] = valid ? brickidx[p] : -1;
+#pragma unroll
+  for (int S = 1; S < NS; ++S) {
+    bool need = valid;
+    int t = 0, w = 1;
+#pragma unroll
+    for (int j = 1; j < D; ++j) {
+      const bool in = (S >> (j - 1)) & 1;
+      need = need && (!in || e[j] != 0);
+      t += (in ? e[j] + 1 : 1) * w;
+      w *= 3;
+    }
+    const int32_t r = nbr[brow + (need ? t : 0)];    // every load in flight at once
+    idx[S] = need ? r : -1;
+  }
+  const int lrow = static_cast<int>(cell0 & lowmask) * ot.K;
+
+  constexpr int B = 8;
+  for (int i0 = 0; i0 < ot.K; i0 += B) {
+    int32_t v[B];
+    bool ok[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int i = i0 + u;
+      const uint32_t t = s_tab[lrow + (i < ot.K ? i : 0)];
+      const uint32_t S = t >> 6;
+      int32_t b = idx[0];
+#pragma unroll
+      for (int q = 1; q < NS; ++q) b = S == static_cast<uint32_t>(q) ? idx[q] : b;
+      ok[u] = valid && i < ot.K && b >= 0;
+      const int64_t a = ok[u] ? (static_cast<int64_t>(b) << m.lb) + (t & 63u) : 0;
+      v[u] = m.pool[a];                   // unconditional: entry 0 exists
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int i = i0 + u;
+      if (i >= ot.K) break;
+      const int32_t row = ok[u] ? v[u] - 1 : -1;
+      if (p < gstride) gmap[i * gstride + p] = row + 1;   // 0 = no input
+      const uint64_t mm = __ballot(row >= 0);
+      if (lane_id() == 0) s_cnt[i][wave] = static_cast<uint8_t>(__popcll(mm));
+    }
+  }
+  publish_counts(s_cnt, ot.K, blk_cnt, wpre, nblk, blk);
+}
+
 // One block per offset: exclusive scan of its per-block counts, in place;
 // total into totals[i].
 __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, int64_t nblk,
@@ -1445,14 +1832,10 @@ size_t schedule_bytes(int64_t n_cap) {
 }
 
 // Output rows in Morton order -> rb->perm (scratch carved from the transient
-// allocation by `cv`).
-void launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow, Carver* cv) {
+// allocation by `cv`); returns the sorted Morton codes.
+const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
+                                Carver* cv) {
   const int64_t n = rb->n_cap;
-  uint64_t* mk = cv->take<uint64_t>(n);
-  uint64_t* mk2 = cv->take<uint64_t>(n);
-  int32_t* mv = cv->take<int32_t>(n);
-  int32_t* mv2 = cv->take<int32_t>(n);
-  void* scratch = cv->take<unsigned char>(radix_sort_scratch_bytes(n));
   int maxb = 0, sbits = 0;
   for (int j = 1; j < crow.D; ++j) {
     const int b = bitlen(crow.fmask[j]);
@@ -1460,6 +1843,14 @@ void launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& c
     sbits += b;
   }
   const int total = sbits + bitlen(crow.fmask[0]);
+  // the values ping-pong between two arrays, one of them the schedule itself,
+  // chosen so that the last pass lands in it
+  const bool odd = ((total + 7) / 8) % 2 == 1;
+  uint64_t* mk = cv->take<uint64_t>(n);
+  uint64_t* mk2 = cv->take<uint64_t>(n);
+  int32_t* mv = odd ? cv->take<int32_t>(n) : rb->perm;
+  int32_t* mv2 = odd ? rb->perm : cv->take<int32_t>(n);
+  void* scratch = cv->take<unsigned char>(radix_sort_scratch_bytes(n));
   const unsigned g = grid_for(n);
   switch (crow.D) {
     case 2: k_morton<2><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
@@ -1467,8 +1858,7 @@ void launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& c
     default: k_morton<4><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
   }
   const bool in_tmp = radix_sort_pairs(mk, mv, mk2, mv2, rb->hdr, n, total, scratch, rb->stream);
-  (void)hipMemcpyAsync(rb->perm, in_tmp ? mv2 : mv, static_cast<size_t>(n) * 4,
-                       hipMemcpyDeviceToDevice, rb->stream);
+  return in_tmp ? mk2 : mk;
 }
 
 int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Codec& cin,
@@ -1519,6 +1909,115 @@ void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, cons
   launch_scan_compact(rb);
 }
 
+// Geometry of the brick map for a VSC book, or false where it does not apply:
+// bricks of up to 64 cells (b = 6 / d bits per coordinate, fewer where a
+// coordinate has fewer), every coordinate's brick side at least f_j - 1 (so
+// a neighbour crosses at most one face per coordinate), at most kBrickK
+// offsets.  SPCONV_RULEBOOK=table, SPCONV_HASH_LAYOUT and
+// SPCONV_TEST_HASH_SLOTS keep the open-addressing table of sites instead.
+bool brick_geom(spconv_rulebook rb, BrickMap* m) {
+  if (rb->kind != SPCONV_VSC || rb->K > kBrickK || rb->in_count) return false;
+  if (std::getenv("SPCONV_HASH_LAYOUT") || std::getenv("SPCONV_TEST_HASH_SLOTS")) return false;
+  if (const char* e = std::getenv("SPCONV_RULEBOOK"))
+    if (std::strcmp(e, "table") == 0) return false;
+  *m = BrickMap{};
+  m->D = rb->D;
+  const int d = rb->D - 1;
+  const int b = 6 / d;
+  int bits[kMaxD] = {0, 0, 0, 0}, maxb = 0, B = 0;
+  for (int j = 1; j < rb->D; ++j) {
+    bits[j] = bitlen(static_cast<uint64_t>(rb->size[j] - 1));
+    maxb = bits[j] > maxb ? bits[j] : maxb;
+    B += bits[j];
+  }
+  if (B + bitlen(static_cast<uint64_t>(rb->size[0] - 1)) > 63) return false;
+  // cell bits: lowest = level 0 of the last coordinate, coordinate 1 on top
+  // inside a level (the order of the schedule's Morton codes)
+  int pos = 0;
+  for (int L = 0; L < maxb; ++L)
+    for (int j = rb->D - 1; j >= 1; --j)
+      if (bits[j] > L) m->M[j] |= 1ull << pos++;
+  m->lb = 0;
+  for (int j = 1; j < rb->D; ++j) {
+    const int bj = bits[j] < b ? bits[j] : b;
+    m->side[j] = 1 << bj;
+    m->lb += bj;
+    if (m->side[j] < rb->f[j] - 1) return false;
+  }
+  if (m->lb < 2) return false;     // a brick is written in 16-byte pieces
+  const uint64_t lowmask = (1ull << m->lb) - 1;
+  for (int j = 1; j < rb->D; ++j) m->BM[j] = (m->M[j] & ~lowmask) >> m->lb;
+  return true;
+}
+
+// VSC book on the brick map: keys, the Morton schedule (sorted), brick runs,
+// directory and pool, then the probe, scan and compaction.
+int build_vsc_bricks(spconv_rulebook rb, const int32_t* coords, BrickMap m) {
+  const int64_t N = rb->n_in;
+  const Codec cin = make_codec(rb->D, rb->size);
+  k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
+  uint64_t dslots = 64;
+  while (dslots < 2 * static_cast<uint64_t>(N)) dslots <<= 1;
+  const int64_t nb = rb->nblk;
+  const size_t bytes = align_up(N * 8, 256) + schedule_bytes(rb->n_cap) +
+                       2 * align_up(static_cast<size_t>(nb) * kBlock / 8, 256) +
+                       align_up(static_cast<size_t>(nb) * 4, 256) + 256 +
+                       align_up(dslots * 16, 256) +
+                       align_up((static_cast<size_t>(N) << m.lb) * 4, 256) +
+                       align_up(static_cast<size_t>(N) * 4, 256) +
+                       align_up(static_cast<size_t>(N) * 8, 256) +
+                       align_up(static_cast<size_t>(N) * 27 * 4, 256) +
+                       align_up(static_cast<size_t>(kBrickCells) * kBrickK * 2, 256) + 256;
+  void* mem = nullptr;
+  if (dev_alloc(rb, bytes, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
+  Carver cv{static_cast<char*>(mem)};
+  uint64_t* keys = cv.take<uint64_t>(N);
+  uint64_t* flagbits = cv.take<uint64_t>(static_cast<size_t>(nb) * (kBlock / kWave));
+  uint64_t* validbits = cv.take<uint64_t>(static_cast<size_t>(nb) * (kBlock / kWave));
+  uint32_t* bsum = cv.take<uint32_t>(static_cast<size_t>(nb));
+  DeviceHeader* bh = cv.take<DeviceHeader>(1);
+  m.dir = cv.take<ulonglong2>(dslots);
+  m.dslots = dslots;
+  m.pool = cv.take<int32_t>(static_cast<size_t>(N) << m.lb);
+  m.nbricks = bh;
+  int32_t* brickidx = cv.take<int32_t>(N);
+  int64_t* starts = cv.take<int64_t>(N);
+  int nb3 = 1;
+  for (int j = 1; j < rb->D; ++j) nb3 *= 3;
+  int32_t* nbr = cv.take<int32_t>(static_cast<size_t>(N) * nb3);
+  uint16_t* tab = cv.take<uint16_t>(static_cast<size_t>(kBrickCells) * kBrickK);
+  k_site_keys<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, cin, keys, rb->out_coords,
+                                                      &rb->hdr->status);
+  const uint64_t* mk = launch_schedule(rb, keys, cin, &cv);
+  const OffsetTable ot = make_offsets(rb);
+  const int64_t ntab = (int64_t{1} << m.lb) * ot.K;
+  const int64_t fb = nb > (ntab + kBlock - 1) / kBlock ? nb : (ntab + kBlock - 1) / kBlock;
+  k_brick_flags<<<static_cast<unsigned>(fb), kBlock, 0, rb->stream>>>(
+      mk, rb->perm, keys, N, nb, m.lb, flagbits, validbits, bsum, &rb->hdr->status, ot, m, tab);
+  k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nb, bh, -1, nullptr);
+  const unsigned gb = static_cast<unsigned>(nb < kPoolBlocks ? nb : kPoolBlocks);
+  k_dir_clear<<<gb, kBlock, 0, rb->stream>>>(m, nbr, nb3);
+  k_bricks<<<static_cast<unsigned>(nb), kBlock, 0, rb->stream>>>(mk, rb->perm, N, flagbits,
+                                                                 validbits, bsum, m, brickidx,
+                                                                 starts);
+  k_pool_fill<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, validbits, N, starts, m);
+  k_brick_nbrs<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, keys, starts, cin, m, nb3, nbr);
+  const unsigned g = probe_grid_size(rb->nblk);
+  auto launch = [&](auto kern) {
+    kern<<<g, kBlock, 0, rb->stream>>>(mk, rb->perm, brickidx, keys, rb->hdr, rb->gstride, cin,
+                                       ot, m, tab, nbr, nb3, rb->gmap, rb->blk_cnt, rb->wpre,
+                                       rb->nblk);
+  };
+  switch (rb->D) {
+    case 2: launch(k_probe_brick<2>); break;
+    case 3: launch(k_probe_brick<3>); break;
+    default: launch(k_probe_brick<4>); break;
+  }
+  launch_scan_compact(rb);
+  if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
+  return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
 int finish(spconv_rulebook rb, Transient& tr) {
   if (dev_free(rb, tr.mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -1561,7 +2060,7 @@ bool make_grid_geom(int D, const int32_t* size, GridGeom* g, uint64_t* cells) {
 // for small inputs).  SPCONV_RULEBOOK=hash / =grid forces a choice.
 bool use_grid(uint64_t cells, int64_t N) {
   if (const char* e = std::getenv("SPCONV_RULEBOOK")) {
-    if (std::strcmp(e, "hash") == 0) return false;
+    if (std::strcmp(e, "hash") == 0 || std::strcmp(e, "table") == 0) return false;
     if (std::strcmp(e, "grid") == 0) return true;
   }
   return cells <= 400ull * static_cast<uint64_t>(N) + (1ull << 22);
@@ -1811,6 +2310,8 @@ int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   uint64_t cells = 0;
   if (N > 0 && make_grid_geom(rb->D, rb->size, &g, &cells) && use_grid(cells, N))
     return build_vsc_grid(rb, coords, g, cells);
+  BrickMap bm;
+  if (N > 0 && brick_geom(rb, &bm)) return build_vsc_bricks(rb, coords, bm);
   const Codec cin = make_codec(rb->D, rb->size);
   k_init_header<<<1, 64, 0, rb->stream>>>(rb->hdr, N);
   Transient tr;

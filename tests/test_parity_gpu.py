@@ -298,12 +298,13 @@ def _rulebook_case_sites(name):
     return dense_ref.random_sites(rng, size, 0.3), size
 
 
-@pytest.mark.parametrize("path", ["hash", "grid", "grid3"])
+@pytest.mark.parametrize("path", ["hash", "table", "grid", "grid3"])
 @pytest.mark.parametrize("case", range(len(RULEBOOK_CASES)))
 def test_rulebook_paths(monkeypatch, path, case):
-    """Hash-table and dense-grid rule books give the same (oracle) result;
-    grid3 ranks a small grid's cells with the three-launch multi-block path
-    instead of one workgroup."""
+    """Hashed and dense-grid rule books give the same (oracle) result: hash
+    = the sorted-brick map for VSC (the site table for SC), table = the
+    open-addressing table of sites for both; grid3 ranks a small grid's cells
+    with the three-launch multi-block path instead of one workgroup."""
     monkeypatch.setenv("SPCONV_RULEBOOK", path)
     kind, name, f, s, ci, co, dt = RULEBOOK_CASES[case]
     coords, size = _rulebook_case_sites(name)
@@ -385,7 +386,7 @@ def _status(kind, coords, size, f, s):
         return e.status
 
 
-@pytest.mark.parametrize("path", ["hash", "grid"])
+@pytest.mark.parametrize("path", ["hash", "table", "grid"])
 @pytest.mark.parametrize("kind", [0, 1])
 def test_errors_match_oracle(monkeypatch, kind, path):
     monkeypatch.setenv("SPCONV_RULEBOOK", path)

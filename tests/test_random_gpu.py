@@ -35,7 +35,7 @@ def _case(seed):
     ci, co = CHANNELS[int(rng.integers(0, len(CHANNELS)))]
     dtype = "bf16" if (ci % 32 == 0 and rng.random() < 0.5) else "f32"
     out_dtype = dtype if rng.random() < 0.7 else ("f32" if dtype == "bf16" else "bf16")
-    path = str(rng.choice(["grid", "hash", "grid3"]))
+    path = str(rng.choice(["grid", "hash", "grid3", "table"]))
     c = dense_ref.random_sites(rng, size, density)
     if len(c) == 0:          # (empty inputs have their own test)
         c = np.array([[int(rng.integers(0, e)) for e in size]], np.int32)
