@@ -1,7 +1,11 @@
 // Rule-book construction on gfx950 (Section 4 of the paper: map the active
 // sites to rows, then list the (input row, output row) pairs of every filter
-// offset).  Two interchangeable site maps, chosen per build:
+// offset).  Site maps, chosen per build:
 //
+// One workgroup (VSC layers of at most 2048 sites on at most 2^18 cells):
+//   k_build_small   an LDS occupancy bitmap over Z-ordered cells, ranked by a
+//                   popcount prefix (the schedule), neighbours by dilated
+//                   arithmetic, G and R_i written directly: one launch.
 // Dense grid (grids of up to 2^29 cells and at most ~400 cells per site):
 //   every cell of the grid holds 1 + row (0 = empty), cells laid out along
 //   the Z-order curve of the sites.
@@ -12,16 +16,24 @@
 //                                 occupancy bitmap, its prefix counts, and
 //                                 the rows in cell order = the Z-order
 //                                 schedule the probe, the compaction and the
-//                                 forward walk
+//                                 forward walk (grids of at most 2^18 cells:
+//                                 one workgroup, k_grid_rank, the bitmap set
+//                                 by the scatter)
 //   k_probe_grid                  per schedule position and offset, one load
 //                                 of the neighbour's cell -> gather map
 //                                 G[i][p] (1 + input row, 0 if none)
-// Hash table (any grid up to 65535 per side):
-//   k_insert     pack every site into an order-preserving key; CAS-insert it
-//                into the open-addressing table (range errors, duplicates)
-//   k_morton + radix sort    the Z-order schedule
-//   k_probe      hash lookups -> G[i][p]
-// Both then run
+// Hashed (any grid up to 65535 per side):
+//   VSC: sorted bricks.  k_site_keys + k_morton + radix sort order the sites
+//   along the Z-order curve (the schedule); runs of one brick (2^b cells per
+//   coordinate) are numbered (k_brick_flags / k_bitscan / k_bricks), each
+//   brick inserted once into a hash directory; k_pool_fill writes the bricks'
+//   cells into a Z-ordered pool, k_brick_nbrs the neighbour bricks of every
+//   brick, and k_probe_brick looks up every neighbour with one pool load.
+//   SC (and SPCONV_RULEBOOK=table): an open-addressing table of sites,
+//   k_insert (pack every site into an order-preserving key; CAS-insert it,
+//   range errors, duplicates), k_morton + radix sort for the schedule, and
+//   k_probe (hash lookups -> G[i][p]).
+// Then
 //   k_scan       per offset, exclusive scan of the per-wave pair counts
 //   k_compact    per-offset stream compaction of G into R_i, in schedule
 //                order (wave ballot + mbcnt, per-wave prefix)
