@@ -323,6 +323,25 @@ def test_grid_forced_on_sparse_wide_grid(monkeypatch):
                   what="grid sparse SC")
 
 
+@pytest.mark.parametrize("f", [3, 5])
+def test_brick_map_on_grids_too_large_for_the_dense_grid(f):
+    """Grids of 2^31 cells (no dense grid): VSC takes the sorted-brick map by
+    default; surfaces cut from a huge volume, sparse scattered sites and
+    sites on the grid's faces and corners (bricks whose neighbours fall off
+    the grid), against the oracle."""
+    rng = np.random.default_rng(35 + f)
+    size = [2, 4096, 2048, 128]
+    shell = inputs.surfaces(2, 64, 6.0, 28.0, seed=40 + f, target=4000)
+    shell = shell + np.array([0, 4000, 100, 60], np.int32)          # near a far face
+    scattered = np.unique(rng.integers(0, size, size=(3000, 4)), axis=0)
+    corners = np.array([[b, x, y, z] for b in (0, 1) for x in (0, 1, 4094, 4095)
+                        for y in (0, 2047) for z in (0, 1, 126, 127)], np.int64)
+    c = np.unique(np.concatenate([shell, scattered, corners]), axis=0)
+    c = c[np.all((c >= 0) & (c < size), axis=1)].astype(np.int32)
+    _say(f"[brick map] f={f} N={len(c)}")
+    compare_layer(spc.VSC, c, size, [1, f, f, f], [1, 1, 1, 1], 16, 16, what=f"brick map f{f}")
+
+
 def test_permuted_rows():
     """VSC output permutes with its input; SC output does not move."""
     coords = inputs.pen_strokes(4, 32, seed=17, target=150)
