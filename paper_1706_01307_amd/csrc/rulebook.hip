@@ -17,8 +17,9 @@
 //                                 the rows in cell order = the Z-order
 //                                 schedule the probe, the compaction and the
 //                                 forward walk (grids of at most 2^18 cells:
-//                                 one workgroup, k_grid_rank, the bitmap set
-//                                 by the scatter)
+//                                 k_grid_emit_self alone, the bitmap set by
+//                                 the scatter, every block counting the
+//                                 words before its own)
 //   k_probe_grid                  per schedule position and offset, one load
 //                                 of the neighbour's cell -> gather map
 //                                 G[i][p] (1 + input row, 0 if none)
@@ -36,17 +37,21 @@
 // Then
 //   k_scan       per offset, exclusive scan of the per-wave pair counts
 //   k_compact    per-offset stream compaction of G into R_i, in schedule
-//                order (wave ballot + mbcnt, per-wave prefix)
+//                order (wave ballot + mbcnt, per-wave prefix); on small
+//                books every block sums the counts itself (no k_scan)
 // except the grouped VSC 3x3x3 grid probe, which counts in a first pass and
 // writes G and R_i together in a second (k_probe_grid_g4<false / true>).
 // SC (output set = sites with an active input in their receptive field):
 //   the input sites go into the grid or table as above, then
 //   k_sc_mark    every input marks the output sites it feeds in a bitmap
-//                over the output grid (lexicographic linear index)
+//                over the output grid (lexicographic linear index); on the
+//                grid path fused with the scatter (k_sc_scatter_mark)
 //   k_bitsum / k_bitscan / k_sc_emit
 //                rank the marked sites by a popcount prefix sum, which
-//                numbers the output rows in lexicographic order
-//   then the schedule of the output sites (an output grid, or Morton codes
+//                numbers the output rows in lexicographic order (small
+//                bitmaps: k_sc_emit alone); on the grid path the emission
+//                also fills the output grid
+//   then the schedule of the output sites (the output grid, or Morton codes
 //   and the sort), and probe / scan / compact on input site s*y + o.
 #include <cstdlib>
 #include <cstring>
@@ -125,7 +130,8 @@ __device__ void fill_offsets(const OffsetTable& ot, int16_t (*s_off)[kMaxD]) {
 // Per-block pair counts.  During a probe every wave leaves its count for
 // offset i in s_cnt[i][wave]; at the end the block writes, per offset, its
 // total (scanned later into the block's base) and the exclusive prefixes of
-// waves 1..3 packed in bytes 0..2 (each at most 192).
+// waves 1..3 packed in bytes 0..2 (each at most 192), wave 3's own count in
+// byte 3 (so bytes 2 + 3 give the total as well).
 __device__ void publish_counts(const uint8_t (*s_cnt)[kBlock / kWave], int K,
                                int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre,
                                int64_t nblk, int64_t blk) {
@@ -133,7 +139,7 @@ __device__ void publish_counts(const uint8_t (*s_cnt)[kBlock / kWave], int K,
   for (int i = threadIdx.x; i < K; i += kBlock) {
     const uint32_t c0 = s_cnt[i][0], c1 = s_cnt[i][1], c2 = s_cnt[i][2], c3 = s_cnt[i][3];
     blk_cnt[i * nblk + blk] = static_cast<int32_t>(c0 + c1 + c2 + c3);
-    wpre[i * nblk + blk] = c0 | ((c0 + c1) << 8) | ((c0 + c1 + c2) << 16);
+    wpre[i * nblk + blk] = c0 | ((c0 + c1) << 8) | ((c0 + c1 + c2) << 16) | (c3 << 24);
   }
 }
 
@@ -1024,22 +1030,57 @@ __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, 
 // writes its pairs of offset i at pair_off[i] + (pairs of the blocks before
 // it) + (pairs of the waves before it in its block) + (set lanes before it in
 // its ballot), so R_i comes out in schedule (Z-order) order without any
-// further sorting.
+// further sorting.  SELF: no k_scan ran; every block sums the probe's counts
+// (from the packed wave prefixes) of all blocks itself, for k_i and for its
+// own base, which it stores in blk_base (small books: K nblk^2 words read).
+template <bool SELF>
 __global__ __launch_bounds__(kBlock) void k_compact(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ blk_base, const uint32_t* __restrict__ wpre,
-    const int64_t* __restrict__ totals, int K, int64_t gstride,
+    int32_t* __restrict__ blk_base, const uint32_t* __restrict__ wpre,
+    int64_t* __restrict__ totals, int K, int64_t gstride, int64_t n_cap,
     const DeviceHeader* __restrict__ hdr, int64_t nblk, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ int64_t s_off[kMaxK + 1];
   __shared__ uint32_t s_wp[kMaxK];
+  __shared__ int64_t s_tot[SELF ? kMaxK : 1];
+  __shared__ int32_t s_base[SELF ? kMaxK : 1];
+  // the gather-map entries of the first kCompactPre offsets and the output
+  // row, requested before anything else so that their latency passes during
+  // the block's prefix work (p < gstride: in bounds; positions past the
+  // output rows are dropped below)
+  constexpr int kCompactPre = 16;
+  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  int32_t pre[kCompactPre];
+#pragma unroll
+  for (int u = 0; u < kCompactPre; ++u)
+    pre[u] = gmap[(u < K ? u : K - 1) * gstride + p] - 1;
+  const int32_t y0 = perm[p < n_cap ? p : 0];
+  if constexpr (SELF) {
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    for (int k = wave; k < K; k += kBlock / kWave) {
+      int64_t tot = 0, base = 0;
+      for (int64_t b = lane; b < nblk; b += kWave) {
+        const uint32_t w = wpre[k * nblk + b];
+        const int64_t c = ((w >> 16) & 0xffu) + (w >> 24);
+        tot += c;
+        base += b < static_cast<int64_t>(blockIdx.x) ? c : 0;
+      }
+      tot = __shfl(wave_incl_scan(tot), kWave - 1, kWave);
+      base = __shfl(wave_incl_scan(base), kWave - 1, kWave);
+      if (lane == 0) {
+        s_tot[k] = tot;
+        s_base[k] = static_cast<int32_t>(base);
+      }
+    }
+    __syncthreads();
+  }
   // pair_off = exclusive prefix of totals (K <= 1024, 4 per thread).
   {
     int64_t v[4], sum = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int k = 4 * threadIdx.x + u;
-      v[u] = k < K ? totals[k] : 0;
+      v[u] = k < K ? (SELF ? s_tot[k] : totals[k]) : 0;
       sum += v[u];
     }
     int64_t tot;
@@ -1054,22 +1095,38 @@ __global__ __launch_bounds__(kBlock) void k_compact(
   }
   __syncthreads();
   if (blockIdx.x == 0)
-    for (int k = threadIdx.x; k <= K; k += kBlock) pair_off[k] = s_off[k];
+    for (int k = threadIdx.x; k <= K; k += kBlock) {
+      pair_off[k] = s_off[k];
+      if (SELF && k < K) totals[k] = s_tot[k];
+    }
   __syncthreads();
   // this block's start inside every R_i, and its waves' packed prefixes
   for (int k = threadIdx.x; k < K; k += kBlock) {
     const int64_t q = static_cast<int64_t>(k) * nblk + blockIdx.x;
-    s_off[k] += blk_base[q];
+    if constexpr (SELF) {
+      s_off[k] += s_base[k];
+      blk_base[q] = s_base[k];
+    } else {
+      s_off[k] += blk_base[q];
+    }
     s_wp[k] = wpre[q];
   }
   __syncthreads();
   const int64_t n_rows = hdr->n_out;
-  const int64_t p = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   const bool valid = p < n_rows;
-  const int32_t y = valid ? perm[p] : 0;
+  const int32_t y = valid ? y0 : 0;
   const int wave = threadIdx.x / kWave;
+#pragma unroll
+  for (int i = 0; i < kCompactPre; ++i) {
+    const int32_t row = valid && i < K ? pre[i] : -1;
+    const uint64_t m = __ballot(row >= 0);
+    if (row >= 0) {
+      const int64_t pos = s_off[i] + wave_prefix(s_wp[i], wave) + prefix_popc(m);
+      pairs[pos] = make_int2(row, y);
+    }
+  }
   constexpr int U = 4;                  // gather-map loads in flight
-  for (int i0 = 0; i0 < K; i0 += U) {
+  for (int i0 = kCompactPre; i0 < K; i0 += U) {
     int32_t row[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -1085,6 +1142,44 @@ __global__ __launch_bounds__(kBlock) void k_compact(
     }
   }
 }
+
+// Cell of site (b, c_1..c_d) = b << B | Z(c), where Z interleaves the bits of
+// the spatial coordinates, most significant level first and coordinate 1
+// first inside a level, keeping only the bits a coordinate can have
+// (B = sum_j bits_j).  Walking cells in increasing order is the Z-order of
+// the sites.  M[j] marks the bits of Z that hold coordinate j.
+struct GridGeom {
+  int D;
+  int B;
+  uint32_t M[kMaxD];
+  int32_t size[kMaxD];
+};
+
+// Scatter bits of v into the set positions of m, lowest first.
+__host__ __device__ inline uint32_t deposit(uint32_t v, uint32_t m) {
+  uint32_t r = 0;
+  for (uint32_t bb = 1; m; bb <<= 1) {
+    const uint32_t low = m & (0u - m);
+    if (v & bb) r |= low;
+    m &= m - 1;
+  }
+  return r;
+}
+
+__device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* x) {
+  uint32_t cell = static_cast<uint32_t>(x[0]) << g.B;
+  for (int j = 1; j < g.D; ++j) cell |= deposit(static_cast<uint32_t>(x[j]), g.M[j]);
+  return cell;
+}
+
+// Output grid an SC emission fills as well (grid = NULL: none): grid[cell] =
+// 1 + row, and with bitmap set the cell's occupancy bit too (for the
+// one-launch schedule of small grids).
+struct OutGrid {
+  GridGeom g;
+  uint32_t* grid;
+  uint32_t* bitmap;
+};
 
 // SC: mark every output site some input feeds.  Output site y with
 // y_j = (x_j - o_j) / s_j when that is a non-negative integer inside the
@@ -1119,6 +1214,50 @@ __global__ __launch_bounds__(kBlock) void k_sc_mark(
       if (!(bitmap[L >> 5] & bit)) atomicOr(&bitmap[L >> 5], bit);
     }
   }
+}
+
+// SC on dense grids, first step in one pass over the input rows: row r is
+// placed at its cell of the input grid by compare-and-swap from 0 (a cell
+// found taken is a duplicate site), and the output sites it feeds are marked
+// as k_sc_mark does.  With `count` set only the first *count rows exist
+// (count_copy, when set, receives that count).
+__global__ __launch_bounds__(kBlock) void k_sc_scatter_mark(
+    const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
+    GridGeom g, uint32_t* __restrict__ grid, uint32_t* __restrict__ status,
+    int64_t* __restrict__ count_copy, OffsetTable ot, Extents E, uint32_t* __restrict__ bitmap) {
+  __shared__ int16_t s_off[kMaxK][kMaxD];
+  fill_offsets(ot, s_off);
+  __syncthreads();
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (count_copy && r == 0) *count_copy = *count;
+  if (r >= N || (count && r >= *count)) return;
+  int32_t x[kMaxD];
+  bool ok = true;
+  for (int j = 0; j < g.D; ++j) {
+    x[j] = coords[r * g.D + j];
+    ok = ok && x[j] >= 0 && x[j] < g.size[j];
+  }
+  if (!ok) {
+    atomicOr(status, kStRange);
+    return;
+  }
+  const uint32_t prev = atomicCAS(&grid[grid_cell(g, x)], 0u, static_cast<uint32_t>(r + 1));
+  // (the compare-and-swap's answer is awaited only after the marking)
+  for (int i = 0; i < ot.K; ++i) {
+    uint32_t L = 0;
+    bool in = true;
+    for (int j = 0; j < ot.D; ++j) {
+      const int32_t t = x[j] - s_off[i][j];
+      const int32_t q = t / ot.s[j];
+      in = in && t >= 0 && q * ot.s[j] == t && q < E.e[j];
+      L = L * static_cast<uint32_t>(E.e[j]) + static_cast<uint32_t>(q);
+    }
+    if (in) {
+      const uint32_t bit = 1u << (L & 31);
+      if (!(bitmap[L >> 5] & bit)) atomicOr(&bitmap[L >> 5], bit);
+    }
+  }
+  if (prev != 0u) atomicOr(status, kStDup);
 }
 
 // Popcount of 256 bitmap words per block (one word per thread).
@@ -1168,32 +1307,57 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
 // Block b works on bitmap block b / kEmitParts (256 words, whose rank base is
 // bbase[b / kEmitParts]) and, of it, the 32 words of part b % kEmitParts;
 // kEmitParts threads share a word, 32 / kEmitParts cells each, so a dense
-// word is not emitted by one thread in 32 serial steps.
+// word is not emitted by one thread in 32 serial steps.  bbase = NULL (at
+// most kSelfWords words): every block counts the words before its bitmap
+// block itself, and the last bitmap block sets n_out, in place of k_bitsum
+// and k_bitscan.
 constexpr int kEmitParts = 8;
 constexpr int kEmitBits = 32 / kEmitParts;
+constexpr int kSelfWords = 8192;   // most words of a bitmap ranked without a scan launch
 __global__ __launch_bounds__(kBlock) void k_sc_emit(
     const uint32_t* __restrict__ bitmap, uint64_t nwords, const uint32_t* __restrict__ bbase,
     Codec cout, Extents E, int32_t* __restrict__ out_coords,
-    uint64_t* __restrict__ out_keys) {
+    uint64_t* __restrict__ out_keys, OutGrid og, DeviceHeader* __restrict__ hdr) {
   __shared__ uint32_t s_pre[kBlock];
+  __shared__ uint32_t s_word[kBlock];
   const uint64_t bw = blockIdx.x / kEmitParts;
   const int part = blockIdx.x % kEmitParts;
+  uint32_t bbw = 0;                                // rank base of the bitmap block
+  if (!bbase) {
+    constexpr int PER = kSelfWords / kBlock;
+    const uint32_t w0 = static_cast<uint32_t>(bw) * kBlock;
+    uint32_t v[PER], before = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {                // every load in flight at once
+      const uint32_t idx = k * kBlock + threadIdx.x;
+      v[k] = bitmap[idx < w0 ? idx : 0u];
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) before += k * kBlock + threadIdx.x < w0 ? __popc(v[k]) : 0u;
+    block_excl_scan<uint32_t>(before, &bbw);
+  } else {
+    bbw = bbase[bw];
+  }
   {
     // exclusive popcount prefix over the 256 words of the bitmap block
     const uint64_t w = bw * kBlock + threadIdx.x;
+    const uint32_t tw = w < nwords ? bitmap[w] : 0u;
     uint32_t tot;
-    s_pre[threadIdx.x] = block_excl_scan<uint32_t>(w < nwords ? __popc(bitmap[w]) : 0u, &tot);
+    s_word[threadIdx.x] = tw;
+    s_pre[threadIdx.x] = block_excl_scan<uint32_t>(__popc(tw), &tot);
+    if (!bbase && blockIdx.x == gridDim.x - kEmitParts && threadIdx.x == 0)
+      hdr->n_out = static_cast<int64_t>(bbw) + tot;
   }
   __syncthreads();
   const int wi = part * (kBlock / kEmitParts) + threadIdx.x / kEmitParts;   // word in block
   const int sub = threadIdx.x % kEmitParts;
   const uint64_t w = bw * kBlock + wi;
   if (w >= nwords) return;
-  const uint32_t full = bitmap[w];
+  const uint32_t full = s_word[wi];
   const uint32_t below = (1u << (sub * kEmitBits)) - 1u;
   uint32_t word = (full >> (sub * kEmitBits)) & ((1u << kEmitBits) - 1u);
   if (!word) return;
-  uint32_t rank = bbase[bw] + s_pre[wi] + __popc(full & below);
+  uint32_t rank = bbw + s_pre[wi] + __popc(full & below);
   // coordinates of the thread's first cell (one division per dimension); a
   // set bit b adds b to the last coordinate, carried into the others only
   // when it passes the extent
@@ -1221,6 +1385,11 @@ __global__ __launch_bounds__(kBlock) void k_sc_emit(
       for (int j = 0; j < cout.D; ++j) out_coords[static_cast<int64_t>(rank) * cout.D + j] = yv[j];
     }
     if (out_keys) out_keys[rank] = pack_site(cout, yv);
+    if (og.grid) {
+      const uint32_t cell = grid_cell(og.g, yv);
+      og.grid[cell] = rank + 1;
+      if (og.bitmap) atomicOr(&og.bitmap[cell >> 5], 1u << (cell & 31));
+    }
     ++rank;
   }
 }
@@ -1256,35 +1425,6 @@ __global__ __launch_bounds__(kBlock) void k_morton(const uint64_t* __restrict__ 
 // Dense index grid (used when the grid is small enough to hold one int32 per
 // cell; the sites' cells are laid out along the Z-order curve)
 // ---------------------------------------------------------------------------
-// Cell of site (b, c_1..c_d) = b << B | Z(c), where Z interleaves the bits of
-// the spatial coordinates, most significant level first and coordinate 1
-// first inside a level, keeping only the bits a coordinate can have
-// (B = sum_j bits_j).  Walking cells in increasing order is the Z-order of
-// the sites.  M[j] marks the bits of Z that hold coordinate j.
-struct GridGeom {
-  int D;
-  int B;
-  uint32_t M[kMaxD];
-  int32_t size[kMaxD];
-};
-
-// Scatter bits of v into the set positions of m, lowest first.
-__host__ __device__ inline uint32_t deposit(uint32_t v, uint32_t m) {
-  uint32_t r = 0;
-  for (uint32_t bb = 1; m; bb <<= 1) {
-    const uint32_t low = m & (0u - m);
-    if (v & bb) r |= low;
-    m &= m - 1;
-  }
-  return r;
-}
-
-__device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* x) {
-  uint32_t cell = static_cast<uint32_t>(x[0]) << g.B;
-  for (int j = 1; j < g.D; ++j) cell |= deposit(static_cast<uint32_t>(x[j]), g.M[j]);
-  return cell;
-}
-
 // Place input row r at its cell: grid[cell] = r + 1 (0 = empty).  With CAS,
 // by compare-and-swap from 0, and a cell found taken is a duplicate site.
 // Without it a plain store; duplicates then leave fewer occupied cells than
@@ -1293,15 +1433,13 @@ __device__ __forceinline__ uint32_t grid_cell(const GridGeom& g, const int32_t* 
 // keys (SC marking).  With `count` set, only the first *count (<= N) rows
 // exist.
 // With `bitmap` set, the cell's occupancy bit is set too (the bitmap cleared
-// with the grid) and cellrow[r] receives r's cell (~0: out of range), for the
-// one-workgroup ranking of small grids.
+// with the grid), for the one-launch schedule of small grids.
 template <bool CAS>
 __global__ __launch_bounds__(kBlock) void k_grid_scatter(
     const int32_t* __restrict__ coords, int64_t N, const int64_t* __restrict__ count,
     GridGeom g, uint32_t* __restrict__ grid, int32_t* __restrict__ copy_out, Codec ckey,
     uint64_t* __restrict__ keys_out, uint32_t* __restrict__ status,
-    int64_t* __restrict__ count_copy, uint32_t* __restrict__ bitmap,
-    uint32_t* __restrict__ cellrow) {
+    int64_t* __restrict__ count_copy, uint32_t* __restrict__ bitmap) {
   const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   if (count_copy && r == 0) *count_copy = *count;   // the book's own copy of the row count
   if (r >= N || (count && r >= *count)) return;
@@ -1314,16 +1452,12 @@ __global__ __launch_bounds__(kBlock) void k_grid_scatter(
   }
   if (!ok) {
     if (keys_out) keys_out[r] = kEmpty;
-    if (cellrow) cellrow[r] = ~0u;
     atomicOr(status, kStRange);
     return;
   }
   if (keys_out) keys_out[r] = pack_site(ckey, x);
   const uint32_t cell = grid_cell(g, x);
-  if (bitmap) {
-    atomicOr(&bitmap[cell >> 5], 1u << (cell & 31));
-    cellrow[r] = cell;
-  }
+  if (bitmap) atomicOr(&bitmap[cell >> 5], 1u << (cell & 31));
   if (!CAS)
     grid[cell] = static_cast<uint32_t>(r + 1);
   else if (atomicCAS(&grid[cell], 0u, static_cast<uint32_t>(r + 1)) != 0u)
@@ -1394,93 +1528,71 @@ __global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict
     if ((word >> k) & 1u) perm[rank++] = static_cast<int32_t>(v[k]) - 1;
 }
 
-// Small grids (at most kRankWords bitmap words, at most kRankRows rows): one
-// workgroup replaces the bitmap, block-sum, scan and emit launches.  The
-// bitmap (set by the scatter) is ranked by a popcount prefix in LDS, every
-// thread taking a run of ceil(words / threads) words; then every row finds
-// its cell's rank, which is its schedule position.  The schedule is gathered
-// in LDS, kRankStage positions per pass, and stored in order: one compute
-// unit storing rows to scattered positions would spend a cycle per lane.
-// n_out = the occupied cells; a count other than `expect` (when >= 0), or
-// than *expect_dev (when given), flags duplicate sites.
-constexpr int kRankThreads = 1024;
-constexpr int kRankWords = 8192;
-constexpr int64_t kRankRows = 65535;
-constexpr int kRankStage = 24576;
-__global__ __launch_bounds__(kRankThreads) void k_grid_rank(
-    const uint32_t* __restrict__ bitmap, int nwords, const uint32_t* __restrict__ cellrow,
-    int64_t N, const int64_t* __restrict__ count, DeviceHeader* __restrict__ hdr, int64_t expect,
-    const int64_t* __restrict__ expect_dev, int32_t* __restrict__ perm) {
-  constexpr int WPT = kRankWords / kRankThreads;   // at most; wpt words per thread in fact
-  constexpr int NW = kRankThreads / kWave;
-  constexpr int RB = 16;                            // rows per thread in flight
-  __shared__ uint32_t s_bits[kRankWords];
-  __shared__ uint16_t s_pre[kRankWords];
-  __shared__ int32_t s_perm[kRankStage];
-  __shared__ uint32_t s_wsum[NW];
-  const int tid = threadIdx.x, wave = tid / kWave;
-  const int wpt = (nwords + kRankThreads - 1) / kRankThreads;
-  uint32_t cnt[WPT], sum = 0;
-  uint32_t v[WPT];
+// Small grids (at most kSelfWords bitmap words, the bitmap set by the
+// scatter): the schedule in one launch instead of three.  Blocks are laid
+// out as in k_sc_emit (bitmap block b / kEmitParts, its words' part b %
+// kEmitParts, kEmitParts threads per word); every block finds its bitmap
+// block's base itself, as the popcount of all the words before it (at most
+// kSelfWords words, loaded by all its threads at once), and each thread
+// emits the rows of its 4 cells (one 16-byte grid load).  The last bitmap
+// block sets n_out to the occupied cells; a count other than `expect` (when
+// >= 0), or than *expect_dev (when given), flags duplicate sites.
+__global__ __launch_bounds__(kBlock) void k_grid_emit_self(
+    const uint32_t* __restrict__ bitmap, uint64_t nwords, uint64_t cells,
+    const uint32_t* __restrict__ grid, int32_t* __restrict__ perm,
+    DeviceHeader* __restrict__ hdr, int64_t expect, const int64_t* __restrict__ expect_dev) {
+  constexpr int PER = kSelfWords / kBlock;
+  static_assert(kEmitBits == 4, "a thread's cells are one 16-byte group of the grid");
+  __shared__ uint32_t s_pre[kBlock];
+  __shared__ uint32_t s_word[kBlock];
+  const uint32_t bw = blockIdx.x / kEmitParts;
+  const int part = blockIdx.x % kEmitParts;
+  const uint32_t w0 = bw * kBlock;                 // first word of the bitmap block
+  uint32_t v[PER];
 #pragma unroll
-  for (int k = 0; k < WPT; ++k) {           // every load in flight at once (no branch)
-    const int w = tid * wpt + k;
-    v[k] = bitmap[w < nwords ? w : nwords - 1];
+  for (int k = 0; k < PER; ++k) {                  // every load in flight at once
+    const uint32_t idx = k * kBlock + threadIdx.x;
+    v[k] = bitmap[idx < w0 ? idx : 0u];
   }
+  const uint64_t wt = w0 + threadIdx.x;
+  const uint32_t tword = wt < nwords ? bitmap[wt] : 0u;
+  uint32_t before = 0;
 #pragma unroll
-  for (int k = 0; k < WPT; ++k) {
-    const int w = tid * wpt + k;
-    const bool mine = k < wpt && w < nwords;
-    if (mine) s_bits[w] = v[k];
-    cnt[k] = mine ? __popc(v[k]) : 0u;
-    sum += cnt[k];
-  }
-  const uint32_t inc = wave_incl_scan(sum);
-  if (lane_id() == kWave - 1) s_wsum[wave] = inc;
-  __syncthreads();
-  uint32_t ex = inc - sum, total = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    if (w < wave) ex += s_wsum[w];
-    total += s_wsum[w];
-  }
-#pragma unroll
-  for (int k = 0; k < WPT; ++k) {
-    const int w = tid * wpt + k;
-    if (k < wpt && w < nwords) s_pre[w] = static_cast<uint16_t>(ex);
-    ex += cnt[k];
-  }
-  __syncthreads();
-  if (tid == 0) {
-    const int64_t t = total;
+  for (int k = 0; k < PER; ++k) before += k * kBlock + threadIdx.x < w0 ? __popc(v[k]) : 0u;
+  uint32_t base, tot;
+  block_excl_scan<uint32_t>(before, &base);
+  s_word[threadIdx.x] = tword;
+  s_pre[threadIdx.x] = block_excl_scan<uint32_t>(__popc(tword), &tot);
+  if (blockIdx.x == gridDim.x - kEmitParts && threadIdx.x == 0) {
+    const int64_t t = static_cast<int64_t>(base) + tot;
     if ((expect >= 0 && t != expect) || (expect_dev && t != *expect_dev))
       atomicOr(&hdr->status, kStDup);
     hdr->n_out = t;
   }
-  const int64_t n = count ? *count : N;
-  for (uint32_t base = 0; base < total; base += kRankStage) {
-    for (int64_t r0 = 0; r0 < n; r0 += int64_t{RB} * kRankThreads) {
-      uint32_t cell[RB];
+  __syncthreads();
+  const int wi = part * (kBlock / kEmitParts) + threadIdx.x / kEmitParts;   // word in block
+  const int sub = threadIdx.x % kEmitParts;
+  const uint64_t w = w0 + wi;
+  if (w >= nwords) return;
+  const uint32_t full = s_word[wi];
+  const uint32_t bits = (full >> (sub * kEmitBits)) & ((1u << kEmitBits) - 1u);
+  if (!bits) return;
+  uint32_t rank = base + s_pre[wi] + __popc(full & ((1u << (sub * kEmitBits)) - 1u));
+  const uint64_t c0 = 32 * w + sub * kEmitBits;
+  uint32_t c[kEmitBits];
+  if (c0 + kEmitBits <= cells) {
+    const uint4 t = *reinterpret_cast<const uint4*>(grid + c0);
+    c[0] = t.x;
+    c[1] = t.y;
+    c[2] = t.z;
+    c[3] = t.w;
+  } else {
 #pragma unroll
-      for (int u = 0; u < RB; ++u) {         // the batch's loads first
-        const int64_t r = r0 + u * kRankThreads + tid;
-        cell[u] = r < n ? cellrow[r] : ~0u;
-      }
-#pragma unroll
-      for (int u = 0; u < RB; ++u) {
-        if (cell[u] == ~0u) continue;
-        const uint32_t w = cell[u] >> 5;
-        const uint32_t pos = s_pre[w] + __popc(s_bits[w] & ((1u << (cell[u] & 31)) - 1u)) - base;
-        if (pos < static_cast<uint32_t>(kRankStage))
-          s_perm[pos] = static_cast<int32_t>(r0 + u * kRankThreads + tid);
-      }
-    }
-    __syncthreads();
-    const uint32_t m = total - base < static_cast<uint32_t>(kRankStage) ? total - base
-                                                                         : kRankStage;
-    for (uint32_t t = tid; t < m; t += kRankThreads) perm[base + t] = s_perm[t];
-    __syncthreads();
+    for (int k = 0; k < kEmitBits; ++k) c[k] = c0 + k < cells ? grid[c0 + k] : 0u;
   }
+#pragma unroll
+  for (int k = 0; k < kEmitBits; ++k)
+    if ((bits >> k) & 1u) perm[rank++] = static_cast<int32_t>(c[k]) - 1;
 }
 
 typedef uint32_t dw4 __attribute__((ext_vector_type(4)));
@@ -1889,12 +2001,18 @@ int launch_insert(spconv_rulebook rb, const int32_t* coords, int64_t N, const Co
 }
 
 // Per-offset pair counts -> k_i and pair_off; gather map -> pair lists.
+// (Small books, at most kSelfScan words of counts read over all blocks: the
+// compaction sums the counts itself, one launch instead of two.)
+constexpr int64_t kSelfScan = int64_t{1} << 22;
 void launch_scan_compact(spconv_rulebook rb) {
-  k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
-                                                                  rb->totals);
-  k_compact<<<static_cast<unsigned>(rb->nblk), kBlock, 0, rb->stream>>>(
+  const bool self = rb->K * rb->nblk * rb->nblk <= kSelfScan;
+  if (!self)
+    k_scan<<<static_cast<unsigned>(rb->K), kBlock, 0, rb->stream>>>(rb->blk_cnt, rb->nblk,
+                                                                    rb->totals);
+  (self ? k_compact<true> : k_compact<false>)<<<static_cast<unsigned>(rb->nblk), kBlock, 0,
+                                               rb->stream>>>(
       rb->gmap, rb->perm, rb->blk_cnt, rb->wpre, rb->totals, static_cast<int>(rb->K), rb->gstride,
-      rb->hdr, rb->nblk, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
+      rb->n_cap, rb->hdr, rb->nblk, reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
 }
 
 void launch_probe_scan_compact(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
@@ -2082,36 +2200,34 @@ struct GridBufs {
   uint32_t* grid;     // [cells] 1 + row, 0 = empty
   uint32_t* bitmap;   // [nwords] occupancy (right after the grid)
   uint32_t* bsum;     // [nbw] occupied cells per 256 words, then their bases
-  uint32_t* cellrow;  // [rows] cell of every row, for a one-workgroup ranking; else NULL
+  bool self;          // small: the scatter sets the bitmap, one launch schedules
   uint64_t nwords;
   int64_t nbw;
 };
 
-// Whether a grid of `cells` cells scheduled for at most `rows` rows is ranked
-// by one workgroup (k_grid_rank) rather than by three launches.
-bool rank_in_one(uint64_t cells, int64_t rows) {
+// Whether a grid of `cells` cells is scheduled by one launch
+// (k_grid_emit_self, the bitmap set by the scatter) rather than by three.
+bool self_schedule(uint64_t cells) {
   if (const char* e = std::getenv("SPCONV_RULEBOOK"))
-    if (std::strcmp(e, "grid3") == 0) return false;    // test knob: the three-launch ranking
-  return (cells + 31) / 32 <= static_cast<uint64_t>(kRankWords) && rows <= kRankRows;
+    if (std::strcmp(e, "grid3") == 0) return false;    // test knob: the three-launch schedule
+  return (cells + 31) / 32 <= static_cast<uint64_t>(kSelfWords);
 }
 
-size_t grid_bytes(uint64_t cells, int64_t rows = -1) {
+size_t grid_bytes(uint64_t cells) {
   const uint64_t nwords = (cells + 31) / 32;
   const uint64_t nbw = (nwords + kBlock - 1) / kBlock;
-  const size_t cr = rows >= 0 && rank_in_one(cells, rows) ? align_up(rows * 4, 256) : 0;
-  return align_up(cells * 4, 256) + align_up(nwords * 4, 256) + align_up(nbw * 4, 256) + cr;
+  return align_up(cells * 4, 256) + align_up(nwords * 4, 256) + align_up(nbw * 4, 256);
 }
 
-// rows >= 0: the grid will be scheduled for at most that many rows.
-GridBufs take_grid(Carver* cv, uint64_t cells, int64_t rows = -1) {
+// sched: the grid will give a schedule.
+GridBufs take_grid(Carver* cv, uint64_t cells, bool sched = false) {
   GridBufs b{};
   b.nwords = (cells + 31) / 32;
   b.nbw = static_cast<int64_t>((b.nwords + kBlock - 1) / kBlock);
   b.grid = cv->take<uint32_t>(cells);
   b.bitmap = cv->take<uint32_t>(b.nwords);
   b.bsum = cv->take<uint32_t>(static_cast<size_t>(b.nbw));
-  b.cellrow = rows >= 0 && rank_in_one(cells, rows)
-                  ? cv->take<uint32_t>(static_cast<size_t>(rows > 0 ? rows : 1)) : nullptr;
+  b.self = sched && self_schedule(cells);
   return b;
 }
 
@@ -2122,28 +2238,25 @@ void launch_grid_scatter(spconv_rulebook rb, const int32_t* coords, int64_t N,
                          const int64_t* count, const GridGeom& g, uint64_t cells,
                          const GridBufs& b, int32_t* copy_out, const Codec& ckey,
                          uint64_t* keys_out, bool cas, int64_t init_n = -1) {
-  // with a one-workgroup ranking the scatter sets the bitmap as well, which
+  // with a one-launch schedule the scatter sets the bitmap as well, which
   // lies right after the grid and is cleared with it
-  const uint64_t nclear =
-      b.cellrow ? static_cast<uint64_t>(b.bitmap + b.nwords - b.grid) : cells;
+  const uint64_t nclear = b.self ? static_cast<uint64_t>(b.bitmap + b.nwords - b.grid) : cells;
   launch_zero(b.grid, nclear, rb->stream, init_n >= 0 ? rb->hdr : nullptr, init_n);
   auto kern = cas ? k_grid_scatter<true> : k_grid_scatter<false>;
   // a book on another book's outputs keeps its own copy of their count
   int64_t* cc = count && count == rb->in_count ? rb->n_in_dev : nullptr;
   kern<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, count, g, b.grid, copy_out, ckey,
                                                keys_out, &rb->hdr->status, cc,
-                                               b.cellrow ? b.bitmap : nullptr, b.cellrow);
+                                               b.self ? b.bitmap : nullptr);
 }
 
 // Z-order schedule from the grid; also sets n_out to the number of occupied
 // cells, flagging duplicates when that is not `expect` (>= 0).
 void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
-                          int64_t expect, const int64_t* expect_dev = nullptr,
-                          int64_t rows = 0, const int64_t* count = nullptr) {
-  if (b.cellrow) {
-    k_grid_rank<<<1, kRankThreads, 0, rb->stream>>>(b.bitmap, static_cast<int>(b.nwords),
-                                                    b.cellrow, rows, count, rb->hdr, expect,
-                                                    expect_dev, rb->perm);
+                          int64_t expect, const int64_t* expect_dev = nullptr) {
+  if (b.self) {
+    k_grid_emit_self<<<static_cast<unsigned>(b.nbw * kEmitParts), kBlock, 0, rb->stream>>>(
+        b.bitmap, b.nwords, cells, b.grid, rb->perm, rb->hdr, expect, expect_dev);
     return;
   }
   k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
@@ -2201,57 +2314,64 @@ int build_vsc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& g,
                    uint64_t cells) {
   const int64_t N = rb->n_in;
   void* mem = nullptr;
-  if (dev_alloc(rb, grid_bytes(cells, N) + 256, rb->stream, &mem) != SPCONV_OK)
+  if (dev_alloc(rb, grid_bytes(cells) + 256, rb->stream, &mem) != SPCONV_OK)
     return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
-  const GridBufs b = take_grid(&cv, cells, N);
+  const GridBufs b = take_grid(&cv, cells, true);
   // rows [0, N), or [0, *in_count) for a book on another book's outputs
   launch_grid_scatter(rb, coords, N, rb->in_count, g, cells, b, rb->out_coords, Codec{}, nullptr,
                       false, rb->in_count ? 0 : N);
-  launch_grid_schedule(rb, b, cells, rb->in_count ? -1 : N, rb->in_count, N, rb->in_count);
+  launch_grid_schedule(rb, b, cells, rb->in_count ? -1 : N, rb->in_count);
   launch_probe_grid(rb, rb->out_coords, g, b, cells);
   if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
-// SC on dense grids: input sites scattered into the input grid; the output
-// set marked in a lexicographic bitmap over the output grid and ranked (rows
-// in lexicographic order); the output sites then scattered into an output
-// grid whose bitmap gives the Z-order schedule.
+// SC on dense grids: input sites scattered into the input grid and, in the
+// same pass, the output set marked in a lexicographic bitmap over the output
+// grid; the bitmap ranked (rows in lexicographic order), and the emission of
+// the output sites fills the output grid, whose occupancy gives the Z-order
+// schedule.  Everything that must start at zero (input grid, lexicographic
+// bitmap, output grid and, for a one-launch schedule, its bitmap) is laid
+// out in one range and cleared by one launch.
 int build_sc_grid(spconv_rulebook rb, const int32_t* coords, const GridGeom& gi,
                   uint64_t cells_in, const GridGeom& go, uint64_t cells_out) {
   const int64_t N = rb->n_in;
-  const Codec cin = make_codec(rb->D, rb->size);
   const Codec cout = make_codec(rb->D, rb->out_size);
   uint64_t lex_cells = 1;
   for (int j = 0; j < rb->D; ++j) lex_cells *= static_cast<uint64_t>(rb->out_size[j]);
   const uint64_t lwords = (lex_cells + 31) / 32;
   const int64_t lnbw = static_cast<int64_t>((lwords + kBlock - 1) / kBlock);
-  const size_t bytes = grid_bytes(cells_in) + grid_bytes(cells_out, rb->n_cap) +
-                       align_up(lwords * 4, 256) +
-                       align_up(static_cast<size_t>(lnbw) * 4, 256) +
-                       align_up(static_cast<size_t>(N) * 8, 256) + 256;
+  const size_t bytes = align_up(cells_in * 4, 256) +
+                       align_up(lwords * 4, 256) + grid_bytes(cells_out) +
+                       align_up(static_cast<size_t>(lnbw) * 4, 256) + 256;
   void* mem = nullptr;
   if (dev_alloc(rb, bytes, rb->stream, &mem) != SPCONV_OK) return SPCONV_ENOMEM;
   Carver cv{static_cast<char*>(mem)};
-  const GridBufs bi = take_grid(&cv, cells_in);
-  const GridBufs bo = take_grid(&cv, cells_out, rb->n_cap);
+  GridBufs bi{};
+  bi.grid = cv.take<uint32_t>(cells_in);
   uint32_t* lex = cv.take<uint32_t>(lwords);
+  const GridBufs bo = take_grid(&cv, cells_out, true);
   uint32_t* lsum = cv.take<uint32_t>(static_cast<size_t>(lnbw));
-  uint64_t* keys = cv.take<uint64_t>(static_cast<size_t>(N));
+  uint32_t* from = bi.grid;
+  uint32_t* to = bo.self ? bo.bitmap + bo.nwords : bo.grid + cells_out;
+  launch_zero(from, static_cast<uint64_t>(to - from), rb->stream, rb->hdr, 0);
   Extents E{};
   for (int j = 0; j < rb->D; ++j) E.e[j] = rb->out_size[j];
-  launch_grid_scatter(rb, coords, N, rb->in_count, gi, cells_in, bi, nullptr, cin, keys, true, 0);
-  k_fill_u32<<<grid_for(static_cast<int64_t>(lwords)), kBlock, 0, rb->stream>>>(lex, 0u, lwords);
   const OffsetTable ot = make_offsets(rb);
-  k_sc_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(keys, N, rb->in_count, cin, ot, E, lex);
-  k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
-  k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1, nullptr);
+  // a book on another book's outputs keeps its own copy of their count
+  int64_t* cc = rb->in_count ? rb->n_in_dev : nullptr;
+  k_sc_scatter_mark<<<grid_for(N), kBlock, 0, rb->stream>>>(
+      coords, N, rb->in_count, gi, bi.grid, &rb->hdr->status, cc, ot, E, lex);
+  const bool lself = lwords <= static_cast<uint64_t>(kSelfWords);
+  if (!lself) {
+    k_bitsum<<<static_cast<unsigned>(lnbw), kBlock, 0, rb->stream>>>(lex, lwords, lsum);
+    k_bitscan<<<1, kBlock, 0, rb->stream>>>(lsum, lnbw, rb->hdr, -1, nullptr);
+  }
+  const OutGrid og{go, bo.grid, bo.self ? bo.bitmap : nullptr};
   k_sc_emit<<<static_cast<unsigned>(lnbw * kEmitParts), kBlock, 0, rb->stream>>>(
-      lex, lwords, lsum, cout, E, rb->out_coords, nullptr);
-  launch_grid_scatter(rb, rb->out_coords, rb->n_cap, &rb->hdr->n_out, go, cells_out, bo, nullptr,
-                      cout, nullptr, false);
-  launch_grid_schedule(rb, bo, cells_out, -1, nullptr, rb->n_cap, &rb->hdr->n_out);
+      lex, lwords, lself ? nullptr : lsum, cout, E, rb->out_coords, nullptr, og, rb->hdr);
+  launch_grid_schedule(rb, bo, cells_out, -1, nullptr);
   launch_probe_grid(rb, rb->out_coords, gi, bi, cells_in);
   if (dev_free(rb, mem, rb->stream) != SPCONV_OK) return SPCONV_EHIP;
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
@@ -2380,7 +2500,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_bitsum<<<static_cast<unsigned>(nbw), kBlock, 0, rb->stream>>>(bitmap, nwords, bsum);
     k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1, nullptr);
     k_sc_emit<<<static_cast<unsigned>(nbw * kEmitParts), kBlock, 0, rb->stream>>>(
-        bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys);
+        bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys, OutGrid{}, rb->hdr);
     launch_schedule(rb, out_keys, cout, &cv);
     launch_probe_scan_compact(rb, out_keys, cout, cin, tr);
   } else {
