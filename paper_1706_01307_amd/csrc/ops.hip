@@ -378,13 +378,14 @@ __global__ __launch_bounds__(256) void k_dw_partial(
 // Matrix-core partial products (bf16 inputs, fp32 accumulation): grid
 // (chunk, offset, 64x64 tile of dW^i).  Per step 128 pairs: their input rows
 // and gradient rows (this tile's 64 columns of each) are gathered into LDS
-// row-major, 8 lanes per 128-byte row; wave w multiplies pairs 32w..32w+31
-// of the step into its own 64x64 fp32 partial.  The contraction runs over
-// pairs, so an operand fragment holds one channel of 8 consecutive pairs: it
-// comes from the row-major tile through gfx950's transposing LDS read (16
-// lanes read 4 pairs x 16 channels, each lane receives one channel of the 4
-// pairs).  At the end of the chunk the 4 wave partials are added in wave
-// order through LDS.  Columns past C_in / C_out are zero.
+// row-major, 8 lanes per 128-byte row; wave w multiplies all pairs of the
+// step, 32 at a time in order, into its own 32x32 quadrant of the tile (so
+// each result is one in-order sum, written straight out, and a wave holds 16
+// accumulator registers, which lets four workgroups share a compute unit).
+// The contraction runs over pairs, so an operand fragment holds one channel
+// of 8 consecutive pairs: it comes from the row-major tile through gfx950's
+// transposing LDS read (16 lanes read 4 pairs x 16 channels, each lane
+// receives one channel of the 4 pairs).  Columns past C_in / C_out are zero.
 typedef short dw_s4 __attribute__((ext_vector_type(4)));
 typedef __bf16 dw_bf8 __attribute__((ext_vector_type(8)));
 typedef float dw_f4 __attribute__((ext_vector_type(4)));
@@ -414,16 +415,18 @@ __device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, 
 }
 
 template <bool DC>
-__global__ __launch_bounds__(256, 2) void k_dw_mfma(
+__global__ __launch_bounds__(256, 3) void k_dw_mfma(
     const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
     const int32_t* __restrict__ blk_base, int64_t nblk, const uint16_t* __restrict__ x,
     const uint16_t* __restrict__ dy, int C_in, int C_out, int K, int nchunk,
     float* __restrict__ part) {
   constexpr int STEP = 128;
   constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
-  // staging tiles; the final wave reduction reuses the same bytes
+  // staging tiles (the final wave reduction reuses the same bytes) and a ring
+  // of the pairs of four steps: 36 KB, so that four workgroups share a
+  // compute unit
   __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * STEP * 64];
-  __shared__ int2 s_pr[kChunk];                  // the chunk's pairs
+  __shared__ int2 s_pr[4][STEP];
   uint16_t* s_x = s_buf;
   uint16_t* s_g = s_buf + STEP * 64;
   DwChunk dc_;
@@ -446,25 +449,33 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
     return;
   }
 
-  // The chunk's pairs go to LDS once.  Then, over steps of STEP pairs: at
-  // step t the data rows of step t + 2 are gathered into one of two register
-  // sets, the MFMAs of step t run on the LDS tiles, and the rows of step t + 1
-  // (the other set) are written to LDS.  Every gather is unconditional (rows
-  // past the chunk and columns past C read row 0 / column 0 and are zeroed
-  // when staged), so no load sits under a branch and the in-order load
-  // counter keeps step t + 2's rows in flight while step t + 1's are waited on.
+  // Over steps of STEP pairs: at step t the pairs of step t + 3 are loaded
+  // (threads 0..STEP-1, one each) and, after the MFMAs, put in the LDS ring;
+  // the data rows of step t + 2 are gathered (their pairs from the ring) into
+  // one of two register sets, the MFMAs of step t run on the LDS tiles, and
+  // the rows of step t + 1 (the other set) are written to LDS.  Every load is
+  // unconditional (pairs past the chunk read its first pair; rows past the
+  // chunk and columns past C read row 0 / column 0 and are zeroed when
+  // staged), so no load sits under a branch, and the issue order (the pair
+  // before the rows) lets the in-order load counter keep the rows in flight
+  // while the pair is waited on.
   const int npairs = static_cast<int>(end - start);
-  for (int e = threadIdx.x; e < npairs; e += 256)
-    s_pr[e] = *reinterpret_cast<const int2*>(pairs + 2 * (base + start + e));
   const int ch = (threadIdx.x % 8) * 8;                // this lane's 8 columns
   const bool colx = ch < cx, colg = ch < cg;
   typedef dw_u4 Rows[PASS];
+  auto pair_load = [&](int t) __attribute__((always_inline)) -> int2 {
+    const int e = t * STEP + (threadIdx.x < STEP ? threadIdx.x : 0);
+    return *reinterpret_cast<const int2*>(pairs + 2 * (base + start + (e < npairs ? e : 0)));
+  };
+  auto pair_put = [&](int t, int2 v) __attribute__((always_inline)) {
+    if (threadIdx.x < STEP) s_pr[t & 3][threadIdx.x] = v;
+  };
   auto gather = [&](int t, Rows& vx, Rows& vg, uint32_t& ok) __attribute__((always_inline)) {
     ok = 0;
 #pragma unroll
     for (int pass = 0; pass < PASS; ++pass) {
       const int e = t * STEP + pass * 32 + threadIdx.x / 8;
-      const int2 pr = s_pr[e < npairs ? e : 0];
+      const int2 pr = s_pr[t & 3][pass * 32 + threadIdx.x / 8];
       // (input row, gradient row); DC reads its pairs backwards
       const int32_t ra = DC ? pr.y : pr.x, rg = DC ? pr.x : pr.y;
       const bool okx = e < npairs && colx, okg = e < npairs && colg;
@@ -485,38 +496,48 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
     }
   };
 
-  dw_f4 acc[4][4];
+  // wave w owns the 32 x 32 quadrant (channel blocks 2 (w / 2) + uu, gradient
+  // blocks 2 (w % 2) + vv) of the 64 x 64 tile, over all pairs of the chunk
+  const int ub = 2 * (wave / 2), vb = 2 * (wave % 2);
+  dw_f4 acc[2][2];
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = dw_f4{0.f, 0.f, 0.f, 0.f};
+    for (int v = 0; v < 2; ++v) acc[u][v] = dw_f4{0.f, 0.f, 0.f, 0.f};
 
   Rows xa, ga, xb, gb;
   uint32_t oka = 0, okb = 0;
-  __syncthreads();                             // pairs in LDS
+  pair_put(0, pair_load(0));
+  pair_put(1, pair_load(1));
+  pair_put(2, pair_load(2));
+  __syncthreads();
   gather(0, xa, ga, oka);
   gather(1, xb, gb, okb);
   stage(xa, ga, oka);
   __syncthreads();
-  const int p0 = wave * 32;
   // step t: the set holding step t + 1 is `nx`, the free set `fr`
   // (the gather of step t + 2 is issued even past the last step, as rows that
   // are all zeroed, so that the number of loads in flight never depends on t)
   auto step = [&](int t, Rows& nxx, Rows& nxg, uint32_t& nok, Rows& frx, Rows& frg,
                   uint32_t& fok) __attribute__((always_inline)) {
+    const int2 pn = pair_load(t + 3);
     gather(t + 2, frx, frg, fok);
-    dw_bf8 fa[4], fb[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) fa[u] = tr_frag(s_x, p0, u * 16, lane);
+    for (int kc = 0; kc < STEP / 32; ++kc) {   // the step's pairs, 32 at a time, in order
+      dw_bf8 fa[2], fb[2];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) fb[v] = tr_frag(s_g, p0, v * 16, lane);
+      for (int u = 0; u < 2; ++u) fa[u] = tr_frag(s_x, kc * 32, (ub + u) * 16, lane);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+      for (int v = 0; v < 2; ++v) fb[v] = tr_frag(s_g, kc * 32, (vb + v) * 16, lane);
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[v], acc[u][v], 0, 0, 0);
-    __syncthreads();                           // tiles free
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int v = 0; v < 2; ++v)
+          acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[v], acc[u][v], 0, 0, 0);
+    }
+    __syncthreads();                           // tiles (and ring slot t + 3 = t - 1) free
     if (t + 1 < nsteps) stage(nxx, nxg, nok);
+    pair_put(t + 3, pn);
     __syncthreads();
   };
   int t = 0;
@@ -525,25 +546,17 @@ __global__ __launch_bounds__(256, 2) void k_dw_mfma(
     step(t + 1, xa, ga, oka, xb, gb, okb);
   }
   if (t < nsteps) step(t, xb, gb, okb, xa, ga, oka);
-  // wave partials -> LDS (one 16-row band of the tile at a time), summed in
-  // wave order; lane (r, g) holds rows 4g + e, column r of each 16x16 block
-  float (*s_red)[16][64 + 4] = reinterpret_cast<float (*)[16][64 + 4]>(s_buf);
+  // lane (r, g) holds rows 4g + e, column r of each 16x16 block
   const int r = lane % 16, g = lane / 16;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
+  for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
+    for (int v = 0; v < 2; ++v)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s_red[wave][4 * g + e][v * 16 + r] = acc[u][v][e];
-    __syncthreads();
-    for (int t = threadIdx.x; t < 16 * 64; t += 256) {
-      const int rr = t / 64, cc = t % 64;
-      const float sum = ((s_red[0][rr][cc] + s_red[1][rr][cc]) + s_red[2][rr][cc]) + s_red[3][rr][cc];
-      const int c = c0 + u * 16 + rr, n = n0 + cc;
-      if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = sum;
-    }
-    __syncthreads();
-  }
+      for (int e = 0; e < 4; ++e) {
+        const int c = c0 + (ub + u) * 16 + 4 * g + e, n = n0 + (vb + v) * 16 + r;
+        if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = acc[u][v][e];
+      }
 }
 
 // dw[i][c][n] = sum over the chunks of R_i: chunk ch goes to accumulator
