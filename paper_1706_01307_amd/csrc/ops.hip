@@ -376,12 +376,14 @@ __global__ __launch_bounds__(256) void k_dw_partial(
 }
 
 // Matrix-core partial products (bf16 inputs, fp32 accumulation): grid
-// (chunk, offset, 64x64 tile of dW^i).  Per step 128 pairs: their input rows
+// (chunk, offset, 64x64 tile of dW^i).  Per step 64 pairs: their input rows
 // and gradient rows (this tile's 64 columns of each) are gathered into LDS
 // row-major, 8 lanes per 128-byte row; wave w multiplies all pairs of the
 // step, 32 at a time in order, into its own 32x32 quadrant of the tile (so
 // each result is one in-order sum, written straight out, and a wave holds 16
-// accumulator registers, which lets four workgroups share a compute unit).
+// accumulator registers; with 64-pair steps four workgroups share a compute
+// unit, which hides the gathers' latency better than larger steps with fewer
+// workgroups).
 // The contraction runs over pairs, so an operand fragment holds one channel
 // of 8 consecutive pairs: it comes from the row-major tile through gfx950's
 // transposing LDS read (16 lanes read 4 pairs x 16 channels, each lane
@@ -415,16 +417,14 @@ __device__ __forceinline__ dw_bf8 tr_frag(const uint16_t* tile, int p0, int c0, 
 }
 
 template <bool DC>
-__global__ __launch_bounds__(256, 3) void k_dw_mfma(
+__global__ __launch_bounds__(256, 4) void k_dw_mfma(
     const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
     const int32_t* __restrict__ blk_base, int64_t nblk, const uint16_t* __restrict__ x,
     const uint16_t* __restrict__ dy, int C_in, int C_out, int K, int nchunk,
     float* __restrict__ part) {
-  constexpr int STEP = 128;
+  constexpr int STEP = 64;
   constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
-  // staging tiles (the final wave reduction reuses the same bytes) and a ring
-  // of the pairs of four steps: 36 KB, so that four workgroups share a
-  // compute unit
+  // staging tiles and a ring of the pairs of four steps: 18 KB
   __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * STEP * 64];
   __shared__ int2 s_pr[4][STEP];
   uint16_t* s_x = s_buf;
