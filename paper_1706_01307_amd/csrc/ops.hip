@@ -388,6 +388,11 @@ __global__ __launch_bounds__(256) void k_dw_partial(
 // of 8 consecutive pairs: it comes from the row-major tile through gfx950's
 // transposing LDS read (16 lanes read 4 pairs x 16 channels, each lane
 // receives one channel of the 4 pairs).  Columns past C_in / C_out are zero.
+// dbpart != NULL (VSC): the workgroups of the centre offset, whose pairs are
+// every output row once, also sum the gradient rows (the bias gradient) with
+// two more products per 32 pairs, a fragment of ones times the staged rows,
+// in waves 0 and 1 of the first channel tile; dbpart[chunk][n] receives the
+// chunk's column sums.
 typedef short dw_s4 __attribute__((ext_vector_type(4)));
 typedef __bf16 dw_bf8 __attribute__((ext_vector_type(8)));
 typedef float dw_f4 __attribute__((ext_vector_type(4)));
@@ -421,7 +426,7 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
     const int32_t* __restrict__ pairs, const int64_t* __restrict__ pair_off,
     const int32_t* __restrict__ blk_base, int64_t nblk, const uint16_t* __restrict__ x,
     const uint16_t* __restrict__ dy, int C_in, int C_out, int K, int nchunk,
-    float* __restrict__ part) {
+    float* __restrict__ part, int centre, float* __restrict__ dbpart) {
   constexpr int STEP = 64;
   constexpr int PASS = STEP / 32;                      // 32 rows per pass of 256 lanes
   // staging tiles and a ring of the pairs of four steps: 18 KB
@@ -441,11 +446,14 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
   const int cx = C_in - c0 < 64 ? C_in - c0 : 64;     // valid columns of this tile
   const int cg = C_out - n0 < 64 ? C_out - n0 : 64;
   float* out = part + (static_cast<int64_t>(i) * nchunk + chunk) * C_in * C_out;
+  const bool dbt = dbpart && i == centre && c0 == 0;    // this tile sums the bias gradient
   if (nsteps == 0) {                                   // no pair of R_i in this chunk
     for (int t = threadIdx.x; t < 64 * 64; t += 256) {
       const int c = c0 + t / 64, n = n0 + t % 64;
       if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = 0.0f;
     }
+    if (dbt && threadIdx.x < 64 && n0 + threadIdx.x < C_out)
+      dbpart[static_cast<int64_t>(chunk) * C_out + n0 + threadIdx.x] = 0.0f;
     return;
   }
 
@@ -504,6 +512,11 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
   for (int u = 0; u < 2; ++u)
 #pragma unroll
     for (int v = 0; v < 2; ++v) acc[u][v] = dw_f4{0.f, 0.f, 0.f, 0.f};
+  const bool dbw = dbt && wave < 2;                    // waves 0, 1 cover all 4 column blocks
+  dw_f4 accb[2] = {dw_f4{0.f, 0.f, 0.f, 0.f}, dw_f4{0.f, 0.f, 0.f, 0.f}};
+  dw_bf8 ones;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) ones[k] = static_cast<__bf16>(1.0f);
 
   Rows xa, ga, xb, gb;
   uint32_t oka = 0, okb = 0;
@@ -534,6 +547,11 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
 #pragma unroll
         for (int v = 0; v < 2; ++v)
           acc[u][v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[v], acc[u][v], 0, 0, 0);
+      if (dbw) {
+#pragma unroll
+        for (int v = 0; v < 2; ++v)
+          accb[v] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, fb[v], accb[v], 0, 0, 0);
+      }
     }
     __syncthreads();                           // tiles (and ring slot t + 3 = t - 1) free
     if (t + 1 < nsteps) stage(nxx, nxg, nok);
@@ -557,6 +575,13 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
         const int c = c0 + (ub + u) * 16 + 4 * g + e, n = n0 + (vb + v) * 16 + r;
         if (c < C_in && n < C_out) out[static_cast<int64_t>(c) * C_out + n] = acc[u][v][e];
       }
+  if (dbw && g == 0) {                                 // every row of accb holds the sums
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const int n = n0 + (vb + v) * 16 + r;
+      if (n < C_out) dbpart[static_cast<int64_t>(chunk) * C_out + n] = accb[v][0];
+    }
+  }
 }
 
 // dw[i][c][n] = sum over the chunks of R_i: chunk ch goes to accumulator
@@ -877,6 +902,15 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
   const int K = static_cast<int>(rb->K);
   float* part = static_cast<float*>(ws);
   const int64_t per = static_cast<int64_t>(C_in) * C_out;
+  // VSC on the matrix cores: the bias gradient comes from the weight
+  // gradient's centre-offset workgroups (its pairs are every output row once,
+  // each with itself), per chunk, into the bias partials' area (at least
+  // nchunk rows of C_out floats)
+  int centre = 0;
+  for (int j = 0; j < rb->D; ++j) centre = centre * rb->f[j] + (rb->f[j] - 1) / 2;
+  const bool db_fused = db && op == SPCONV_OP_VSC && nchunk > 0 && dt == SPCONV_BF16 &&
+                        C_in % 8 == 0 && C_out % 8 == 0;
+  float* partb_fused = part + static_cast<int64_t>(rb->K) * nchunk * per;
   if (nchunk > 0) {
     const int tiles = ((C_in + 63) / 64) * ((C_out + 63) / 64);
     // (offset, chunk) pairs: 8 XCDs x K offsets x ceil(nchunk / 8) chunks each
@@ -888,7 +922,8 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
       auto kern = dc ? k_dw_mfma<true> : k_dw_mfma<false>;
       kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, rb->blk_cnt, rb->nblk,
                                  static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(dy),
-                                 C_in, C_out, K, nchunk, part);
+                                 C_in, C_out, K, nchunk, part, db_fused ? centre : -1,
+                                 db_fused ? partb_fused : nullptr);
     } else if (dt == SPCONV_F32) {
       auto kern = dc ? k_dw_partial<float, true> : k_dw_partial<float, false>;
       kern<<<grid, 256, 0, st>>>(rb->pairs, rb->pair_off, rb->blk_cnt, rb->nblk,
@@ -902,7 +937,9 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
     }
   }
   k_dw_reduce<<<grid_of(rb->K * per, 1ll << 30), 256, 0, st>>>(part, K, C_in, C_out, nchunk, dw);
-  if (db) {
+  if (db_fused) {
+    k_db_reduce<<<(C_out + 3) / 4, 256, 0, st>>>(partb_fused, nchunk, C_out, db);
+  } else if (db) {
     const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_out;
     const int nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
     float* partb = part + static_cast<int64_t>(rb->K) * nchunk * per;
