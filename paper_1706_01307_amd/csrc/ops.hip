@@ -98,11 +98,17 @@ inline unsigned grid_of(int64_t n, int64_t cap = 65536) {
 // ---------------------------------------------------------------------------
 // Pooling
 // ---------------------------------------------------------------------------
+// Thread = (output position, VEC channels).  The gather-map entries of 8
+// offsets are loaded together, then their input rows (an absent neighbour
+// reads row 0 and is not taken), so the loads of a batch are in flight at
+// once instead of one offset after another behind a branch; the rows are
+// taken in ascending offset order.
 template <typename T, int VEC, bool MAX>
 __global__ __launch_bounds__(256) void k_pool(const int32_t* __restrict__ gmap,
                                               const int32_t* __restrict__ perm, int64_t gstride,
                                               const DeviceHeader* __restrict__ hdr, int K,
                                               const T* __restrict__ x, T* __restrict__ y, int C) {
+  constexpr int KB = 8;
   const int nch = C / VEC;
   const int64_t total = hdr->n_out * nch;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
@@ -113,18 +119,31 @@ __global__ __launch_bounds__(256) void k_pool(const int32_t* __restrict__ gmap,
     float acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;   // MP: the zero vector; AP: empty sum
-    for (int i = 0; i < K; ++i) {
-      const int32_t g = gmap[i * gstride + p] - 1;
-      if (g < 0) continue;
-      float v[VEC];
-      const int64_t base = static_cast<int64_t>(g) * C + c0;
-      if constexpr (VEC == 1) {
-        v[0] = IO<T>::ld(x, base);
-      } else {
-        IO<T>::ld16(x, base, v);
+    for (int i0 = 0; i0 < K; i0 += KB) {
+      int32_t g[KB];
+#pragma unroll
+      for (int u = 0; u < KB; ++u) {
+        const int i = i0 + u < K ? i0 + u : K - 1;
+        g[u] = gmap[i * gstride + p] - 1;
       }
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] = MAX ? fmaxf(acc[e], v[e]) : acc[e] + v[e];
+      for (int u = 0; u < KB; ++u) g[u] = i0 + u < K ? g[u] : -1;
+      float v[KB][VEC];
+#pragma unroll
+      for (int u = 0; u < KB; ++u) {
+        const int64_t base = static_cast<int64_t>(g[u] >= 0 ? g[u] : 0) * C + c0;
+        if constexpr (VEC == 1) {
+          v[u][0] = IO<T>::ld(x, base);
+        } else {
+          IO<T>::ld16(x, base, v[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < KB; ++u) {
+        if (g[u] < 0) continue;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = MAX ? fmaxf(acc[e], v[u][e]) : acc[e] + v[u][e];
+      }
     }
     if constexpr (!MAX) {
       const float k = static_cast<float>(K);
