@@ -24,7 +24,8 @@ __device__ __forceinline__ uint64_t lanes_below() {
 }
 
 // ---------------------------------------------------------------------------
-// Exclusive scan of a uint32 array of `n` elements (three launches).
+// Exclusive scan of a uint32 array of `n` elements (three launches, two when
+// there are at most kSelfParts chunks).
 // ---------------------------------------------------------------------------
 constexpr int kScanChunk = 4 * kBlock;          // elements per scan block
 
@@ -91,6 +92,11 @@ __global__ __launch_bounds__(kBlock) void k_scan_top(uint32_t* __restrict__ part
   }
 }
 
+// (SELF: `part` holds the chunk sums themselves, not yet scanned; every block
+// adds up those before its own, at most kSelfParts of them, in place of
+// k_scan_top.)
+constexpr int64_t kSelfParts = 4 * kBlock;
+template <bool SELF>
 __global__ __launch_bounds__(kBlock) void k_scan_apply(uint32_t* __restrict__ a, int64_t n,
                                                        const uint32_t* __restrict__ part) {
   const int64_t base = blockIdx.x * static_cast<int64_t>(kScanChunk) + 4 * threadIdx.x;
@@ -100,8 +106,22 @@ __global__ __launch_bounds__(kBlock) void k_scan_apply(uint32_t* __restrict__ a,
     v[u] = base + u < n ? a[base + u] : 0u;
     sum += v[u];
   }
+  uint32_t pbase;
+  if constexpr (SELF) {
+    uint32_t pv = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = 4 * threadIdx.x + u;
+      pv += k < static_cast<int64_t>(blockIdx.x) ? part[k] : 0u;
+    }
+    uint32_t ptot;
+    block_excl<uint32_t>(pv, &ptot);
+    pbase = ptot;
+  } else {
+    pbase = part[blockIdx.x];
+  }
   uint32_t tot;
-  uint32_t ex = block_excl<uint32_t>(sum, &tot) + part[blockIdx.x];
+  uint32_t ex = block_excl<uint32_t>(sum, &tot) + pbase;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     if (base + u < n) a[base + u] = ex;
@@ -208,8 +228,12 @@ bool radix_sort_pairs(uint64_t* keys, int32_t* vals, uint64_t* keys_tmp, int32_t
     k_rs_hist<<<static_cast<unsigned>(nblocks), kBlock, 0, stream>>>(ki, hdr, shift, nblocks,
                                                                       hist);
     k_scan_reduce<<<static_cast<unsigned>(np), kBlock, 0, stream>>>(hist, nh, part);
-    k_scan_top<<<1, kBlock, 0, stream>>>(part, np);
-    k_scan_apply<<<static_cast<unsigned>(np), kBlock, 0, stream>>>(hist, nh, part);
+    if (np <= kSelfParts) {
+      k_scan_apply<true><<<static_cast<unsigned>(np), kBlock, 0, stream>>>(hist, nh, part);
+    } else {
+      k_scan_top<<<1, kBlock, 0, stream>>>(part, np);
+      k_scan_apply<false><<<static_cast<unsigned>(np), kBlock, 0, stream>>>(hist, nh, part);
+    }
     k_rs_scatter<<<static_cast<unsigned>(nblocks), kBlock, 0, stream>>>(ki, vi, ko, vo, hdr,
                                                                          shift, nblocks, hist);
     flipped = !flipped;
