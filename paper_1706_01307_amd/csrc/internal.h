@@ -246,7 +246,8 @@ int build_sc(spconv_rulebook rb, const int32_t* coords);
 size_t radix_sort_scratch_bytes(int64_t n_cap);
 bool radix_sort_pairs(uint64_t* keys, int32_t* vals, uint64_t* keys_tmp, int32_t* vals_tmp,
                       const DeviceHeader* hdr, int64_t n_cap, int key_bits, void* scratch,
-                      hipStream_t stream);
+                      hipStream_t stream, int lo_bit = 0);
+int radix_sort_passes(int key_bits, int lo_bit);
 
 FwdView view_of(spconv_rulebook rb);
 // wmode 0: W^i = w[i] ([K][C_in][C_out]); 1: w[K-1-i]^T; 2: w[i]^T (w given

@@ -25,11 +25,13 @@
 //                                 G[i][p] (1 + input row, 0 if none)
 // Hashed (any grid up to 65535 per side):
 //   VSC: sorted bricks.  k_site_keys + k_morton + radix sort order the sites
-//   along the Z-order curve (the schedule); runs of one brick (2^b cells per
-//   coordinate) are numbered (k_brick_flags / k_bitscan / k_bricks), each
-//   brick inserted once into a hash directory; k_pool_fill writes the bricks'
-//   cells into a Z-ordered pool, k_brick_nbrs the neighbour bricks of every
-//   brick, and k_probe_brick looks up every neighbour with one pool load.
+//   by brick (2^b cells per coordinate; the Morton code's bits above the
+//   brick's own); runs of one brick are numbered (k_brick_flags / k_bitscan /
+//   k_bricks), each brick inserted once into a hash directory; k_pool_fill
+//   writes the bricks' cells into a Z-ordered pool and puts every run in cell
+//   order, which completes the Z-order schedule; k_brick_nbrs finds the
+//   neighbour bricks of every brick, and k_probe_brick looks up every
+//   neighbour with one pool load.
 //   SC (and SPCONV_RULEBOOK=table): an open-addressing table of sites,
 //   k_insert (pack every site into an order-preserving key; CAS-insert it,
 //   range errors, duplicates), k_morton + radix sort for the schedule, and
@@ -813,28 +815,41 @@ __global__ __launch_bounds__(kBlock) void k_bricks(
 // Pool entries of every brick, one wave per brick (bricks dealt out in steps
 // of the grid's waves): the run's sites go into an LDS image of the brick,
 // which the wave then stores whole (zeros included) in one coalesced pass.
+// The schedule was sorted by brick only: the occupied cells of the image, in
+// cell order, are the run's sites in Morton order, and the wave writes them
+// back over the run (codes and rows).  Two sites on one cell are duplicates.
 constexpr int kPoolBlocks = 2048;
 __global__ __launch_bounds__(kBlock) void k_pool_fill(
-    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
+    uint64_t* __restrict__ mk, int32_t* __restrict__ perm,
     const uint64_t* __restrict__ validbits, int64_t n, const int64_t* __restrict__ starts,
-    BrickMap m) {
+    BrickMap m, uint32_t* __restrict__ status) {
   __shared__ int32_t s_img[kBlock / kWave][kBrickCells];
   const int lane = lane_id(), wave = threadIdx.x / kWave;
   const int64_t nbr = m.nbricks->n_out;
   const int cells = 1 << m.lb;
   const uint64_t lowmask = static_cast<uint64_t>(cells - 1);
   const int64_t nw = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  bool dup = false;
   for (int64_t bi = blockIdx.x * static_cast<int64_t>(kBlock / kWave) + wave; bi < nbr; bi += nw) {
     const int64_t first = starts[bi];
     const int64_t last = bi + 1 < nbr ? starts[bi + 1] : n;
+    const uint64_t brick = mk[first] >> m.lb;      // a run starts on a site in range
     s_img[wave][lane] = 0;
     for (int64_t q0 = first; q0 < last; q0 += kWave) {
       const int64_t q = q0 + lane;
       if (q < last && ((validbits[q >> 6] >> (q & 63)) & 1ull))
-        s_img[wave][mk[q] & lowmask] = perm[q] + 1;
+        dup |= atomicExch(&s_img[wave][mk[q] & lowmask], perm[q] + 1) != 0;
     }
-    if (lane < cells) m.pool[(bi << m.lb) + lane] = s_img[wave][lane];
+    const int32_t v = lane < cells ? s_img[wave][lane] : 0;
+    if (lane < cells) m.pool[(bi << m.lb) + lane] = v;
+    const uint64_t occ = __ballot(v != 0);
+    if (v != 0) {
+      const int64_t pos = first + __popcll(occ & ((1ull << lane) - 1));
+      perm[pos] = v - 1;
+      mk[pos] = (brick << m.lb) | static_cast<uint64_t>(lane);
+    }
   }
+  if (dup) atomicOr(status, kStDup);
 }
 
 // Neighbour bricks of every brick: entry [bi][t] = the number of the brick
@@ -1956,9 +1971,11 @@ size_t schedule_bytes(int64_t n_cap) {
 }
 
 // Output rows in Morton order -> rb->perm (scratch carved from the transient
-// allocation by `cv`); returns the sorted Morton codes.
+// allocation by `cv`); returns the sorted Morton codes.  With lo_bit > 0 the
+// lowest lo_bit bits of the codes are left out of the sort (the brick map
+// orders each brick's sites itself).
 const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
-                                Carver* cv) {
+                                Carver* cv, int lo_bit) {
   const int64_t n = rb->n_cap;
   int maxb = 0, sbits = 0;
   for (int j = 1; j < crow.D; ++j) {
@@ -1969,7 +1986,7 @@ const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, con
   const int total = sbits + bitlen(crow.fmask[0]);
   // the values ping-pong between two arrays, one of them the schedule itself,
   // chosen so that the last pass lands in it
-  const bool odd = ((total + 7) / 8) % 2 == 1;
+  const bool odd = radix_sort_passes(total, lo_bit) % 2 == 1;
   uint64_t* mk = cv->take<uint64_t>(n);
   uint64_t* mk2 = cv->take<uint64_t>(n);
   int32_t* mv = odd ? cv->take<int32_t>(n) : rb->perm;
@@ -1981,7 +1998,8 @@ const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, con
     case 3: k_morton<3><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
     default: k_morton<4><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
   }
-  const bool in_tmp = radix_sort_pairs(mk, mv, mk2, mv2, rb->hdr, n, total, scratch, rb->stream);
+  const bool in_tmp =
+      radix_sort_pairs(mk, mv, mk2, mv2, rb->hdr, n, total, scratch, rb->stream, lo_bit);
   return in_tmp ? mk2 : mk;
 }
 
@@ -2118,7 +2136,8 @@ int build_vsc_bricks(spconv_rulebook rb, const int32_t* coords, BrickMap m) {
   uint16_t* tab = cv.take<uint16_t>(static_cast<size_t>(kBrickCells) * kBrickK);
   k_site_keys<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, cin, keys, rb->out_coords,
                                                       &rb->hdr->status);
-  const uint64_t* mk = launch_schedule(rb, keys, cin, &cv);
+  // sorted by brick only; k_pool_fill puts each brick's sites in cell order
+  uint64_t* mk = const_cast<uint64_t*>(launch_schedule(rb, keys, cin, &cv, m.lb));
   const OffsetTable ot = make_offsets(rb);
   const int64_t ntab = (int64_t{1} << m.lb) * ot.K;
   const int64_t fb = nb > (ntab + kBlock - 1) / kBlock ? nb : (ntab + kBlock - 1) / kBlock;
@@ -2130,7 +2149,8 @@ int build_vsc_bricks(spconv_rulebook rb, const int32_t* coords, BrickMap m) {
   k_bricks<<<static_cast<unsigned>(nb), kBlock, 0, rb->stream>>>(mk, rb->perm, N, flagbits,
                                                                  validbits, bsum, m, brickidx,
                                                                  starts);
-  k_pool_fill<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, validbits, N, starts, m);
+  k_pool_fill<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, validbits, N, starts, m,
+                                              &rb->hdr->status);
   k_brick_nbrs<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, keys, starts, cin, m, nb3, nbr);
   const unsigned g = probe_grid_size(rb->nblk);
   auto launch = [&](auto kern) {
@@ -2452,7 +2472,7 @@ int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   if (st != SPCONV_OK) return st;
   launch_insert(rb, coords, N, cin, tr, rb->out_coords);
   if (N > 0) {
-    launch_schedule(rb, tr.keys, cin, &cv);
+    launch_schedule(rb, tr.keys, cin, &cv, 0);
     launch_probe_scan_compact(rb, tr.keys, cin, cin, tr);
   }
   else
@@ -2501,7 +2521,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1, nullptr);
     k_sc_emit<<<static_cast<unsigned>(nbw * kEmitParts), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys, OutGrid{}, rb->hdr);
-    launch_schedule(rb, out_keys, cout, &cv);
+    launch_schedule(rb, out_keys, cout, &cv, 0);
     launch_probe_scan_compact(rb, out_keys, cout, cin, tr);
   } else {
     k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,
