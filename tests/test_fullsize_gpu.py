@@ -114,6 +114,35 @@ def test_fullsize_headline_surf128x8_c64_bf16():
     assert torch.equal(y0, y2.view(torch.int16))
 
 
+def test_fullsize_headline_on_the_hashed_site_map(monkeypatch):
+    """The headline book built on the hashed site map (sorted bricks: the
+    sites sorted by their brick bits only, two 9-bit radix passes, each
+    brick's run put in cell order by the pool fill) is the oracle's, bit for
+    bit, and its forward equals the dense grid's bit for bit; a duplicate
+    site placed far from its twin in the input is reported."""
+    wl = inputs.make_workload("surf128x8_vsc3_c64_bf16")
+    N = len(wl.coords)
+    f = [1, 3, 3, 3]
+    x = _bf16_tensor(inputs.to_bf16_bits(inputs.normal_f32((N, 64), seed=61)))
+    w, b = make_layer(62, 27, 64, 64, "bf16")
+    wd, bd = _bf16_tensor(w), _t(b)
+    monkeypatch.setenv("SPCONV_RULEBOOK", "grid")
+    rbg = spc.build_rulebook(spc.VSC, _t(wl.coords), wl.spatial_size, f)
+    yg = spc.vsc_forward(rbg, x, wd, bd)
+    monkeypatch.setenv("SPCONV_RULEBOOK", "hash")
+    rbh = spc.build_rulebook(spc.VSC, _t(wl.coords), wl.spatial_size, f)
+    yh = spc.vsc_forward(rbh, x, wd, bd)
+    torch.cuda.synchronize()
+    assert torch.equal(yg.view(torch.int16), yh.view(torch.int16))
+    ref = oracle.Rulebook(oracle.VSC, wl.coords, wl.spatial_size, f)
+    oc, pairs = rbh.export()
+    check_rulebook(oc.cpu().numpy(), pairs.cpu().numpy(), rbh.pair_off, ref)
+    _say(f"[hash headline] N={N}: book exact, forward equal to the grid's")
+    dup = np.concatenate([wl.coords, wl.coords[N // 3:N // 3 + 1]], axis=0)
+    st = spc.build_rulebook(spc.VSC, _t(dup), wl.spatial_size, f, sync=False).status()
+    assert st == spc.EDUP
+
+
 def test_fullsize_surf64x16_c32_f32():
     _full_check("surf64x16_vsc3_c32")
 
