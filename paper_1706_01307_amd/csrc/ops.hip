@@ -603,26 +603,45 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
   }
 }
 
-// dw[i][c][n] = sum over the chunks of R_i: chunk ch goes to accumulator
-// ch mod 8, the 8 accumulators are added in order (a fixed order, so the
-// result is reproducible, with 8 loads in flight per lane).
+// dw[i][c][n] = sum over the chunks of R_i.  The chunks are split into S
+// consecutive segments (S = 1, 2, 4 or 8, chosen on the host so that small
+// weight tensors still fill the device); in a segment chunk ch goes to
+// accumulator ch mod 8 and the 8 accumulators are added in a fixed tree; the
+// segments' sums are added in a fixed tree through LDS.  Every order is
+// fixed, so the result is reproducible.  A workgroup covers 256 / S
+// consecutive elements; its threads with the same segment read consecutive
+// elements of a partial.
 __global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ part, int K,
-                                                   int C_in, int C_out, int nch,
+                                                   int C_in, int C_out, int nch, int S,
                                                    float* __restrict__ dw) {
+  __shared__ float s_seg[256];
   const int64_t per = static_cast<int64_t>(C_in) * C_out;
-  const int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
-  if (idx >= K * per) return;
-  const int i = static_cast<int>(idx / per);
-  const int64_t rem = idx - i * per;
-  const float* p = part + static_cast<int64_t>(i) * nch * per + rem;
+  const int E = 256 / S;                       // elements per workgroup
+  const int el = threadIdx.x % E, seg = threadIdx.x / E;
+  const int64_t idx = blockIdx.x * static_cast<int64_t>(E) + el;
+  const bool live = idx < K * per;
+  const int L = (nch + S - 1) / S;
+  const int c0 = seg * L < nch ? seg * L : nch;
+  const int c1 = c0 + L < nch ? c0 + L : nch;
   float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  int ch = 0;
-  for (; ch + 8 <= nch; ch += 8) {
+  if (live) {
+    const int i = static_cast<int>(idx / per);
+    const int64_t rem = idx - i * per;
+    const float* p = part + static_cast<int64_t>(i) * nch * per + rem;
+    int ch = c0;
+    for (; ch + 8 <= c1; ch += 8) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
+      for (int j = 0; j < 8; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
+    }
+    for (int j = 0; ch + j < c1; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
   }
-  for (int j = 0; ch + j < nch; ++j) a[j] += p[static_cast<int64_t>(ch + j) * per];
-  dw[idx] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  s_seg[threadIdx.x] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  __syncthreads();
+  for (int h = S / 2; h >= 1; h /= 2) {        // segment t += segment t + h, t < h
+    if (seg < h) s_seg[threadIdx.x] += s_seg[threadIdx.x + h * E];
+    __syncthreads();
+  }
+  if (seg == 0 && live) dw[idx] = s_seg[threadIdx.x];
 }
 
 // Bias gradient, stage 1: a chunk of kRowChunk rows per workgroup and up to
@@ -955,7 +974,18 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
                                  C_in, C_out, K, nchunk, part);
     }
   }
-  k_dw_reduce<<<grid_of(rb->K * per, 1ll << 30), 256, 0, st>>>(part, K, C_in, C_out, nchunk, dw);
+  {
+    // segments per element: enough threads for the device (~128 K), at
+    // least 8 chunks per segment (more segments did not speed up the
+    // headline's 95 MB of partials)
+    const int64_t elems = static_cast<int64_t>(rb->K) * per;
+    int S = 1;
+    while (S < 8 && elems * S < (int64_t{1} << 17) && nchunk / (2 * S) >= 8) S *= 2;
+    const int64_t E = 256 / S;
+    if (elems > 0)
+      k_dw_reduce<<<static_cast<unsigned>((elems + E - 1) / E), 256, 0, st>>>(
+          part, K, C_in, C_out, nchunk, S, dw);
+  }
   if (db_fused) {
     k_db_reduce<<<(C_out + 3) / 4, 256, 0, st>>>(partb_fused, nchunk, C_out, db);
   } else if (db) {
