@@ -603,6 +603,38 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
   }
 }
 
+// Bias gradient, stage 2 (workgroups of k_dw_reduce past the weight's): 4
+// columns per workgroup; lane (phase q of 64, column) adds chunk partials q,
+// q + 64, ... eight loads at a time into 8 accumulators (by round), then the
+// 64 phases are added in a fixed tree.
+__device__ void db_reduce_block(const float* __restrict__ partb, int nchunks, int C_out,
+                                float* __restrict__ db, int blk) {
+  constexpr int kPh = 64, kCols = 4;
+  __shared__ float s[kPh][kCols + 1];
+  const int q = threadIdx.x / kCols, cn = threadIdx.x % kCols;
+  const int n = blk * kCols + cn;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (n < C_out) {
+    int ch = q;
+    for (; ch + 7 * kPh < nchunks; ch += 8 * kPh) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = partb[static_cast<int64_t>(ch + u * kPh) * C_out + n];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a[u] += v[u];
+    }
+    for (int u = 0; ch < nchunks; ch += kPh, ++u)
+      a[u] += partb[static_cast<int64_t>(ch) * C_out + n];
+  }
+  s[q][cn] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  __syncthreads();
+  for (int h = kPh / 2; h >= 1; h >>= 1) {
+    if (q < h) s[q][cn] += s[q + h][cn];
+    __syncthreads();
+  }
+  if (q == 0 && n < C_out) db[n] = s[0][cn];
+}
+
 // dw[i][c][n] = sum over the chunks of R_i.  The chunks are split into S
 // consecutive segments (S = 1, 2, 4 or 8, chosen on the host so that small
 // weight tensors still fill the device); in a segment chunk ch goes to
@@ -610,10 +642,17 @@ __global__ __launch_bounds__(256, 4) void k_dw_mfma(
 // segments' sums are added in a fixed tree through LDS.  Every order is
 // fixed, so the result is reproducible.  A workgroup covers 256 / S
 // consecutive elements; its threads with the same segment read consecutive
-// elements of a partial.
+// elements of a partial.  Workgroups from nb_dw on reduce the bias
+// gradient's partials instead (db_reduce_block).
 __global__ __launch_bounds__(256) void k_dw_reduce(const float* __restrict__ part, int K,
                                                    int C_in, int C_out, int nch, int S,
-                                                   float* __restrict__ dw) {
+                                                   float* __restrict__ dw, int64_t nb_dw,
+                                                   const float* __restrict__ partb, int nrc,
+                                                   float* __restrict__ db) {
+  if (blockIdx.x >= nb_dw) {
+    db_reduce_block(partb, nrc, C_out, db, static_cast<int>(blockIdx.x - nb_dw));
+    return;
+  }
   __shared__ float s_seg[256];
   const int64_t per = static_cast<int64_t>(C_in) * C_out;
   const int E = 256 / S;                       // elements per workgroup
@@ -712,36 +751,6 @@ __global__ __launch_bounds__(256) void k_db_partial(const T* __restrict__ dy, in
   }
 }
 
-// Bias gradient, stage 2: 4 columns per workgroup; lane (phase q of 64,
-// column) adds chunk partials q, q + 64, ... eight loads at a time into 8
-// accumulators (by round), then the 64 phases are added in a fixed tree.
-__global__ __launch_bounds__(256) void k_db_reduce(const float* __restrict__ partb, int nchunks,
-                                                   int C_out, float* __restrict__ db) {
-  constexpr int kPh = 64, kCols = 4;
-  __shared__ float s[kPh][kCols + 1];
-  const int q = threadIdx.x / kCols, cn = threadIdx.x % kCols;
-  const int n = blockIdx.x * kCols + cn;
-  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (n < C_out) {
-    int ch = q;
-    for (; ch + 7 * kPh < nchunks; ch += 8 * kPh) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = partb[static_cast<int64_t>(ch + u * kPh) * C_out + n];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) a[u] += v[u];
-    }
-    for (int u = 0; ch < nchunks; ch += kPh, ++u)
-      a[u] += partb[static_cast<int64_t>(ch) * C_out + n];
-  }
-  s[q][cn] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
-  __syncthreads();
-  for (int h = kPh / 2; h >= 1; h >>= 1) {
-    if (q < h) s[q][cn] += s[q + h][cn];
-    __syncthreads();
-  }
-  if (q == 0 && n < C_out) db[n] = s[0][cn];
-}
 
 int64_t dw_nchunk(spconv_rulebook rb) {
   constexpr int64_t kBpc = kChunk / kBlock;
@@ -974,35 +983,42 @@ int backward_weight(spconv_rulebook rb, int op, int dt, const void* x, const voi
                                  C_in, C_out, K, nchunk, part);
     }
   }
-  {
-    // segments per element: enough threads for the device (~128 K), at
-    // least 8 chunks per segment (more segments did not speed up the
-    // headline's 95 MB of partials)
-    const int64_t elems = static_cast<int64_t>(rb->K) * per;
-    int S = 1;
-    while (S < 8 && elems * S < (int64_t{1} << 17) && nchunk / (2 * S) >= 8) S *= 2;
-    const int64_t E = 256 / S;
-    if (elems > 0)
-      k_dw_reduce<<<static_cast<unsigned>((elems + E - 1) / E), 256, 0, st>>>(
-          part, K, C_in, C_out, nchunk, S, dw);
-  }
+  // bias-gradient partials: from k_dw_mfma (fused) or one pass over dy
+  const float* partb = nullptr;
+  int nrc = 0;
   if (db_fused) {
-    k_db_reduce<<<(C_out + 3) / 4, 256, 0, st>>>(partb_fused, nchunk, C_out, db);
+    partb = partb_fused;
+    nrc = static_cast<int>(nchunk);
   } else if (db) {
     const int64_t rows = op == SPCONV_OP_DC ? rb->n_in : rb->n_out;
-    const int nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
-    float* partb = part + static_cast<int64_t>(rb->K) * nchunk * per;
+    nrc = static_cast<int>((rows + kRowChunk - 1) / kRowChunk);
+    float* pb = part + static_cast<int64_t>(rb->K) * nchunk * per;
+    partb = pb;
     if (nrc > 0) {
       const int vec = dt == SPCONV_F32 ? 4 : 8;
       const int groups = (C_out + vec - 1) / vec;
       dim3 g(static_cast<unsigned>(nrc), static_cast<unsigned>((groups + 31) / 32));
       if (dt == SPCONV_F32)
-        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out, partb);
+        k_db_partial<float><<<g, 256, 0, st>>>(static_cast<const float*>(dy), rows, C_out, pb);
       else
         k_db_partial<uint16_t><<<g, 256, 0, st>>>(static_cast<const uint16_t*>(dy), rows, C_out,
-                                                  partb);
+                                                  pb);
     }
-    k_db_reduce<<<(C_out + 3) / 4, 256, 0, st>>>(partb, nrc, C_out, db);
+  }
+  {
+    // one launch sums both: the weight's elements, then the bias columns.
+    // Segments per weight element: enough threads for the device (~128 K),
+    // at least 8 chunks per segment (more segments did not speed up the
+    // headline's 95 MB of partials)
+    const int64_t elems = static_cast<int64_t>(rb->K) * per;
+    int S = 1;
+    while (S < 8 && elems * S < (int64_t{1} << 17) && nchunk / (2 * S) >= 8) S *= 2;
+    const int64_t E = 256 / S;
+    const int64_t nb_dw = (elems + E - 1) / E;
+    const int64_t nb_db = db ? (C_out + 3) / 4 : 0;
+    if (nb_dw + nb_db > 0)
+      k_dw_reduce<<<static_cast<unsigned>(nb_dw + nb_db), 256, 0, st>>>(
+          part, K, C_in, C_out, nchunk, S, dw, nb_dw, partb, nrc, db);
   }
   return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
