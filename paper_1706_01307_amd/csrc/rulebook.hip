@@ -16,10 +16,12 @@
 //                                 occupancy bitmap, its prefix counts, and
 //                                 the rows in cell order = the Z-order
 //                                 schedule the probe, the compaction and the
-//                                 forward walk (grids of at most 2^18 cells:
-//                                 k_grid_emit_self alone, the bitmap set by
-//                                 the scatter, every block counting the
-//                                 words before its own)
+//                                 forward walk (up to 2^25 cells no
+//                                 k_bitscan: every emitting block adds up the
+//                                 block counts before its own; grids of at
+//                                 most 2^18 cells: k_grid_emit_self alone,
+//                                 the bitmap set by the scatter, every block
+//                                 counting the words before its own)
 //   k_probe_grid                  per schedule position and offset, one load
 //                                 of the neighbour's cell -> gather map
 //                                 G[i][p] (1 + input row, 0 if none)
@@ -1509,15 +1511,47 @@ __global__ __launch_bounds__(kBlock) void k_grid_bits(const uint32_t* __restrict
 
 // Rows of the occupied cells in cell order -> perm (the Z-order schedule),
 // one bitmap word per thread; block bases from k_grid_bits + k_bitscan.
+// SELF (at most kSelfBlocks blocks): bbase holds k_grid_bits' block sums as
+// they are; every block adds up those before its own (a few loads per
+// thread), and the last block sets n_out to the occupied cells and flags
+// duplicate sites as k_bitscan would (a count other than `expect` when >= 0,
+// or than *expect_dev when given).
+constexpr int kSelfBlocks = 4096;
+template <bool SELF>
 __global__ __launch_bounds__(kBlock) void k_grid_emit(const uint32_t* __restrict__ bitmap,
                                                       uint64_t nwords, uint64_t cells,
                                                       const uint32_t* __restrict__ bbase,
                                                       const uint32_t* __restrict__ grid,
-                                                      int32_t* __restrict__ perm) {
+                                                      int32_t* __restrict__ perm,
+                                                      DeviceHeader* __restrict__ hdr,
+                                                      int64_t expect,
+                                                      const int64_t* __restrict__ expect_dev) {
   const uint64_t w = blockIdx.x * static_cast<uint64_t>(kBlock) + threadIdx.x;
   const uint32_t word = w < nwords ? bitmap[w] : 0u;
+  uint32_t base;
+  if constexpr (SELF) {
+    constexpr int PER = kSelfBlocks / kBlock;
+    uint32_t v[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {                // every load in flight at once
+      const uint32_t idx = k * kBlock + threadIdx.x;
+      v[k] = idx < blockIdx.x ? bbase[idx] : 0u;
+    }
+    uint32_t before = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) before += v[k];
+    block_excl_scan<uint32_t>(before, &base);
+  } else {
+    base = bbase[blockIdx.x];
+  }
   uint32_t tot;
-  uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + bbase[blockIdx.x];
+  uint32_t rank = block_excl_scan<uint32_t>(__popc(word), &tot) + base;
+  if (SELF && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+    const int64_t t = static_cast<int64_t>(base) + tot;
+    if ((expect >= 0 && t != expect) || (expect_dev && t != *expect_dev))
+      atomicOr(&hdr->status, kStDup);
+    hdr->n_out = t;
+  }
   if (!word) return;
   // the word's 32 cells as eight 16-byte loads issued together (a loop of
   // one load per occupied cell waits out each load's latency in turn); a
@@ -2281,9 +2315,14 @@ void launch_grid_schedule(spconv_rulebook rb, const GridBufs& b, uint64_t cells,
   }
   k_grid_bits<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(b.grid, cells, b.nwords,
                                                                         b.bitmap, b.bsum);
+  if (b.nbw <= kSelfBlocks) {
+    k_grid_emit<true><<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
+        b.bitmap, b.nwords, cells, b.bsum, b.grid, rb->perm, rb->hdr, expect, expect_dev);
+    return;
+  }
   k_bitscan<<<1, kBlock, 0, rb->stream>>>(b.bsum, b.nbw, rb->hdr, expect, expect_dev);
-  k_grid_emit<<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
-      b.bitmap, b.nwords, cells, b.bsum, b.grid, rb->perm);
+  k_grid_emit<false><<<static_cast<unsigned>(b.nbw), kBlock, 0, rb->stream>>>(
+      b.bitmap, b.nwords, cells, b.bsum, b.grid, rb->perm, rb->hdr, expect, expect_dev);
 }
 
 void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const GridGeom& g,
