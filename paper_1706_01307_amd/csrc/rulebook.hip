@@ -1738,18 +1738,20 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid(
 //
 // It runs twice.  WRITE = false counts, per block and offset, the positions
 // with a neighbour (and the per-wave prefixes), which k_scan turns into each
-// block's base inside every R_i.  WRITE = true repeats the same lookups and
-// writes the gather map and, at once, every pair at its final place in R_i
-// (pair_off[i] + the block's base + the waves before it + the set lanes
-// before it), so the pair lists never need a second pass over the gather
-// map.  Workgroup 0 of the writing pass also stores pair_off.
+// block's base inside every R_i; it needs occupancy only, so it reads the
+// same four-cell groups from the occupancy bitmap (4 bits of a word, 1/32 of
+// the grid's bytes) instead of the grid.  WRITE = true repeats the lookups in
+// the grid and writes the gather map and, at once, every pair at its final
+// place in R_i (pair_off[i] + the block's base + the waves before it + the
+// set lanes before it), so the pair lists never need a second pass over the
+// gather map.  Workgroup 0 of the writing pass also stores pair_off.
 template <bool WRITE>
 __global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
     const int32_t* __restrict__ rows_sites, const int32_t* __restrict__ perm,
     const DeviceHeader* __restrict__ hdr, int64_t gstride, GridGeom g,
-    const uint32_t* __restrict__ grid, uint32_t cells, int32_t* __restrict__ gmap,
-    int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre, int64_t nblk,
-    const int64_t* __restrict__ totals, int2* __restrict__ pairs,
+    const uint32_t* __restrict__ grid, uint32_t cells, const uint32_t* __restrict__ bitmap,
+    int32_t* __restrict__ gmap, int32_t* __restrict__ blk_cnt, uint32_t* __restrict__ wpre,
+    int64_t nblk, const int64_t* __restrict__ totals, int2* __restrict__ pairs,
     int64_t* __restrict__ pair_off) {
   __shared__ uint8_t s_cnt[kMaxK][kBlock / kWave];
   __shared__ int64_t s_off[28];
@@ -1796,19 +1798,38 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
   const uint32_t xp[3] = {(z1 + dm[1]) & g.M[1], z1 & g.M[1], (z1 + dp[1]) & g.M[1]};
   const uint32_t yp[2] = {(z2 + dm[2]) & g.M[2], (z2 + dp[2]) & g.M[2]};
   const uint32_t zp[2] = {(z3 + dm[3]) & g.M[3], (z3 + dp[3]) & g.M[3]};
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint32_t*>(grid), 0, static_cast<int>(cells * 4), static_cast<int>(kBufDword3));
-  dw4 v[3][2][2];
+  dw4 v[3][2][2];          // WRITE: the groups' four cells
+  uint32_t nib[3][2][2];   // otherwise: their four occupancy bits
+  if constexpr (WRITE) {
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(grid), 0, static_cast<int>(cells * 4),
+        static_cast<int>(kBufDword3));
 #pragma unroll
-  for (int a = 0; a < 3; ++a)
+    for (int a = 0; a < 3; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int d = 0; d < 2; ++d) {
-        const uint32_t cell = (base | xp[a] | yp[b] | zp[d]) & ~3u;
-        v[a][b][d] = __builtin_bit_cast(
-            dw4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, valid ? cell * 4 : kOOB, 0, 0));
-      }
+        for (int d = 0; d < 2; ++d) {
+          const uint32_t cell = (base | xp[a] | yp[b] | zp[d]) & ~3u;
+          v[a][b][d] = __builtin_bit_cast(
+              dw4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, valid ? cell * 4 : kOOB, 0, 0));
+        }
+  } else {
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(bitmap), 0, static_cast<int>(((cells + 31) / 32) * 4),
+        static_cast<int>(kBufDword3));
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const uint32_t cell = (base | xp[a] | yp[b] | zp[d]) & ~3u;
+          const uint32_t word =
+              __builtin_amdgcn_raw_buffer_load_b32(rsrc, valid ? (cell >> 5) * 4 : kOOB, 0, 0);
+          nib[a][b][d] = (word >> (cell & 31u)) & 15u;
+        }
+  }
   const int yo = c.z & 1, zo = c.w & 1;
   bool xok[3], yok[3], zok[3];
 #pragma unroll
@@ -1827,13 +1848,21 @@ __global__ __launch_bounds__(kBlock) void k_probe_grid_g4(
       // group in y: the lower one holds y - 1 (and y when y is odd)
       const bool bh = dy == 2 || (dy == 1 && !yo);
       const bool dh = dz == 2 || (dz == 1 && !zo);
-      const dw4 w0 = bh ? v[dx][1][0] : v[dx][0][0];
-      const dw4 w1 = bh ? v[dx][1][1] : v[dx][0][1];
-      const dw4 w = dh ? w1 : w0;
       const int ey = dy == 1 ? yo : yo ^ 1;       // bit 0 of y + dy - 1
       const int ez = dz == 1 ? zo : zo ^ 1;
-      const uint32_t lo = ez ? w.y : w.x, hi = ez ? w.w : w.z;
-      const uint32_t val = ey ? hi : lo;
+      uint32_t val;
+      if constexpr (WRITE) {
+        const dw4 w0 = bh ? v[dx][1][0] : v[dx][0][0];
+        const dw4 w1 = bh ? v[dx][1][1] : v[dx][0][1];
+        const dw4 w = dh ? w1 : w0;
+        const uint32_t lo = ez ? w.y : w.x, hi = ez ? w.w : w.z;
+        val = ey ? hi : lo;
+      } else {
+        // cell 2 ey + ez of the group (bit 0: coordinate 3, bit 1: coordinate 2)
+        const uint32_t n0 = bh ? nib[dx][1][0] : nib[dx][0][0];
+        const uint32_t n1 = bh ? nib[dx][1][1] : nib[dx][0][1];
+        val = ((dh ? n1 : n0) >> (2 * ey + ez)) & 1u;
+      }
       e = (xok[dx] && yok[dy] && zok[dz]) ? static_cast<int32_t>(val) : 0;
     }
     const uint64_t m = __ballot(e != 0);
@@ -2341,7 +2370,7 @@ void launch_probe_grid(spconv_rulebook rb, const int32_t* rows_sites, const Grid
     auto probe = [&](auto kern) {
       kern<<<probe_grid_size(rb->nblk), kBlock, 0, rb->stream>>>(
           rows_sites, rb->perm, rb->hdr, rb->gstride, g, b.grid, static_cast<uint32_t>(cells),
-          rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk, rb->totals,
+          b.bitmap, rb->gmap, rb->blk_cnt, rb->wpre, rb->nblk, rb->totals,
           reinterpret_cast<int2*>(rb->pairs), rb->pair_off);
     };
     probe(k_probe_grid_g4<false>);
