@@ -26,9 +26,9 @@
 //                                 of the neighbour's cell -> gather map
 //                                 G[i][p] (1 + input row, 0 if none)
 // Hashed (any grid up to 65535 per side):
-//   VSC: sorted bricks.  k_site_keys + k_morton + radix sort order the sites
-//   by brick (2^b cells per coordinate; the Morton code's bits above the
-//   brick's own); runs of one brick are numbered (k_brick_flags / k_bitscan /
+//   VSC: sorted bricks.  k_site_morton (keys and Morton codes in one pass)
+//   and a radix sort order the sites by brick (2^b cells per coordinate; the
+//   Morton code's bits above the brick's own); runs of one brick are numbered (k_brick_flags / k_bitscan /
 //   k_bricks), each brick inserted once into a hash directory; k_pool_fill
 //   writes the bricks' cells into a Z-ordered pool and puts every run in cell
 //   order, which completes the Z-order schedule; k_brick_nbrs finds the
@@ -680,23 +680,6 @@ __host__ __device__ inline uint64_t deposit64(uint64_t v, uint64_t m) {
     m &= m - 1;
   }
   return r;
-}
-
-// Packed key of input row r (kEmpty: out of range), the coordinates copied.
-__global__ __launch_bounds__(kBlock) void k_site_keys(
-    const int32_t* __restrict__ coords, int64_t N, Codec c, uint64_t* __restrict__ keys,
-    int32_t* __restrict__ copy_out, uint32_t* __restrict__ status) {
-  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
-  if (r >= N) return;
-  int32_t x[kMaxD];
-  bool ok = true;
-  for (int j = 0; j < c.D; ++j) {
-    x[j] = coords[r * c.D + j];
-    ok = ok && x[j] >= 0 && x[j] < c.size[j];
-    if (copy_out) copy_out[r * c.D + j] = x[j];
-  }
-  keys[r] = ok ? pack_site(c, x) : kEmpty;
-  if (!ok) atomicOr(status, kStRange);
 }
 
 // Bits of v at the set positions of m, packed from the lowest.
@@ -1438,6 +1421,40 @@ __global__ __launch_bounds__(kBlock) void k_morton(const uint64_t* __restrict__ 
   mv[y] = static_cast<int32_t>(y);
 }
 
+// The sorted-brick build's first pass over the sites: packed key of row r (kEmpty: out of range, flagged), the
+// coordinates copied, and the Morton code of the key with r beside it.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_site_morton(
+    const int32_t* __restrict__ coords, int64_t N, Codec c, uint64_t* __restrict__ keys,
+    int32_t* __restrict__ copy_out, uint32_t* __restrict__ status, int maxb, int sbits,
+    uint64_t* __restrict__ mk, int32_t* __restrict__ mv) {
+  const int64_t r = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (r >= N) return;
+  int32_t x[D];
+  bool ok = true;
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    x[j] = coords[r * D + j];
+    ok = ok && x[j] >= 0 && x[j] < c.size[j];
+    if (copy_out) copy_out[r * D + j] = x[j];
+  }
+  const uint64_t key = ok ? pack_site(c, x) : kEmpty;
+  keys[r] = key;
+  if (!ok) atomicOr(status, kStRange);
+  uint32_t v[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) v[j] = static_cast<uint32_t>((key >> c.shift[j]) & c.fmask[j]);
+  uint64_t m = 0;
+  for (int L = maxb - 1; L >= 0; --L) {
+#pragma unroll
+    for (int j = 1; j < D; ++j)
+      if (c.fmask[j] >> L) m = (m << 1) | ((v[j] >> L) & 1u);
+  }
+  m |= static_cast<uint64_t>(v[0]) << sbits;
+  mk[r] = m;
+  mv[r] = static_cast<int32_t>(r);
+}
+
 // ---------------------------------------------------------------------------
 // Dense index grid (used when the grid is small enough to hold one int32 per
 // cell; the sites' cells are laid out along the Z-order curve)
@@ -2036,9 +2053,17 @@ size_t schedule_bytes(int64_t n_cap) {
 // Output rows in Morton order -> rb->perm (scratch carved from the transient
 // allocation by `cv`); returns the sorted Morton codes.  With lo_bit > 0 the
 // lowest lo_bit bits of the codes are left out of the sort (the brick map
-// orders each brick's sites itself).
+// orders each brick's sites itself).  With si the site keys (si->keys, which
+// is rowkeys) are packed in the same pass as the Morton codes.
+struct SiteIn {
+  const int32_t* coords;
+  int64_t N;
+  uint64_t* keys;
+  int32_t* copy_out;
+  uint32_t* status;
+};
 const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, const Codec& crow,
-                                Carver* cv, int lo_bit) {
+                                Carver* cv, int lo_bit, const SiteIn* si) {
   const int64_t n = rb->n_cap;
   int maxb = 0, sbits = 0;
   for (int j = 1; j < crow.D; ++j) {
@@ -2056,10 +2081,23 @@ const uint64_t* launch_schedule(spconv_rulebook rb, const uint64_t* rowkeys, con
   int32_t* mv2 = odd ? rb->perm : cv->take<int32_t>(n);
   void* scratch = cv->take<unsigned char>(radix_sort_scratch_bytes(n));
   const unsigned g = grid_for(n);
-  switch (crow.D) {
-    case 2: k_morton<2><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
-    case 3: k_morton<3><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
-    default: k_morton<4><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+  if (si) {
+    const unsigned gs = grid_for(si->N);
+#define SPC_SITE_MORTON(DD)                                                                   \
+  k_site_morton<DD><<<gs, kBlock, 0, rb->stream>>>(si->coords, si->N, crow, si->keys,          \
+                                                   si->copy_out, si->status, maxb, sbits, mk, mv)
+    switch (crow.D) {
+      case 2: SPC_SITE_MORTON(2); break;
+      case 3: SPC_SITE_MORTON(3); break;
+      default: SPC_SITE_MORTON(4); break;
+    }
+#undef SPC_SITE_MORTON
+  } else {
+    switch (crow.D) {
+      case 2: k_morton<2><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+      case 3: k_morton<3><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+      default: k_morton<4><<<g, kBlock, 0, rb->stream>>>(rowkeys, rb->hdr, crow, maxb, sbits, mk, mv); break;
+    }
   }
   const bool in_tmp =
       radix_sort_pairs(mk, mv, mk2, mv2, rb->hdr, n, total, scratch, rb->stream, lo_bit);
@@ -2197,10 +2235,10 @@ int build_vsc_bricks(spconv_rulebook rb, const int32_t* coords, BrickMap m) {
   for (int j = 1; j < rb->D; ++j) nb3 *= 3;
   int32_t* nbr = cv.take<int32_t>(static_cast<size_t>(N) * nb3);
   uint16_t* tab = cv.take<uint16_t>(static_cast<size_t>(kBrickCells) * kBrickK);
-  k_site_keys<<<grid_for(N), kBlock, 0, rb->stream>>>(coords, N, cin, keys, rb->out_coords,
-                                                      &rb->hdr->status);
-  // sorted by brick only; k_pool_fill puts each brick's sites in cell order
-  uint64_t* mk = const_cast<uint64_t*>(launch_schedule(rb, keys, cin, &cv, m.lb));
+  // keys and Morton codes in one pass; sorted by brick only (k_pool_fill
+  // puts each brick's sites in cell order)
+  const SiteIn si{coords, N, keys, rb->out_coords, &rb->hdr->status};
+  uint64_t* mk = const_cast<uint64_t*>(launch_schedule(rb, keys, cin, &cv, m.lb, &si));
   const OffsetTable ot = make_offsets(rb);
   const int64_t ntab = (int64_t{1} << m.lb) * ot.K;
   const int64_t fb = nb > (ntab + kBlock - 1) / kBlock ? nb : (ntab + kBlock - 1) / kBlock;
@@ -2540,7 +2578,7 @@ int build_vsc(spconv_rulebook rb, const int32_t* coords) {
   if (st != SPCONV_OK) return st;
   launch_insert(rb, coords, N, cin, tr, rb->out_coords);
   if (N > 0) {
-    launch_schedule(rb, tr.keys, cin, &cv, 0);
+    launch_schedule(rb, tr.keys, cin, &cv, 0, nullptr);
     launch_probe_scan_compact(rb, tr.keys, cin, cin, tr);
   }
   else
@@ -2589,7 +2627,7 @@ int build_sc(spconv_rulebook rb, const int32_t* coords) {
     k_bitscan<<<1, kBlock, 0, rb->stream>>>(bsum, nbw, rb->hdr, -1, nullptr);
     k_sc_emit<<<static_cast<unsigned>(nbw * kEmitParts), kBlock, 0, rb->stream>>>(
         bitmap, nwords, bsum, cout, E, rb->out_coords, out_keys, OutGrid{}, rb->hdr);
-    launch_schedule(rb, out_keys, cout, &cv, 0);
+    launch_schedule(rb, out_keys, cout, &cv, 0, nullptr);
     launch_probe_scan_compact(rb, out_keys, cout, cin, tr);
   } else {
     k_fill_u64<<<1, 64, 0, rb->stream>>>(reinterpret_cast<uint64_t*>(rb->pair_off), 0,
