@@ -815,9 +815,15 @@ __global__ __launch_bounds__(kBlock) void k_pool_fill(
   const uint64_t lowmask = static_cast<uint64_t>(cells - 1);
   const int64_t nw = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
   bool dup = false;
-  for (int64_t bi = blockIdx.x * static_cast<int64_t>(kBlock / kWave) + wave; bi < nbr; bi += nw) {
-    const int64_t first = starts[bi];
-    const int64_t last = bi + 1 < nbr ? starts[bi + 1] : n;
+  // the next brick's run bounds are requested while this brick is filled
+  int64_t bi = blockIdx.x * static_cast<int64_t>(kBlock / kWave) + wave;
+  int64_t nfirst = bi < nbr ? starts[bi] : 0;
+  int64_t nlast = bi + 1 < nbr ? starts[bi + 1] : n;
+  for (; bi < nbr; bi += nw) {
+    const int64_t first = nfirst, last = nlast;
+    const int64_t bn = bi + nw;
+    nfirst = bn < nbr ? starts[bn] : 0;
+    nlast = bn + 1 < nbr ? starts[bn + 1] : n;
     const uint64_t brick = mk[first] >> m.lb;      // a run starts on a site in range
     s_img[wave][lane] = 0;
     for (int64_t q0 = first; q0 < last; q0 += kWave) {
