@@ -851,9 +851,8 @@ __global__ __launch_bounds__(kBlock) void k_pool_fill(
 // NB-1-t, so each lookup fills both entries (the lower halves start at -1,
 // cleared with the directory).  Pairs are dealt out in steps of the grid.
 __global__ __launch_bounds__(kBlock) void k_brick_nbrs(
-    const uint64_t* __restrict__ mk, const int32_t* __restrict__ perm,
-    const uint64_t* __restrict__ rowkeys, const int64_t* __restrict__ starts, Codec crow,
-    BrickMap m, int nb3, int32_t* __restrict__ nbr) {
+    const uint64_t* __restrict__ mk, const int64_t* __restrict__ starts, Codec crow, BrickMap m,
+    int nb3, int32_t* __restrict__ nbr) {
   const int half = nb3 / 2;
   const int per = nb3 - half;                 // offsets half .. nb3-1
   const int64_t total = m.nbricks->n_out * per;
@@ -868,16 +867,22 @@ __global__ __launch_bounds__(kBlock) void k_brick_nbrs(
       continue;
     }
     const int64_t p = starts[bi];
-    const uint64_t rk = rowkeys[perm[p]];
-    uint64_t k = mk[p] >> m.lb;
+    // the brick's coordinates are the brick-number bits of its key (no trip
+    // through the row's packed key)
+    const uint64_t k0 = mk[p] >> m.lb;
+    uint64_t k = k0;
     bool ok = true;
     int t = t0;
     for (int j = 1; j < m.D; ++j) {
       const int dj = t % 3 - 1;
       t /= 3;
       if (dj == 0) continue;
-      const int32_t c = static_cast<int32_t>((rk >> crow.shift[j]) & crow.fmask[j]);
-      const int32_t bc = c / m.side[j] + dj, bmax = (crow.size[j] - 1) / m.side[j];
+      uint64_t bj = 0, bm = m.BM[j];              // bits of k0 at BM[j], packed from the lowest
+      for (uint64_t bb = 1; bm; bb <<= 1) {
+        if (k0 & bm & (0ull - bm)) bj |= bb;
+        bm &= bm - 1;
+      }
+      const int32_t bc = static_cast<int32_t>(bj) + dj, bmax = (crow.size[j] - 1) / m.side[j];
       ok = ok && m.BM[j] != 0 && bc >= 0 && bc <= bmax;
       k = zmove64(k, m.BM[j], m.BM[j] & (0ull - m.BM[j]), dj < 0);
     }
@@ -2258,7 +2263,7 @@ int build_vsc_bricks(spconv_rulebook rb, const int32_t* coords, BrickMap m) {
                                                                  starts);
   k_pool_fill<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, validbits, N, starts, m,
                                               &rb->hdr->status);
-  k_brick_nbrs<<<gb, kBlock, 0, rb->stream>>>(mk, rb->perm, keys, starts, cin, m, nb3, nbr);
+  k_brick_nbrs<<<gb, kBlock, 0, rb->stream>>>(mk, starts, cin, m, nb3, nbr);
   const unsigned g = probe_grid_size(rb->nblk);
   auto launch = [&](auto kern) {
     kern<<<g, kBlock, 0, rb->stream>>>(mk, rb->perm, brickidx, keys, rb->hdr, rb->gstride, cin,
