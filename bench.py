@@ -104,6 +104,20 @@ def cpu_model():
     return None
 
 
+def forward_kernel(c_in, c_out, bf16, n):
+    """The forward kernel the library picks for these channel counts (the
+    library's own dispatch rule): the matrix cores for bf16 C_in of 32 / 64 /
+    96 / 128 or fp32 C_in of 16 ... 128 with C_out a multiple of 16, else the
+    one-plane-group kernel for at most 4 input planes on at least 2048 rows
+    (C_out a multiple of 16), else one lane per output element."""
+    mfma_cin = (32, 64, 96, 128) if bf16 else (16, 32, 64, 96, 128)
+    if c_out % 16 == 0 and c_in in mfma_cin:
+        return "k_fwd_mfma"
+    if c_in <= 4 and n >= 2048 and c_out % 16 == 0:
+        return "k_fwd_lowc"
+    return "k_fwd_vec"
+
+
 def cpu_baseline(wl, x_bits, w_bits, bias, n_samples):
     """The oracle (std::map rule book + double-precision forward, both
     parallel over output rows on OpenMP threads) timed on this host: the whole
@@ -276,7 +290,7 @@ def main():
     tflops = flops / (fwd_ms * 1e-3) / 1e12
     dt = "bf16" if bf16 else "f32"
     peak = PEAKS[dt]
-    kernel = "k_fwd_mfma"
+    kernel = forward_kernel(Cin, Cout, bf16, N)
     traffic = load_traffic(kernel, a.workload)
     # forward algorithmic bytes: features in/out, gather map, weights, bias
     esz = 2 if bf16 else 4
@@ -326,9 +340,14 @@ def main():
                                    "rulebook": float(np.median(cold_rb)),
                                    "forward": float(np.median(cold_fwd))}
                                   if a.cold_steps > 0 else None),
-        "roofline": {"bound": "mfma", "kernel": kernel, "achieved": tflops, "peak": peak,
-                     "unit": "TFLOP/s", "frac": tflops / peak, "traffic": traffic,
-                     "algorithmic_bytes": fwd_bytes},
+        "roofline": ({"bound": "mfma", "kernel": kernel, "achieved": tflops, "peak": peak,
+                      "unit": "TFLOP/s", "frac": tflops / peak, "traffic": traffic,
+                      "algorithmic_bytes": fwd_bytes}
+                     if kernel == "k_fwd_mfma" else
+                     {"bound": "hbm", "kernel": kernel,
+                      "achieved": fwd_bytes / (fwd_ms * 1e-3) / 1e9, "peak": PEAKS["hbm"],
+                      "unit": "GB/s", "frac": fwd_bytes / (fwd_ms * 1e-3) / 1e9 / PEAKS["hbm"],
+                      "traffic": traffic, "algorithmic_bytes": fwd_bytes}),
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_bits, w_bits, bias, a.cpu_samples)
@@ -617,6 +636,26 @@ def run_ops(a, torch, dev, spc, inputs):
          "TFLOP/s", PEAKS["bf16"],
          {"active_sites": N, "sum_k": sum_k, "plain_forward_ms": ms_plain,
           "forward_then_torch_epilogue_ms": ms_sep})
+    rb.close()
+
+    # ---- the low-channel path: one input plane (pen strokes), VSC 3x3,
+    # 1 -> 32 fp32 on 1,024 grids of 64^2 (the one-plane kernel k_fwd_lowc;
+    # HBM-bound: features, gather map and output each move once)
+    coords = inputs.pen_strokes(1024, 64, seed=31, target=400)
+    n = len(coords)
+    ct = torch.from_numpy(coords).to(dev)
+    rb = spc.build_rulebook(spc.VSC, ct, [1024, 64, 64], [1, 3, 3])
+    K, sum_k = rb.K, int(rb.pair_off[-1])
+    ci, co = 1, 32
+    x1 = torch.from_numpy(inputs.normal_f32((n, ci), seed=32)).to(dev)
+    w1 = torch.from_numpy(inputs.normal_f32((K, ci, co), std=1.0 / 3, seed=33)).to(dev)
+    b1 = torch.from_numpy(inputs.normal_f32((co,), std=0.1, seed=34)).to(dev)
+    y1 = torch.empty((n, co), dtype=torch.float32, device=dev)
+    ms = timed(lambda: spc.vsc_forward(rb, x1, w1, b1, out=y1))
+    nbytes = n * ci * 4 + n * co * 4 + 4 * K * n + K * ci * co * 4 + 4 * co
+    emit("vsc_lowc_3x3_c1_c32_f32", "pen 1024 x 64^2", ms, "hbm", nbytes / (ms * 1e-3) / 1e9,
+         "GB/s", PEAKS["hbm"], {"dtype": "f32", "kernel": "k_fwd_lowc", "active_sites": n,
+                                "sum_k": sum_k, "algorithmic_bytes": nbytes})
     rb.close()
 
 
