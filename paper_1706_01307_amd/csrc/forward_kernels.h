@@ -248,10 +248,11 @@ template <int NCB> struct OutLoad<uint16_t, NCB> {
 
 // Few input planes (C_in <= kLowCin, C_out a multiple of kLowCols): one
 // thread per output position and kLowCols output columns, a block of threads
-// on one column group.  The gather-map entries and input values of
-// 16 offsets at a time are loaded together into registers; meanwhile the
-// block stages those offsets' weights of its columns in LDS, which every lane
-// then reads at the same address (a broadcast).  The finished rows go
+// on one column group.  The gather-map entries and input values of KB
+// offsets at a time (9, or 16 for larger filters) are loaded together into
+// registers; meanwhile the block stages those offsets' weights of its
+// columns in LDS, which every lane then reads at the same address (a
+// broadcast).  The finished rows go
 // through LDS once more, so that each store instruction writes whole 16-byte
 // pieces of few rows (4 lanes per row) instead of one element of 64 rows
 // (on 476,000 pen-stroke rows, 1 -> 32 fp32: 40 us against 87 us; 32
@@ -259,13 +260,12 @@ template <int NCB> struct OutLoad<uint16_t, NCB> {
 // order as k_fwd_vec.
 constexpr int kLowCin = 4;
 constexpr int kLowCols = 16;
-template <typename TIn, typename TOut, int WT>
+template <typename TIn, typename TOut, int WT, int KB>
 __global__ __launch_bounds__(256) void k_fwd_lowc(
     const int32_t* __restrict__ gmap, const int32_t* __restrict__ perm, int64_t gstride,
     int64_t n_cap, const DeviceHeader* __restrict__ hdr, int K, const TIn* __restrict__ x,
     const TIn* __restrict__ w, const float* __restrict__ bias, TOut* __restrict__ y, int C_in,
     int C_out, uint32_t x_bytes, Epilogue epi) {
-  constexpr int KB = 16;
   constexpr int NCOL = kLowCols;
   constexpr int kW = KB * kLowCin * NCOL;         // staged weights (floats)
   constexpr int kO = 4 * 64 * (NCOL + 1);         // finished rows, per wave 64 x NCOL (+1 pad)
@@ -865,7 +865,10 @@ template <typename TIn, typename TOut, int WT>
 void launch_lowc(const Call& c, int C_in, uint32_t x_bytes) {
   const dim3 grid(static_cast<unsigned>((c.v.n_cap + 255) / 256),
                   static_cast<unsigned>(c.C_out / kLowCols));
-  k_fwd_lowc<TIn, TOut, WT><<<grid, 256, 0, c.stream>>>(
+  // offsets in batches of KB: 9 covers a 3x3 filter in one batch (no map
+  // loads for offsets past K), 16 anything larger
+  auto kern = c.v.K <= 9 ? k_fwd_lowc<TIn, TOut, WT, 9> : k_fwd_lowc<TIn, TOut, WT, 16>;
+  kern<<<grid, 256, 0, c.stream>>>(
       c.v.gmap, c.v.perm, c.v.gstride, c.v.n_cap, c.v.hdr, static_cast<int>(c.v.K),
       static_cast<const TIn*>(c.x), static_cast<const TIn*>(c.w), c.bias, static_cast<TOut*>(c.y),
       C_in, c.C_out, x_bytes, c.epi);
