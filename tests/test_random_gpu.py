@@ -163,3 +163,49 @@ def test_random_few_input_planes(seed):
     assert len(c) >= 2048
     compare_layer(kind, c, size, f, s, ci, co, dtype=dtype, out_dtype=out_dtype, seed=seed,
                   what=f"few planes {seed}")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_few_input_planes_fused_epilogue(seed):
+    """The block epilogue (scale, shift, residual, ReLU, each on or off) on
+    layers of 1-4 input planes and at least 2048 sites, where the
+    low-channel kernel stores its rows through LDS, against the oracle."""
+    import oracle
+    from paper_1706_01307_amd import inputs
+    from tests.test_ops_gpu import _dev, _feats, _odt
+    from tests.test_parity_gpu import RTOL_BF16, RTOL_F32, _t, _to_np, check_features
+    rng = np.random.default_rng(7500 + seed)
+    D = int(rng.integers(3, 5))
+    size = [int(rng.integers(1, 3))] + [int(rng.choice([72, 80] if D == 3 else [24, 31]))
+                                       for _ in range(D - 1)]
+    c = dense_ref.random_sites(rng, size, 0.5 if D == 3 else 0.2)
+    assert len(c) >= 2048
+    f, s_ = [1] + [3] * (D - 1), [1] * D
+    ci, co = int(rng.integers(1, 5)), int(rng.choice([16, 32, 48]))
+    dtype = "bf16" if seed % 2 else "f32"
+    out_dtype = "f32" if seed % 4 < 2 else "bf16"
+    use_s, use_b, use_r, relu = (bool(v) for v in rng.integers(0, 2, size=4))
+    if seed == 0:
+        use_s = use_b = use_r = relu = True
+    rb = spc.build_rulebook(spc.VSC, _t(c), size, f, s_)
+    ref = oracle.Rulebook(oracle.VSC, c, size, f, s_)
+    K = ref.K
+    x = _feats(len(c), ci, dtype, 13 * seed + 1)
+    wf = inputs.normal_f32((K, ci, co), std=1.0 / np.sqrt(K * ci), seed=13 * seed + 2)
+    w = inputs.to_bf16_bits(wf) if dtype == "bf16" else wf
+    scale = inputs.normal_f32((co,), std=1.0, seed=13 * seed + 3)
+    shift = inputs.normal_f32((co,), std=0.5, seed=13 * seed + 4)
+    res = _feats(ref.n_out, co, out_dtype, 13 * seed + 5)
+    _say(f"[few planes fused {seed}] N={len(c)} C={ci}->{co} {dtype}->{out_dtype} "
+         f"parts={use_s, use_b, use_r, relu}")
+    odt = torch.bfloat16 if out_dtype == "bf16" else torch.float32
+    y = spc.forward_fused(rb, _dev(x, dtype), _dev(w, dtype),
+                          scale=_t(scale) if use_s else None, shift=_t(shift) if use_b else None,
+                          residual=_dev(res, out_dtype) if use_r else None, relu=relu,
+                          out_dtype=odt)
+    y64, absb = ref.forward(x, w, None, in_dt=_odt(dtype))
+    zo, bound = oracle.fused_epilogue(y64, absb, scale if use_s else None,
+                                      shift if use_b else None, res if use_r else None,
+                                      relu, _odt(out_dtype))
+    rtol = RTOL_F32 if dtype == "f32" and out_dtype == "f32" else RTOL_BF16
+    check_features(_to_np(y), zo, bound, rtol, "few planes fused")
