@@ -1,6 +1,7 @@
 // Stable LSD radix sort of (uint64 key, int32 value) pairs on gfx950, and the
 // device-wide exclusive scan it uses.  8-bit digits, or 9-bit ones where that
-// saves a pass (a key of 17 or 18 bits); one pass is
+// saves a pass (17-18, 25-27 or 33-36 bits to sort, e.g. the 18 brick bits of
+// the headline's Morton codes); one pass is
 //   k_rs_hist     per-block digit histogram (LDS atomics)   -> hist[digit][block]
 //   scan          exclusive scan of hist in digit-major order (global offsets)
 //   k_rs_scatter  per-block stable ranking (wave ballots for equal digits,
