@@ -1013,22 +1013,26 @@ __global__ __launch_bounds__(kBlock) void k_probe_brick(
 // total into totals[i].
 __global__ __launch_bounds__(kBlock) void k_scan(int32_t* __restrict__ blk_cnt, int64_t nblk,
                                                  int64_t* __restrict__ totals) {
+  // 16 counts per thread, all requested at once: one round of load latency
+  // per 4,096 blocks (the headline's 3,526 blocks in one)
+  constexpr int PER = 16;
   int32_t* c = blk_cnt + blockIdx.x * nblk;
   int64_t carry = 0;
-  for (int64_t base = 0; base < nblk; base += 4 * kBlock) {
-    int32_t v[4];
+  for (int64_t base = 0; base < nblk; base += PER * kBlock) {
+    int32_t v[PER];
     int64_t sum = 0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t k = base + 4 * threadIdx.x + u;
+    for (int u = 0; u < PER; ++u) {
+      const int64_t k = base + PER * threadIdx.x + u;
       v[u] = k < nblk ? c[k] : 0;
-      sum += v[u];
     }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) sum += v[u];
     int64_t tot;
     int64_t ex = block_excl_scan<int64_t>(sum, &tot) + carry;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t k = base + 4 * threadIdx.x + u;
+    for (int u = 0; u < PER; ++u) {
+      const int64_t k = base + PER * threadIdx.x + u;
       if (k < nblk) c[k] = static_cast<int32_t>(ex);
       ex += v[u];
     }
