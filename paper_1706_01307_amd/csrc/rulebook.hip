@@ -1291,21 +1291,23 @@ __global__ __launch_bounds__(kBlock) void k_bitscan(uint32_t* __restrict__ bsum,
                                                     DeviceHeader* __restrict__ hdr,
                                                     int64_t expect,
                                                     const int64_t* __restrict__ expect_dev) {
+  constexpr int PER = 16;                          // all requested at once
   int64_t carry = 0;
-  for (int64_t base = 0; base < nb; base += 4 * kBlock) {
-    uint32_t v[4];
+  for (int64_t base = 0; base < nb; base += PER * kBlock) {
+    uint32_t v[PER];
     int64_t sum = 0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t k = base + 4 * threadIdx.x + u;
+    for (int u = 0; u < PER; ++u) {
+      const int64_t k = base + PER * threadIdx.x + u;
       v[u] = k < nb ? bsum[k] : 0;
-      sum += v[u];
     }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) sum += v[u];
     int64_t tot;
     int64_t ex = block_excl_scan<int64_t>(sum, &tot) + carry;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t k = base + 4 * threadIdx.x + u;
+    for (int u = 0; u < PER; ++u) {
+      const int64_t k = base + PER * threadIdx.x + u;
       if (k < nb) bsum[k] = static_cast<uint32_t>(ex);
       ex += v[u];
     }
